@@ -1,0 +1,213 @@
+#!/usr/bin/env python
+"""Benchmark of the CompressKV prefill-time eviction path on one MI355X.
+
+A step compresses every layer of the workload once (score -> select ->
+gather per layer, all on one stream) with inputs already resident in HBM.
+The reported value is prompt tokens compressed per second per layer:
+sum_b L_b * n_layers / step_time.
+
+Default workload: 32 layers of the Llama-3-8B shape (32 query / 8 KV heads,
+head_dim 128, bf16) at a 32768-token prompt, window 32, max pooling 7,
+per-layer budgets from a Dirichlet split of 32 x 256 tokens per group (>= 64)
+and 1-3 SRHs per group and layer.
+
+Rank 0 prints one JSON line (see the contract in the repository's design notes),
+including a roofline object for the dominant kernel phase (HIP events on the
+launch stream) and the fp64 CPU oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "prompt tokens compressed/sec per layer (1 GPU); % HBM roofline; MFMA util"
+HBM_PEAK_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(lens, Hkv, D, es, W, n_srh_total, budget):
+    """Bytes the method must move for one layer: all of K once, the SRH window
+    queries, the kept K/V rows read and written, and the int32 indices."""
+    k_bytes = sum(lens) * Hkv * D * es
+    q_bytes = len(lens) * W * n_srh_total * D * es
+    kept = sum(min(budget, L) for L in lens)
+    gather = 4 * kept * Hkv * D * es + 4 * kept * Hkv
+    return k_bytes + q_bytes, gather
+
+
+def cpu_baseline(layer, w, seconds):
+    """The fp64 oracle on (sequence, group) units of one layer until about
+    `seconds` of CPU time, scaled to tokens per second per layer."""
+    import numpy as np
+    import torch
+    import oracle as O
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()
+                       if i.get("user_api") == "blas"] or [1])
+    except Exception:
+        threads = 1
+    cu = layer["cu_seqlens_host"]
+    G = w.n_q_heads // w.n_kv_heads
+    units = [(b, g) for b in range(w.batch) for g in range(w.n_kv_heads)]
+    total_tokens = sum(int(cu[b + 1] - cu[b]) for b, _ in units)
+    done_tokens = 0
+    t_total = 0.0
+    n = 0
+    for b, g in units:
+        s0, s1 = int(cu[b]), int(cu[b + 1])
+        q = layer["q_win"][b:b + 1, :, g * G:(g + 1) * G, :].float().cpu().numpy()
+        k = layer["k"][s0:s1, g:g + 1, :].float().cpu().numpy()
+        v = layer["v"][s0:s1, g:g + 1, :].float().cpu().numpy()
+        mask = layer["srh_mask"][g * G:(g + 1) * G]
+        t0 = time.perf_counter()
+        O.compress_layer(q, k, v, np.array([0, s1 - s0]), mask, layer["budget"],
+                         w.pool_kernel, w.pool_type)
+        t_total += time.perf_counter() - t0
+        done_tokens += s1 - s0
+        n += 1
+        if t_total >= seconds:
+            break
+    t_layer = t_total * total_tokens / done_tokens
+    tokens_layer = sum(int(cu[b + 1] - cu[b]) for b in range(w.batch))
+    del torch
+    return {"value": tokens_layer / t_layer, "unit": "tokens/s/layer", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"layer 0, {n} of {len(units)} (sequence, KV group) units "
+                      f"({done_tokens} of {total_tokens} group-tokens), {t_total:.1f} s, "
+                      f"scaled to a whole layer"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="llama32",
+                    help="tiny | llama1 | llama32 | qwen128k | ragged8")
+    ap.add_argument("--layers", type=int, default=0, help="limit the layer count (0: all)")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: this path has no multi-GPU mode "
+              f"(asked for --gpus {args.gpus}); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2606_24467_amd import build as B
+    from paper_2606_24467_amd import compresskv as C
+    from paper_2606_24467_amd import workloads as wl
+
+    if not os.path.exists(B.lib_path()):
+        B.build()
+    dev = torch.device("cuda:0")
+    w = wl.get(args.workload)
+    n_layers = args.layers or w.n_layers
+    G = w.n_q_heads // w.n_kv_heads
+    es = 2 if w.dtype == wl.BF16 else 4
+    log(f"bench: workload {w.name}, {n_layers} layers, generating inputs on the GPU")
+    layers = []
+    for l in range(n_layers):
+        layers.append(wl.make_layer_device(w, l, args.seed, dev))
+    torch.cuda.synchronize()
+    lens = [int(x) for x in np.diff(layers[0]["cu_seqlens_host"])]
+    log(f"bench: inputs ready, lengths {lens[:8]}, budgets "
+        f"{[lay['budget'] for lay in layers][:8]}...")
+
+    # Per-layer problems, outputs and one shared workspace.
+    probs, outs = [], []
+    ws_need = 0
+    score_bytes_total = 0
+    alg_bytes_total = 0
+    for lay in layers:
+        p = C.Problem(lay["q_win"], lay["k"], lay["v"], lay["cu_seqlens"],
+                      cu_seqlens_host=lay["cu_seqlens_host"], pool_kernel=w.pool_kernel,
+                      pool_type=w.pool_type)
+        probs.append(p)
+        ws_need = max(ws_need, C.compresskv_workspace_bytes(p, lay["srh_mask"], lay["budget"]))
+        B_l = lay["budget"]
+        shape = (w.batch, w.n_kv_heads, B_l, w.head_dim)
+        outs.append((torch.empty((w.batch, w.n_kv_heads, B_l), dtype=torch.int32, device=dev),
+                     torch.empty(shape, dtype=lay["k"].dtype, device=dev),
+                     torch.empty(shape, dtype=lay["v"].dtype, device=dev)))
+        n_srh = int(lay["srh_mask"].sum())
+        sb, gb = algorithmic_bytes(lens, w.n_kv_heads, w.head_dim, es, w.window, n_srh, B_l)
+        score_bytes_total += sb
+        alg_bytes_total += sb + gb
+    ws = torch.empty(ws_need, dtype=torch.uint8, device=dev)
+    scores = torch.empty((w.n_kv_heads, probs[0].total_tokens), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step(events=None):
+        for li, (lay, p, (idx, k_out, v_out)) in enumerate(zip(layers, probs, outs)):
+            if events is not None:
+                events[li][0].record(stream)
+            C.compresskv_score(p, lay["q_win"], lay["k"], lay["srh_mask"], scores, ws, stream)
+            if events is not None:
+                events[li][1].record(stream)
+            C.compresskv_select(p, scores, lay["budget"], idx, None, stream)
+            C.compresskv_gather(p, lay["k"], lay["v"], idx, lay["budget"], k_out, v_out, stream)
+
+    for i in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"bench: {args.warmup} warmup steps done")
+    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in layers]
+          for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        step(ev[s])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    log(f"bench: {args.steps} timed steps in {elapsed * 1e3:.2f} ms")
+    score_ms = [e[0].elapsed_time(e[1]) for per_step in ev for e in per_step]
+    score_ms_avg = float(np.mean(score_ms))
+    score_bytes_avg = score_bytes_total / n_layers
+    ms_per_step = elapsed * 1e3 / args.steps
+    tokens = sum(lens)
+    value = tokens * n_layers / (ms_per_step / 1e3)
+    achieved = score_bytes_avg / (score_ms_avg / 1e3) / 1e9
+    e2e_gbs = alg_bytes_total / (ms_per_step / 1e3) / 1e9
+
+    result = {
+        "metric": METRIC, "value": value, "unit": "tokens/s/layer", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == wl.BF16 else "f32", "data": "synthetic",
+        "config": {"workload": f"{w.name}: {n_layers} layers, batch {w.batch}, "
+                               f"{w.n_q_heads}q/{w.n_kv_heads}kv heads, D={w.head_dim}, "
+                               f"L={'ragged ' + str(w.ragged) if w.ragged else w.seq_len}, "
+                               f"W={w.window}, maxpool {w.pool_kernel}",
+                   "layers": n_layers, "batch": w.batch, "seq_lens": lens[:16],
+                   "budgets": [lay["budget"] for lay in layers]},
+        "roofline": {"bound": "hbm", "kernel": "score phase (compresskv_score: statistics + "
+                     "column-sum kernels)", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "avg_ms": score_ms_avg, "bytes_per_launch": score_bytes_avg},
+        "end_to_end": {"algorithmic_bytes_per_step": alg_bytes_total, "achieved_gbs": e2e_gbs,
+                       "frac": e2e_gbs / HBM_PEAK_GBS},
+    }
+    if not args.no_cpu_baseline:
+        log("bench: timing the fp64 oracle on a bounded sample")
+        result["cpu_baseline"] = cpu_baseline(layers[0], w, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,144 @@
+/*
+ * compresskv.h -- C ABI of the MI355X (gfx950) CompressKV prefill-time KV-cache
+ * eviction library (libcompresskv.so).
+ *
+ * The operation (CompressKV, section 3.3, with the SnapKV observation-window
+ * setting of section 4): for every sequence b and KV group g of one layer,
+ *   S1  logits of the last W queries of each Semantic Retrieval Head (SRH) of
+ *       the group against every key of the sequence, causal inside the window;
+ *   S2  softmax of every window row over its whole visible length;
+ *   S3  sum of each SRH's attention over the W window rows, prefix keys only;
+ *   S4  1-D pooling of that vector along the token axis, then the mean over
+ *       the group's SRHs;
+ *   S5  the (budget - W) best prefix tokens (ties: lowest position) plus the W
+ *       window tokens, in ascending position order;
+ *   S6  the retained K/V rows copied into a compact cache.
+ * Budgets per layer come from an offline allocation (section 3.4) and the SRH
+ * sets from an offline calibration (section 3.2, equation 1); both are inputs.
+ *
+ * Conventions shared by every entry point:
+ *   - Pointers are DEVICE pointers unless the name ends in _host.  The caller
+ *     owns every buffer; the library never allocates, frees or synchronizes.
+ *   - All work is enqueued on `stream` (a hipStream_t; NULL = default stream).
+ *     CKV_OK means "enqueued"; kernel faults surface at the caller's next sync.
+ *     Buffers must stay alive until the stream has passed them.
+ *   - Every argument is validated on the host before any HIP call; a failed
+ *     check returns a nonzero status and enqueues nothing.  No exception
+ *     crosses the ABI and nothing aborts.  compresskv_last_error() gives a
+ *     thread-local description of the last failure.
+ *   - Results are deterministic: the same inputs give the same bits.
+ *   - Tensor layouts (elements, D = head_dim contiguous):
+ *       q_win  [batch, W, n_q_heads, D]            dense
+ *       k, v   [T, n_kv_heads, D] packed over the sequences of cu_seqlens,
+ *              element (t, g, d) at t*stride_tok + g*stride_head + d
+ *       scores [n_kv_heads, T] fp32                dense
+ *       idx    [batch, n_kv_heads, budget] int32   dense
+ *       k_out, v_out [batch, n_kv_heads, budget, D] dense, dtype of k / v
+ *   - Query head h belongs to KV group h / (n_q_heads / n_kv_heads).
+ */
+#ifndef COMPRESSKV_H
+#define COMPRESSKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* status codes */
+#define CKV_OK 0
+#define CKV_INVALID_ARGUMENT 1    /* null pointer, inconsistent sizes, budget < W, ... */
+#define CKV_UNSUPPORTED 2         /* head_dim, dtype, alignment or size outside what the kernels take */
+#define CKV_WORKSPACE_TOO_SMALL 3 /* ws_bytes < compresskv_workspace_bytes(...) */
+#define CKV_HIP_ERROR 4           /* a kernel launch was rejected by the HIP runtime */
+
+/* element types of q_win, k and v (all three share one) */
+#define CKV_F32 0
+#define CKV_BF16 1
+
+/* pooling of the window sums along the token axis */
+#define CKV_POOL_MAX 0 /* maximum over the in-range part of the window */
+#define CKV_POOL_AVG 1 /* zero padding, divided by the kernel size */
+
+/* order of pooling and SRH averaging */
+#define CKV_POOL_THEN_MEAN 0 /* pool each SRH, then average (section 3.3) */
+#define CKV_MEAN_THEN_POOL 1 /* average the SRH window sums, then pool once */
+
+/* Sizes and options of one layer.  head_dim must be 64 or 128. */
+typedef struct ckv_problem {
+  int32_t batch;        /* number of packed sequences, >= 1 */
+  int32_t n_q_heads;    /* query heads Hq, a multiple of n_kv_heads, <= 256 */
+  int32_t n_kv_heads;   /* KV groups Hkv, <= 128 */
+  int32_t head_dim;     /* D: 64 or 128 */
+  int32_t window;       /* W: observation-window length, >= 1 */
+  int32_t dtype;        /* CKV_F32 or CKV_BF16 */
+  int32_t pool_type;    /* CKV_POOL_MAX or CKV_POOL_AVG */
+  int32_t pool_kernel;  /* odd, 1 .. 31 */
+  int32_t reduce_order; /* CKV_POOL_THEN_MEAN or CKV_MEAN_THEN_POOL */
+  float scale;          /* softmax scale; <= 0 selects 1/sqrt(head_dim) */
+  const int32_t *cu_seqlens;      /* device [batch+1], cu[0] = 0, non-decreasing */
+  const int32_t *cu_seqlens_host; /* host copy of the same offsets */
+  int64_t k_stride_tok, k_stride_head; /* elements; >= D, 16-byte aligned rows */
+  int64_t v_stride_tok, v_stride_head;
+} ckv_problem;
+
+/*
+ * Bytes of device workspace that compresskv_score / _select / _compress_layer
+ * need for this problem, SRH mask (uint8 [n_q_heads], host) and budget.
+ * Returns 0 if the arguments are invalid (see compresskv_last_error()).
+ */
+size_t compresskv_workspace_bytes(const ckv_problem *p, const uint8_t *srh_mask_host,
+                                  int32_t budget);
+
+/*
+ * S1-S4: pooled, SRH-averaged score of every prefix token, per KV group.
+ *   scores[g, t] for t in sequence b: the score of position t - cu[b] if that
+ *   position is a prefix position (< L_b - W), +inf on the W window positions.
+ * srh_mask_host: uint8 [n_q_heads]; every KV group needs at least one SRH and
+ *   at most 12 row tiles (ceil(W/16) * n_srh <= 12).
+ * Every sequence needs L_b >= W.  ws: >= compresskv_workspace_bytes(), any
+ * contents, 256-byte aligned.
+ */
+int compresskv_score(const ckv_problem *p, const void *q_win, const void *k,
+                     const uint8_t *srh_mask_host, float *scores, void *ws, size_t ws_bytes,
+                     void *stream);
+
+/*
+ * S5: retained positions per (sequence, KV group), ascending, from scores laid
+ * out as compresskv_score writes them.  If L_b <= budget all L_b positions
+ * are kept; otherwise the (budget - W) highest prefix scores (ties: lowest
+ * position) and the W window positions.  Entries past the kept count are -1.
+ * Requires budget >= W.  Scores must be non-negative or +inf (NaN: undefined).
+ */
+int compresskv_select(const ckv_problem *p, const float *scores, int32_t budget, int32_t *idx,
+                      void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * S6: k_out[b, g, r, :] = k[cu[b] + idx[b, g, r], g, :] (same for v), bit for
+ * bit; rows whose idx is -1 are written as zeros.  idx entries must be -1 or
+ * in [0, L_b).
+ */
+int compresskv_gather(const ckv_problem *p, const void *k, const void *v, const int32_t *idx,
+                      int32_t budget, void *k_out, void *v_out, void *stream);
+
+/*
+ * S1-S6 for one layer: score, select and gather in one call.  scores_or_null
+ * receives the scores when not NULL (otherwise they live in ws).
+ */
+int compresskv_compress_layer(const ckv_problem *p, const void *q_win, const void *k,
+                              const void *v, const uint8_t *srh_mask_host, int32_t budget,
+                              int32_t *idx, void *k_out, void *v_out, float *scores_or_null,
+                              void *ws, size_t ws_bytes, void *stream);
+
+/* Static text of a status code. */
+const char *compresskv_status_string(int status);
+
+/* Thread-local description of the last failure of this thread ("" if none). */
+const char *compresskv_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* COMPRESSKV_H */

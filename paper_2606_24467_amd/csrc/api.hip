@@ -1,0 +1,381 @@
+// C ABI of libcompresskv: host-side validation, workspace layout and dispatch.
+// Every check runs before the first HIP call, so invalid arguments never touch
+// the device and can be tested without a GPU.
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <string>
+#include <vector>
+
+#include "../../include/compresskv.h"
+#include "ckv_launch.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int status, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return status;
+}
+
+int ok() {
+  g_last_error.clear();
+  return CKV_OK;
+}
+
+bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+int elem_size(const ckv_problem *p) { return p->dtype == CKV_BF16 ? 2 : 4; }
+
+// Everything derived from a validated problem.
+struct Plan {
+  int64_t T = 0;
+  int lmax = 0;
+  int64_t n_keys = 0;
+  int th = 0;          // row tiles per SRH
+  int rt_max = 0;      // max row tiles of a group
+  int chunk1 = 0, max_chunks1 = 0;
+  int chunk2 = 0, max_chunks2 = 0;
+  size_t scores_off = 0, stats_off = 0, total = 0;
+  std::vector<uint16_t> srh_off;
+  std::vector<uint8_t> srh_head;
+  uint32_t head_end_mask = 0;
+};
+
+int env_int(const char *name, int dflt) {
+  const char *s = std::getenv(name);
+  if (!s || !*s) return dflt;
+  return std::atoi(s);
+}
+
+// Keys per workgroup: the smallest power of two >= lo such that doubling it
+// would leave fewer than `target` workgroups, capped at hi.
+int pick_chunk(const ckv_problem *p, int lo, int hi, int target) {
+  int c = lo;
+  while (c < hi) {
+    int64_t wg = 0;
+    for (int b = 0; b < p->batch; ++b) {
+      const int L = p->cu_seqlens_host[b + 1] - p->cu_seqlens_host[b];
+      wg += (L + 2 * c - 1) / (2 * c);
+    }
+    wg *= p->n_kv_heads;
+    if (wg < target) break;
+    c *= 2;
+  }
+  return c;
+}
+
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Shape and option checks shared by every entry point.
+int check_problem(const ckv_problem *p) {
+  if (!p) return fail(CKV_INVALID_ARGUMENT, "problem is NULL");
+  if (p->batch < 1) return fail(CKV_INVALID_ARGUMENT, "batch must be >= 1 (got %d)", p->batch);
+  if (p->n_kv_heads < 1 || p->n_q_heads < 1)
+    return fail(CKV_INVALID_ARGUMENT, "head counts must be >= 1");
+  if (p->n_q_heads % p->n_kv_heads != 0)
+    return fail(CKV_INVALID_ARGUMENT, "n_q_heads (%d) must be a multiple of n_kv_heads (%d)",
+                p->n_q_heads, p->n_kv_heads);
+  if (p->n_kv_heads > ckv::kMaxKvHeads || p->n_q_heads > ckv::kMaxQHeads)
+    return fail(CKV_UNSUPPORTED, "at most %d KV heads and %d query heads", ckv::kMaxKvHeads,
+                ckv::kMaxQHeads);
+  if (p->head_dim != 64 && p->head_dim != 128)
+    return fail(CKV_UNSUPPORTED, "head_dim must be 64 or 128 (got %d)", p->head_dim);
+  if (p->dtype != CKV_F32 && p->dtype != CKV_BF16)
+    return fail(CKV_UNSUPPORTED, "dtype must be CKV_F32 or CKV_BF16 (got %d)", p->dtype);
+  if (p->window < 1) return fail(CKV_INVALID_ARGUMENT, "window must be >= 1 (got %d)", p->window);
+  if (p->pool_type != CKV_POOL_MAX && p->pool_type != CKV_POOL_AVG)
+    return fail(CKV_INVALID_ARGUMENT, "pool_type must be CKV_POOL_MAX or CKV_POOL_AVG");
+  if (p->pool_kernel < 1 || p->pool_kernel % 2 == 0 || p->pool_kernel > ckv::kMaxPoolKernel)
+    return fail(CKV_INVALID_ARGUMENT, "pool_kernel must be odd and in [1, %d] (got %d)",
+                ckv::kMaxPoolKernel, p->pool_kernel);
+  if (p->reduce_order != CKV_POOL_THEN_MEAN && p->reduce_order != CKV_MEAN_THEN_POOL)
+    return fail(CKV_INVALID_ARGUMENT, "reduce_order must be CKV_POOL_THEN_MEAN or CKV_MEAN_THEN_POOL");
+  if (!(std::isfinite(p->scale)))
+    return fail(CKV_INVALID_ARGUMENT, "scale must be finite");
+  if (!p->cu_seqlens || !p->cu_seqlens_host)
+    return fail(CKV_INVALID_ARGUMENT, "cu_seqlens and cu_seqlens_host are both required");
+  if (!aligned(p->cu_seqlens, 4)) return fail(CKV_UNSUPPORTED, "cu_seqlens must be 4-byte aligned");
+  if (p->cu_seqlens_host[0] != 0) return fail(CKV_INVALID_ARGUMENT, "cu_seqlens[0] must be 0");
+  for (int b = 0; b < p->batch; ++b) {
+    const int L = p->cu_seqlens_host[b + 1] - p->cu_seqlens_host[b];
+    if (L < 0) return fail(CKV_INVALID_ARGUMENT, "cu_seqlens is decreasing at %d", b);
+    if (L < p->window)
+      return fail(CKV_INVALID_ARGUMENT, "sequence %d has length %d < window %d", b, L, p->window);
+  }
+  const int es = elem_size(p);
+  const int64_t strides[4] = {p->k_stride_tok, p->k_stride_head, p->v_stride_tok, p->v_stride_head};
+  for (int i = 0; i < 4; ++i) {
+    if (strides[i] < 1) return fail(CKV_INVALID_ARGUMENT, "K/V strides must be >= 1");
+    if ((strides[i] * es) % 16 != 0)
+      return fail(CKV_UNSUPPORTED, "K/V strides must be multiples of 16 bytes");
+  }
+  return CKV_OK;
+}
+
+// Per-group SRH lists from the host mask.
+int check_mask(const ckv_problem *p, const uint8_t *mask, Plan &pl) {
+  if (!mask) return fail(CKV_INVALID_ARGUMENT, "srh_mask_host is NULL");
+  const int G = p->n_q_heads / p->n_kv_heads;
+  pl.th = (p->window + 15) / 16;
+  pl.srh_off.assign(p->n_kv_heads + 1, 0);
+  pl.srh_head.clear();
+  int nmax = 0;
+  for (int g = 0; g < p->n_kv_heads; ++g) {
+    int n = 0;
+    for (int h = g * G; h < (g + 1) * G; ++h) {
+      if (mask[h]) {
+        pl.srh_head.push_back((uint8_t)h);
+        ++n;
+      }
+    }
+    if (n == 0) return fail(CKV_INVALID_ARGUMENT, "KV group %d has no Semantic Retrieval Head", g);
+    nmax = std::max(nmax, n);
+    pl.srh_off[g + 1] = (uint16_t)pl.srh_head.size();
+  }
+  pl.rt_max = nmax * pl.th;
+  if (pl.rt_max > 12)
+    return fail(CKV_UNSUPPORTED,
+                "ceil(window/16) * SRHs per group must be <= 12 (window %d, %d SRHs)", p->window,
+                nmax);
+  pl.head_end_mask = 0;
+  for (int rt = 0; rt < 32; ++rt)
+    if ((rt + 1) % pl.th == 0) pl.head_end_mask |= 1u << rt;
+  return CKV_OK;
+}
+
+void make_plan(const ckv_problem *p, Plan &pl) {
+  pl.T = p->cu_seqlens_host[p->batch];
+  pl.lmax = 0;
+  for (int b = 0; b < p->batch; ++b)
+    pl.lmax = std::max(pl.lmax, p->cu_seqlens_host[b + 1] - p->cu_seqlens_host[b]);
+  int c1 = env_int("CKV_CHUNK1", 0), c2 = env_int("CKV_CHUNK2", 0);
+  if (c1 <= 0 || c1 % 64 != 0) c1 = pick_chunk(p, 256, 4096, 1024);
+  if (c2 <= 0 || c2 % 64 != 0 || c2 > 1024) c2 = pick_chunk(p, 512, 1024, 1024);
+  pl.chunk1 = c1;
+  pl.chunk2 = c2;
+  pl.max_chunks1 = std::max(1, (pl.lmax + c1 - 1) / c1);
+  pl.max_chunks2 = std::max(1, (pl.lmax + c2 - 1) / c2);
+  pl.scores_off = 0;
+  pl.stats_off = round_up((size_t)p->n_kv_heads * pl.T * sizeof(float), 256);
+  pl.total = pl.stats_off + round_up((size_t)p->batch * p->n_kv_heads * pl.max_chunks1 *
+                                         (size_t)pl.rt_max * 16 * sizeof(float2),
+                                     256);
+}
+
+ckv::ScoreArgs score_args(const ckv_problem *p, const Plan &pl, const void *q, const void *k,
+                          float *scores, void *ws) {
+  ckv::ScoreArgs a{};
+  a.q = q;
+  a.k = k;
+  a.cu = p->cu_seqlens;
+  a.stats = reinterpret_cast<float2 *>(static_cast<char *>(ws) + pl.stats_off);
+  a.scores = scores;
+  a.k_stride_tok = p->k_stride_tok;
+  a.k_stride_head = p->k_stride_head;
+  a.T = (int32_t)pl.T;
+  a.batch = p->batch;
+  a.Hq = p->n_q_heads;
+  a.Hkv = p->n_kv_heads;
+  a.W = p->window;
+  a.th = pl.th;
+  a.row_slots = pl.rt_max * 16;
+  a.chunk1 = pl.chunk1;
+  a.max_chunks1 = pl.max_chunks1;
+  a.chunk2 = pl.chunk2;
+  a.max_chunks2 = pl.max_chunks2;
+  const double scale = p->scale > 0.f ? (double)p->scale : 1.0 / std::sqrt((double)p->head_dim);
+  a.c1 = (float)(scale * 1.4426950408889634);
+  a.pool_kernel = p->pool_kernel;
+  a.pool_type = p->pool_type;
+  a.reduce_order = p->reduce_order;
+  a.head_end_mask = pl.head_end_mask;
+  for (size_t i = 0; i < pl.srh_off.size(); ++i) a.srh_off[i] = pl.srh_off[i];
+  for (size_t i = 0; i < pl.srh_head.size(); ++i) a.srh_head[i] = pl.srh_head[i];
+  return a;
+}
+
+int check_ptr(const void *ptr, const char *name, size_t align) {
+  if (!ptr) return fail(CKV_INVALID_ARGUMENT, "%s is NULL", name);
+  if (!aligned(ptr, align)) return fail(CKV_UNSUPPORTED, "%s must be %zu-byte aligned", name, align);
+  return CKV_OK;
+}
+
+int check_budget(const ckv_problem *p, int32_t budget) {
+  if (budget < p->window)
+    return fail(CKV_INVALID_ARGUMENT, "budget (%d) must be >= window (%d)", budget, p->window);
+  return CKV_OK;
+}
+
+int check_ws(const Plan &pl, const void *ws, size_t ws_bytes) {
+  if (ws_bytes < pl.total)
+    return fail(CKV_WORKSPACE_TOO_SMALL, "workspace of %zu bytes, %zu needed", ws_bytes, pl.total);
+  if (pl.total > 0) {
+    if (!ws) return fail(CKV_INVALID_ARGUMENT, "workspace is NULL");
+    if (!aligned(ws, 256)) return fail(CKV_UNSUPPORTED, "workspace must be 256-byte aligned");
+  }
+  return CKV_OK;
+}
+
+int hip_status(hipError_t e, const char *what) {
+  if (e != hipSuccess)
+    return fail(CKV_HIP_ERROR, "%s launch failed: %s", what, hipGetErrorString(e));
+  return CKV_OK;
+}
+
+ckv::SelectArgs select_args(const ckv_problem *p, const Plan &pl, const float *scores,
+                            int32_t budget, int32_t *idx) {
+  ckv::SelectArgs s{};
+  s.scores = scores;
+  s.cu = p->cu_seqlens;
+  s.idx = idx;
+  s.T = (int32_t)pl.T;
+  s.Hkv = p->n_kv_heads;
+  s.W = p->window;
+  s.budget = budget;
+  return s;
+}
+
+ckv::GatherArgs gather_args(const ckv_problem *p, const void *k, const void *v, const int32_t *idx,
+                            int32_t budget, void *k_out, void *v_out) {
+  const int es = elem_size(p);
+  ckv::GatherArgs g{};
+  g.k = static_cast<const char *>(k);
+  g.v = static_cast<const char *>(v);
+  g.cu = p->cu_seqlens;
+  g.idx = idx;
+  g.k_out = static_cast<char *>(k_out);
+  g.v_out = static_cast<char *>(v_out);
+  g.k_stride_tok = p->k_stride_tok * es;
+  g.k_stride_head = p->k_stride_head * es;
+  g.v_stride_tok = p->v_stride_tok * es;
+  g.v_stride_head = p->v_stride_head * es;
+  g.Hkv = p->n_kv_heads;
+  g.budget = budget;
+  g.row_bytes = p->head_dim * es;
+  return g;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *compresskv_status_string(int status) {
+  switch (status) {
+    case CKV_OK: return "ok";
+    case CKV_INVALID_ARGUMENT: return "invalid argument";
+    case CKV_UNSUPPORTED: return "unsupported";
+    case CKV_WORKSPACE_TOO_SMALL: return "workspace too small";
+    case CKV_HIP_ERROR: return "HIP error";
+    default: return "unknown status";
+  }
+}
+
+const char *compresskv_last_error(void) { return g_last_error.c_str(); }
+
+size_t compresskv_workspace_bytes(const ckv_problem *p, const uint8_t *srh_mask_host,
+                                  int32_t budget) {
+  Plan pl;
+  if (check_problem(p) || check_mask(p, srh_mask_host, pl) || check_budget(p, budget)) return 0;
+  make_plan(p, pl);
+  ok();
+  return pl.total;
+}
+
+int compresskv_score(const ckv_problem *p, const void *q_win, const void *k,
+                     const uint8_t *srh_mask_host, float *scores, void *ws, size_t ws_bytes,
+                     void *stream) {
+  Plan pl;
+  int st;
+  if ((st = check_problem(p))) return st;
+  if ((st = check_mask(p, srh_mask_host, pl))) return st;
+  if ((st = check_ptr(q_win, "q_win", 16)) || (st = check_ptr(k, "k", 16)) ||
+      (st = check_ptr(scores, "scores", 4)))
+    return st;
+  make_plan(p, pl);
+  if ((st = check_ws(pl, ws, ws_bytes))) return st;
+  ckv::ScoreArgs a = score_args(p, pl, q_win, k, scores, ws);
+  if ((st = hip_status(ckv::launch_score(a, p->dtype == CKV_BF16, p->head_dim, pl.rt_max,
+                                         p->batch, (hipStream_t)stream),
+                       "score")))
+    return st;
+  return ok();
+}
+
+int compresskv_select(const ckv_problem *p, const float *scores, int32_t budget, int32_t *idx,
+                      void *ws, size_t ws_bytes, void *stream) {
+  (void)ws;
+  (void)ws_bytes;
+  int st;
+  if ((st = check_problem(p))) return st;
+  if ((st = check_budget(p, budget))) return st;
+  if ((st = check_ptr(scores, "scores", 4)) || (st = check_ptr(idx, "idx", 4))) return st;
+  Plan pl;
+  pl.T = p->cu_seqlens_host[p->batch];
+  if ((st = hip_status(ckv::launch_select(select_args(p, pl, scores, budget, idx), p->batch,
+                                          (hipStream_t)stream),
+                       "select")))
+    return st;
+  return ok();
+}
+
+int compresskv_gather(const ckv_problem *p, const void *k, const void *v, const int32_t *idx,
+                      int32_t budget, void *k_out, void *v_out, void *stream) {
+  int st;
+  if ((st = check_problem(p))) return st;
+  if (budget < 1) return fail(CKV_INVALID_ARGUMENT, "budget must be >= 1 (got %d)", budget);
+  if ((st = check_ptr(k, "k", 16)) || (st = check_ptr(v, "v", 16)) ||
+      (st = check_ptr(idx, "idx", 4)) || (st = check_ptr(k_out, "k_out", 16)) ||
+      (st = check_ptr(v_out, "v_out", 16)))
+    return st;
+  if ((st = hip_status(ckv::launch_gather(gather_args(p, k, v, idx, budget, k_out, v_out),
+                                          p->batch, (hipStream_t)stream),
+                       "gather")))
+    return st;
+  return ok();
+}
+
+int compresskv_compress_layer(const ckv_problem *p, const void *q_win, const void *k,
+                              const void *v, const uint8_t *srh_mask_host, int32_t budget,
+                              int32_t *idx, void *k_out, void *v_out, float *scores_or_null,
+                              void *ws, size_t ws_bytes, void *stream) {
+  Plan pl;
+  int st;
+  if ((st = check_problem(p))) return st;
+  if ((st = check_mask(p, srh_mask_host, pl))) return st;
+  if ((st = check_budget(p, budget))) return st;
+  if ((st = check_ptr(q_win, "q_win", 16)) || (st = check_ptr(k, "k", 16)) ||
+      (st = check_ptr(v, "v", 16)) || (st = check_ptr(idx, "idx", 4)) ||
+      (st = check_ptr(k_out, "k_out", 16)) || (st = check_ptr(v_out, "v_out", 16)))
+    return st;
+  if (scores_or_null && (st = check_ptr(scores_or_null, "scores", 4))) return st;
+  make_plan(p, pl);
+  if ((st = check_ws(pl, ws, ws_bytes))) return st;
+  float *scores = scores_or_null
+                      ? scores_or_null
+                      : reinterpret_cast<float *>(static_cast<char *>(ws) + pl.scores_off);
+  hipStream_t s = (hipStream_t)stream;
+  ckv::ScoreArgs a = score_args(p, pl, q_win, k, scores, ws);
+  if ((st = hip_status(
+           ckv::launch_score(a, p->dtype == CKV_BF16, p->head_dim, pl.rt_max, p->batch, s),
+           "score")))
+    return st;
+  if ((st = hip_status(ckv::launch_select(select_args(p, pl, scores, budget, idx), p->batch, s),
+                       "select")))
+    return st;
+  if ((st = hip_status(
+           ckv::launch_gather(gather_args(p, k, v, idx, budget, k_out, v_out), p->batch, s),
+           "gather")))
+    return st;
+  return ok();
+}
+
+}  // extern "C"

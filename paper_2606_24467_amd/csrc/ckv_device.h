@@ -1,0 +1,108 @@
+// Device-side building blocks of the CompressKV eviction kernels (gfx950).
+//
+// Operand layout used by every scoring kernel.  One wavefront (64 lanes)
+// multiplies a 16-row tile of one matrix with a 16-row tile of another along
+// the head dimension D with v_mfma_f32_16x16x32_bf16 (bf16) or
+// v_mfma_f32_16x16x4_f32 (fp32).  Lane l = 16*quad + c holds row c of each
+// operand tile; for the 16-byte slice s of a row it holds bytes
+// [64*s + 16*quad, 64*s + 16*quad + 16).  A and B use the same slicing, so the
+// pairing of reduction indices is consistent and the MFMA returns plain dot
+// products.  The 16x16 result is held as: lane l, element r = C[4*quad + r][c],
+// where the first index runs over the A rows and the second over the B rows.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ckv {
+
+constexpr int kMaxKvHeads = 128;
+constexpr int kMaxQHeads = 256;
+constexpr int kMaxPoolKernel = 31;   // pooling halo (k-1)/2 <= 15 fits one 16-key tile
+constexpr float kLog2e = 1.4426950408889634f;
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Arguments of the two scoring kernels (one layer).
+struct ScoreArgs {
+  const void *q;          // [batch, W, Hq, D]
+  const void *k;          // [T, Hkv, D] with strides below (elements)
+  const int32_t *cu;      // [batch+1] sequence offsets
+  float2 *stats;          // [batch][Hkv][max_chunks1][row_slots] partial (ref, sum)
+  float *scores;          // [Hkv][T]
+  int64_t k_stride_tok, k_stride_head;
+  int32_t T, batch, Hq, Hkv, W;
+  int32_t th;             // 16-row tiles per SRH: ceil(W / 16)
+  int32_t row_slots;      // padded rows per (sequence, group, chunk) in stats
+  int32_t chunk1, max_chunks1;   // keys per workgroup in the statistics pass
+  int32_t chunk2, max_chunks2;   // keys per workgroup in the column-sum pass
+  float c1;               // softmax scale * log2(e): logits in base-2 units
+  int32_t pool_kernel, pool_type, reduce_order;
+  uint32_t head_end_mask;  // bit rt set if row tile rt is the last tile of an SRH
+  uint16_t srh_off[kMaxKvHeads + 1];   // SRHs of group g: srh_head[srh_off[g] .. srh_off[g+1])
+  uint8_t srh_head[kMaxQHeads];        // query-head indices
+};
+
+struct SelectArgs {
+  const float *scores;    // [Hkv][T]
+  const int32_t *cu;
+  int32_t *idx;           // [batch][Hkv][budget]
+  int32_t T, Hkv, W, budget;
+};
+
+struct GatherArgs {
+  const char *k, *v;
+  const int32_t *cu;
+  const int32_t *idx;
+  char *k_out, *v_out;
+  int64_t k_stride_tok, k_stride_head, v_stride_tok, v_stride_head;  // bytes
+  int32_t Hkv, budget, row_bytes;
+};
+
+// 16-byte slices per row per quad: D * sizeof(T) / 64.
+template <typename T, int D>
+struct Slices {
+  static constexpr int n = D * (int)sizeof(T) / 64;
+};
+
+__device__ __forceinline__ uint4 load16(const char *p) {
+  return *reinterpret_cast<const uint4 *>(p);
+}
+
+// acc += A_tile * B_tile^T over one 16-byte slice of each row.
+template <typename T>
+__device__ __forceinline__ f32x4 mfma_slice(uint4 a, uint4 b, f32x4 acc);
+
+template <>
+__device__ __forceinline__ f32x4 mfma_slice<__bf16>(uint4 a, uint4 b, f32x4 acc) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), acc, 0, 0, 0);
+}
+
+template <>
+__device__ __forceinline__ f32x4 mfma_slice<float>(uint4 a, uint4 b, f32x4 acc) {
+  float4 fa = __builtin_bit_cast(float4, a);
+  float4 fb = __builtin_bit_cast(float4, b);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa.x, fb.x, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa.y, fb.y, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa.z, fb.z, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa.w, fb.w, acc, 0, 0, 0);
+  return acc;
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
+
+// Merge two (reference, sum) pairs, sum_i exp2(y_i - ref), into one.
+__device__ __forceinline__ void merge_stats(float &ref, float &sum, float ref_o, float sum_o) {
+  float m = fmaxf(ref, ref_o);
+  if (m == -INFINITY) {
+    sum = 0.f;
+  } else {
+    sum = sum * fast_exp2(ref - m) + sum_o * fast_exp2(ref_o - m);
+  }
+  ref = m;
+}
+
+}  // namespace ckv

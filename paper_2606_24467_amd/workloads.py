@@ -225,3 +225,55 @@ def make_layer(w: Workload, layer: int = 0, seed: int = 0,
         k[s0:s0 + L] = rnd(kb)
     return LayerInputs(workload=w, layer=layer, cu_seqlens=cu, srh_mask=mask,
                        budget=int(budget), q_win=q, k=k, v=v, needles=needles)
+
+
+def make_layer_device(w: Workload, layer: int, seed: int, device, lengths=None,
+                      budget: int | None = None):
+    """The same recipe drawn with torch's generator on ``device`` (fast for the
+    multi-GiB benchmark stacks).  Returns a dict of device tensors plus the
+    host-side cu_seqlens, SRH mask and budget.  Values differ from make_layer's
+    (another random stream) but follow the same distributions and structure."""
+    import torch
+
+    W, Hq, Hkv, D = w.window, w.n_q_heads, w.n_kv_heads, w.head_dim
+    G = Hq // Hkv
+    lens = seq_lengths(w, seed) if lengths is None else np.asarray(lengths, dtype=np.int64)
+    cu = cu_seqlens(lens)
+    T = int(cu[-1])
+    mask = srh_mask(w, layer, seed)
+    if budget is None:
+        budget = int(layer_budgets(w, seed)[layer])
+    dt = torch.bfloat16 if w.dtype == BF16 else torch.float32
+    gen = torch.Generator(device=device)
+    gen.manual_seed(int(np.random.SeedSequence([seed, w.cid, 7, layer]).generate_state(1)[0]))
+    q = torch.randn((w.batch, W, Hq, D), generator=gen, device=device).to(dt)
+    k32 = torch.randn((T, Hkv, D), generator=gen, device=device)
+    v = torch.randn((T, Hkv, D), generator=gen, device=device).to(dt)
+    needles = {}
+    for b in range(w.batch):
+        L = int(lens[b])
+        s0 = int(cu[b])
+        P = L - W
+        rng = _rng(seed, w.cid, 8, layer, b)
+        qb = q[b].float()
+        for g in range(Hkv):
+            heads = list(range(g * G, (g + 1) * G))
+            srh = [h for h in heads if mask[h]] or heads
+            sink_dir = qb[:, heads, :].mean(dim=(0, 1))
+            needle_dir = qb[:, srh, :].mean(dim=(0, 1))
+            sink_dir = sink_dir / sink_dir.norm().clamp_min(1e-30)
+            needle_dir = needle_dir / needle_dir.norm().clamp_min(1e-30)
+            n_sink = min(w.n_sink, max(P, 0))
+            if n_sink:
+                k32[s0:s0 + n_sink, g, :] = 3.0 * math.sqrt(D) * sink_dir
+            lo, hi = n_sink + 2 * w.pool_kernel, P - 2 * w.pool_kernel
+            pos = _needle_positions(rng, w.n_needle, lo, hi, 2 * w.pool_kernel) if hi > lo \
+                else np.zeros(0, dtype=np.int64)
+            if pos.size:
+                k32[s0 + torch.from_numpy(pos).to(device), g, :] = 3.0 * math.sqrt(D) * needle_dir
+            needles[(b, g)] = pos
+    k = k32.to(dt)
+    del k32
+    cu_dev = torch.from_numpy(cu.astype(np.int32)).to(device)
+    return dict(q_win=q, k=k, v=v, cu_seqlens=cu_dev, cu_seqlens_host=cu, srh_mask=mask,
+                budget=int(budget), needles=needles)

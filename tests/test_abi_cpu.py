@@ -1,0 +1,157 @@
+"""The C ABI without a GPU: the library loads, exports every symbol the header
+declares, sizes workspaces, and rejects invalid arguments on the host before
+any HIP call (so no device is touched).  Only invalid calls are made here."""
+import ctypes
+import subprocess
+
+import numpy as np
+import pytest
+
+from paper_2606_24467_amd import build as B
+from paper_2606_24467_amd import compresskv as C
+
+FAKE = 0x10000000  # aligned, never dereferenced: every call below fails validation first
+
+
+@pytest.fixture(scope="module")
+def L():
+    import os
+    if not os.path.exists(B.lib_path()):
+        B.build()
+    return C.lib()
+
+
+def test_every_header_symbol_is_exported(L):
+    names = C.exported_names()
+    assert {"compresskv_score", "compresskv_select", "compresskv_gather",
+            "compresskv_compress_layer", "compresskv_workspace_bytes",
+            "compresskv_status_string", "compresskv_last_error"} <= set(names)
+    out = subprocess.run(["nm", "-D", "--defined-only", B.lib_path()], capture_output=True,
+                         text=True).stdout
+    defined = {line.split()[-1] for line in out.splitlines() if line.strip()}
+    for n in names:
+        assert n in defined, n
+        assert hasattr(L, n)
+
+
+def test_status_strings(L):
+    for s, text in [(0, "ok"), (1, "invalid argument"), (2, "unsupported"),
+                    (3, "workspace too small"), (4, "HIP error")]:
+        assert L.compresskv_status_string(s).decode() == text
+
+
+class Case:
+    """A valid problem description plus host arrays kept alive for the call."""
+
+    def __init__(self, lens=(100, 200), Hq=8, Hkv=2, D=128, W=16, dtype=C.BF16):
+        self.cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+        self.mask = np.zeros(Hq, dtype=np.uint8)
+        G = Hq // Hkv
+        self.mask[::G] = 1
+        self.p = C.CkvProblem(batch=len(lens), n_q_heads=Hq, n_kv_heads=Hkv, head_dim=D,
+                              window=W, dtype=dtype, pool_type=C.POOL_MAX, pool_kernel=7,
+                              reduce_order=C.POOL_THEN_MEAN, scale=0.0, cu_seqlens=FAKE,
+                              cu_seqlens_host=self.cu.ctypes.data, k_stride_tok=Hkv * D,
+                              k_stride_head=D, v_stride_tok=Hkv * D, v_stride_head=D)
+
+    def ws_bytes(self, L, budget=64):
+        return L.compresskv_workspace_bytes(ctypes.byref(self.p), self.mask.ctypes.data, budget)
+
+    def score(self, L, q=FAKE, k=FAKE, scores=FAKE, ws=FAKE, ws_bytes=1 << 40):
+        return L.compresskv_score(ctypes.byref(self.p), q, k, self.mask.ctypes.data, scores, ws,
+                                  ws_bytes, None)
+
+    def compress(self, L, budget=64, ws_bytes=1 << 40, ws=FAKE, k_out=FAKE):
+        return L.compresskv_compress_layer(ctypes.byref(self.p), FAKE, FAKE, FAKE,
+                                           self.mask.ctypes.data, budget, FAKE, k_out, FAKE, None,
+                                           ws, ws_bytes, None)
+
+    def select(self, L, budget=64):
+        return L.compresskv_select(ctypes.byref(self.p), FAKE, budget, FAKE, None, 0, None)
+
+    def gather(self, L, budget=64, idx=FAKE):
+        return L.compresskv_gather(ctypes.byref(self.p), FAKE, FAKE, idx, budget, FAKE, FAKE,
+                                   None)
+
+
+def test_workspace_bytes_layout(L):
+    c = Case()
+    n = c.ws_bytes(L)
+    assert n > 0 and n % 256 == 0
+    T = int(c.cu[-1])
+    scores = -(-2 * T * 4 // 256) * 256
+    assert n >= scores + 2 * 2 * 16 * 8          # scores + one chunk of row stats per group
+    assert L.compresskv_last_error().decode() == ""
+
+
+def _mutate(case, **fields):
+    for k, v in fields.items():
+        setattr(case.p, k, v)
+    return case
+
+
+INVALID = [
+    ("batch", dict(batch=0), C.INVALID_ARGUMENT),
+    ("heads", dict(n_q_heads=7), C.INVALID_ARGUMENT),
+    ("head_dim", dict(head_dim=96), C.UNSUPPORTED),
+    ("dtype", dict(dtype=7), C.UNSUPPORTED),
+    ("window", dict(window=0), C.INVALID_ARGUMENT),
+    ("even pool", dict(pool_kernel=4), C.INVALID_ARGUMENT),
+    ("big pool", dict(pool_kernel=33), C.INVALID_ARGUMENT),
+    ("pool type", dict(pool_type=2), C.INVALID_ARGUMENT),
+    ("order", dict(reduce_order=2), C.INVALID_ARGUMENT),
+    ("cu null", dict(cu_seqlens=None), C.INVALID_ARGUMENT),
+    ("cu misaligned", dict(cu_seqlens=FAKE + 2), C.UNSUPPORTED),
+    ("stride", dict(k_stride_tok=100), C.UNSUPPORTED),
+    ("stride zero", dict(v_stride_head=0), C.INVALID_ARGUMENT),
+    ("too many kv heads", dict(n_kv_heads=256, n_q_heads=256), C.UNSUPPORTED),
+]
+
+
+@pytest.mark.parametrize("name,fields,status", INVALID, ids=[c[0] for c in INVALID])
+def test_invalid_problem_is_rejected_everywhere(L, name, fields, status):
+    for call in ("score", "compress", "select", "gather"):
+        c = _mutate(Case(), **fields)
+        st = getattr(c, call)(L)
+        assert st == status, (call, st, L.compresskv_last_error())
+        assert L.compresskv_last_error().decode() != ""
+    c = _mutate(Case(), **fields)
+    assert c.ws_bytes(L) == 0
+
+
+@pytest.mark.parametrize("cu,status", [
+    ([0, 100, 90], C.INVALID_ARGUMENT),     # decreasing
+    ([0, 10, 200], C.INVALID_ARGUMENT),     # a sequence shorter than the window
+    ([5, 100, 300], C.INVALID_ARGUMENT),    # cu[0] != 0
+])
+def test_bad_cu_seqlens(L, cu, status):
+    c = Case()
+    c.cu[:] = cu
+    assert c.score(L) == status
+    assert c.compress(L) == status
+
+
+def test_mask_rules(L):
+    c = Case()
+    c.mask[:] = 0
+    c.mask[0] = 1                      # group 1 has no SRH
+    assert c.score(L) == C.INVALID_ARGUMENT
+    assert "no Semantic Retrieval Head" in L.compresskv_last_error().decode()
+    c = Case(W=64, Hq=32, Hkv=4)
+    c.mask[:] = 1                      # 8 SRHs x 4 row tiles = 32 > 12
+    assert c.score(L) == C.UNSUPPORTED
+
+
+def test_budget_pointer_and_workspace_rules(L):
+    c = Case()
+    assert c.compress(L, budget=15) == C.INVALID_ARGUMENT          # budget < W
+    assert c.select(L, budget=15) == C.INVALID_ARGUMENT
+    assert c.gather(L, budget=0) == C.INVALID_ARGUMENT
+    assert c.score(L, q=0) == C.INVALID_ARGUMENT
+    assert c.score(L, k=FAKE + 8) == C.UNSUPPORTED                 # 16-byte alignment
+    assert c.gather(L, idx=FAKE + 2) == C.UNSUPPORTED
+    assert c.compress(L, k_out=0) == C.INVALID_ARGUMENT
+    need = c.ws_bytes(L)
+    assert c.compress(L, ws_bytes=need - 1) == C.WORKSPACE_TOO_SMALL
+    assert c.score(L, ws_bytes=need - 1) == C.WORKSPACE_TOO_SMALL
+    assert c.compress(L, ws=FAKE + 16) == C.UNSUPPORTED            # 256-byte alignment

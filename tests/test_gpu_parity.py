@@ -1,0 +1,212 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle on the
+same seeded inputs.  Acceptance rules are in tests/parity_helpers.py."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2606_24467_amd import compresskv as C
+from paper_2606_24467_amd import workloads as wl
+from tests import parity_helpers as H
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def run_case(x: wl.LayerInputs, dev, *, budget=None, pool_kernel=None, pool_type=None,
+             reduce_order=C.POOL_THEN_MEAN, scale=None, groups=None, check=True):
+    w = x.workload
+    budget = x.budget if budget is None else budget
+    pk = w.pool_kernel if pool_kernel is None else pool_kernel
+    pt = w.pool_type if pool_type is None else pool_type
+    _say(f"case {w.name} L={np.diff(x.cu_seqlens).tolist()[:8]} budget={budget} pool={pk}/{pt} "
+         f"order={reduce_order}")
+    q, k, v, cu = H.device_tensors(x, dev)
+    p = C.Problem(q, k, v, cu, cu_seqlens_host=x.cu_seqlens, pool_kernel=pk, pool_type=pt,
+                  reduce_order=reduce_order, scale=scale)
+    idx, k_out, v_out, scores = C.compress_layer(p, q, k, v, x.srh_mask, budget, want_scores=True)
+    torch.cuda.synchronize()
+    res = dict(idx=idx.cpu().numpy(), k_out=H.raw_bits(k_out), v_out=H.raw_bits(v_out),
+               scores=scores.cpu().numpy())
+    if not check:
+        return res, None
+    ora = H.run_oracle(x, budget, pk, pt, reduce_order, scale)
+    W = w.window
+    H.check_scores(res["scores"], ora, x.cu_seqlens, W, groups)
+    swaps = H.check_indices(res["idx"], ora, x.cu_seqlens, W, budget, groups)
+    kb = x.bits("k") if x.dtype == wl.BF16 else x.k.view(np.uint32)
+    vb = x.bits("v") if x.dtype == wl.BF16 else x.v.view(np.uint32)
+    H.check_gather(res["k_out"], res["v_out"], res["idx"], kb, vb, x.cu_seqlens, groups)
+    _say(f"  ok, boundary swaps {swaps}")
+    return res, ora
+
+
+def test_tiny_full(gpu):
+    x = wl.make_layer(wl.get("tiny"), 0, seed=0)
+    res, _ = run_case(x, gpu)
+    for (b, g), pos in x.needles.items():      # needles survive on the GPU path too
+        assert set(pos.tolist()) <= set(res["idx"][b, g].tolist())
+
+
+@pytest.mark.parametrize("seed", [1, 2])
+def test_tiny_seeds_and_orders(gpu, seed):
+    x = wl.make_layer(wl.get("tiny"), 0, seed=seed)
+    run_case(x, gpu, reduce_order=C.MEAN_THEN_POOL)
+    run_case(x, gpu, pool_type=C.POOL_AVG)
+
+
+def test_llama_shape_reduced_length(gpu):
+    w = wl.get("llama1", seq_len=4096 + 37, n_needle=8)     # ragged tail, several chunks
+    run_case(wl.make_layer(w, 0, seed=3), gpu)
+
+
+def test_llama_full_length_single_layer(gpu):
+    x = wl.make_layer(wl.get("llama1"), 0, seed=0)
+    res, _ = run_case(x, gpu)
+    for (b, g), pos in x.needles.items():
+        assert set(pos.tolist()) <= set(res["idx"][b, g].tolist())
+
+
+@pytest.mark.parametrize("layer", [0, 5])
+def test_llama_stack_layers_varying_srh(gpu, layer):
+    w = wl.get("llama32", seq_len=6000)
+    x = wl.make_layer(w, layer, seed=0)
+    assert x.srh_mask.reshape(8, 4).sum(1).max() >= 2
+    run_case(x, gpu)
+
+
+def test_qwen_shape_reduced(gpu):
+    w = wl.get("qwen128k", seq_len=9000, n_needle=8)
+    x = wl.make_layer(w, 0, seed=0, budget=400)
+    run_case(x, gpu)
+
+
+def test_ragged_batch(gpu):
+    w = wl.get("ragged8", batch=4, ragged=(900, 2500))
+    x = wl.make_layer(w, 0, seed=4)
+    run_case(x, gpu)
+
+
+def test_paper_setting_window8_kernel5(gpu):
+    """Section 4 setting: window 8, pooling kernel 5, 4 SRHs in a group."""
+    w = wl.get("llama1", seq_len=3000, window=8, pool_kernel=5, n_needle=4,
+               srh_per_group=(4,), budget=256)
+    run_case(wl.make_layer(w, 0, seed=5), gpu)
+
+
+@pytest.mark.parametrize("D", [64, 128])
+def test_fp32_head_dims(gpu, D):
+    w = wl.get("tiny", head_dim=D, seq_len=2000 + 5)
+    run_case(wl.make_layer(w, 0, seed=6), gpu)
+
+
+def test_bf16_head_dim_64(gpu):
+    w = wl.get("llama1", head_dim=64, seq_len=2500, n_needle=4)
+    run_case(wl.make_layer(w, 0, seed=7), gpu)
+
+
+def test_edge_lengths_and_budgets(gpu):
+    """L = W (no prefix), L <= budget (keep all), budget = W (window only),
+    lengths not multiples of 16, pooling kernels 1 and 31."""
+    w = wl.get("llama1", batch=5, n_needle=0, n_sink=2, ragged=(1, 1))
+    lens = np.array([32, 33, 47, 700, 1201])
+    x = wl.make_layer(w, 0, seed=8, lengths=lens, budget=64)
+    run_case(x, gpu)
+    run_case(x, gpu, budget=32)
+    run_case(x, gpu, budget=2000)
+    run_case(x, gpu, pool_kernel=1)
+    run_case(x, gpu, pool_kernel=31)
+
+
+def test_custom_scale(gpu):
+    w = wl.get("tiny", seq_len=1500)
+    run_case(wl.make_layer(w, 0, seed=9), gpu, scale=0.05)
+
+
+def test_select_alone_matches_oracle_on_same_fp32_scores(gpu):
+    """S5 in isolation: fed the oracle's scores rounded to fp32, both sides
+    decide on identical values, so the indices must match exactly."""
+    w = wl.get("ragged8", batch=3, ragged=(700, 3000))
+    x = wl.make_layer(w, 0, seed=10)
+    ora = H.run_oracle(x, budget=256)
+    s32 = ora.scores.astype(np.float32)
+    s32[:, :] = np.where(np.isinf(ora.scores), np.inf, s32)
+    q, k, v, cu = H.device_tensors(x, gpu)
+    p = C.Problem(q, k, v, cu, cu_seqlens_host=x.cu_seqlens)
+    for budget in (32, 33, 256, 1000, 5000):
+        idx = C.select(p, torch.from_numpy(s32).to(gpu), budget).cpu().numpy()
+        for b in range(3):
+            s0, s1 = x.cu_seqlens[b], x.cu_seqlens[b + 1]
+            L = s1 - s0
+            for g in range(x.workload.n_kv_heads):
+                sel = O.select_tokens(s32[g, s0:s1 - 32].astype(np.float64), L, 32, budget)
+                n = len(sel)
+                assert np.array_equal(idx[b, g, :n], sel), (budget, b, g)
+                assert np.all(idx[b, g, n:] == -1)
+
+
+def test_select_ties_go_to_lowest_position(gpu):
+    """Constant scores keep the lowest prefix positions; a block of higher
+    scores is kept first and the rest of the budget goes to the lowest ties."""
+    w = wl.get("llama1", seq_len=5000, n_needle=0)
+    x = wl.make_layer(w, 0, seed=11)
+    q, k, v, cu = H.device_tensors(x, gpu)
+    p = C.Problem(q, k, v, cu, cu_seqlens_host=x.cu_seqlens)
+    s = np.full((8, 5000), 0.25, dtype=np.float32)
+    s[:, 4968:] = np.inf
+    s[3, 3000:3010] = 0.5
+    idx = C.select(p, torch.from_numpy(s).to(gpu), 200).cpu().numpy()
+    window = list(range(4968, 5000))
+    assert idx[0, 0].tolist() == list(range(168)) + window
+    assert idx[0, 3].tolist() == list(range(158)) + list(range(3000, 3010)) + window
+
+
+def test_gather_alone_is_bit_exact_with_oracle_indices(gpu):
+    w = wl.get("ragged8", batch=3, ragged=(500, 1500))
+    x = wl.make_layer(w, 0, seed=12)
+    ora = H.run_oracle(x, budget=600)
+    q, k, v, cu = H.device_tensors(x, gpu)
+    p = C.Problem(q, k, v, cu, cu_seqlens_host=x.cu_seqlens)
+    idx = torch.from_numpy(ora.idx.astype(np.int32)).to(gpu)
+    k_out, v_out = C.gather(p, k, v, idx, 600)
+    np.testing.assert_array_equal(H.raw_bits(k_out), ora.k_out)
+    np.testing.assert_array_equal(H.raw_bits(v_out), ora.v_out)
+
+
+def test_strided_kv_layout(gpu):
+    """K/V stored head-major [Hkv, T, D] and passed as a strided [T, Hkv, D] view."""
+    w = wl.get("llama1", seq_len=3000, n_needle=4)
+    x = wl.make_layer(w, 0, seed=13)
+    q, k, v, cu = H.device_tensors(x, gpu)
+    kh = k.permute(1, 0, 2).contiguous().permute(1, 0, 2)
+    vh = v.permute(1, 0, 2).contiguous().permute(1, 0, 2)
+    assert kh.stride() != k.stride()
+    p1 = C.Problem(q, k, v, cu, cu_seqlens_host=x.cu_seqlens)
+    p2 = C.Problem(q, kh, vh, cu, cu_seqlens_host=x.cu_seqlens)
+    a = C.compress_layer(p1, q, k, v, x.srh_mask, 512, want_scores=True)
+    b = C.compress_layer(p2, q, kh, vh, x.srh_mask, 512, want_scores=True)
+    for t1, t2 in zip(a, b):
+        assert torch.equal(t1, t2)
+
+
+def test_deterministic_bits(gpu):
+    w = wl.get("llama1", seq_len=8192, n_needle=8)
+    x = wl.make_layer(w, 0, seed=14)
+    r1, _ = run_case(x, gpu, check=False)
+    r2, _ = run_case(x, gpu, check=False)
+    for key in r1:
+        assert np.array_equal(r1[key], r2[key]), key
+
+
+def test_score_entry_point_alone(gpu):
+    w = wl.get("llama1", seq_len=2048 + 3, n_needle=4)
+    x = wl.make_layer(w, 0, seed=15)
+    q, k, v, cu = H.device_tensors(x, gpu)
+    p = C.Problem(q, k, v, cu, cu_seqlens_host=x.cu_seqlens)
+    s = C.score(p, q, k, x.srh_mask).cpu().numpy()
+    H.check_scores(s, H.run_oracle(x), x.cu_seqlens, 32)
