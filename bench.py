@@ -1,8 +1,9 @@
 #!/usr/bin/env python
 """Benchmark of the CompressKV prefill-time eviction path on one MI355X.
 
-A step compresses every layer of the workload once (score -> select ->
-gather per layer, all on one stream) with inputs already resident in HBM.
+A step compresses every layer of the workload once (compresskv_compress_layer
+per layer: score -> select -> gather) with inputs already resident in HBM;
+layers are independent, so they alternate over --streams streams.
 The reported value is prompt tokens compressed per second per layer:
 sum_b L_b * n_layers / step_time.
 
@@ -101,6 +102,8 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--streams", type=int, default=2,
+                    help="layers are independent: alternate them over this many streams")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: this path has no multi-GPU mode "
@@ -149,19 +152,32 @@ def main():
         sb, gb = algorithmic_bytes(lens, w.n_kv_heads, w.head_dim, es, w.window, n_srh, B_l)
         score_bytes_total += sb
         alg_bytes_total += sb + gb
-    ws = torch.empty(ws_need, dtype=torch.uint8, device=dev)
-    scores = torch.empty((w.n_kv_heads, probs[0].total_tokens), dtype=torch.float32, device=dev)
-    stream = torch.cuda.current_stream()
+    # One workspace (row statistics, histogram, scores) per stream; every
+    # stream keeps the default priority.
+    n_streams = max(1, args.streams)
+    streams = [torch.cuda.current_stream()] + [torch.cuda.Stream() for _ in range(n_streams - 1)]
+    ws = [torch.empty(ws_need, dtype=torch.uint8, device=dev) for _ in streams]
+    main = streams[0]
 
     def step(events=None):
+        # fork: every stream starts after the work already queued on the main stream
+        fork = torch.cuda.Event()
+        fork.record(main)
+        for st in streams[1:]:
+            st.wait_event(fork)
         for li, (lay, p, (idx, k_out, v_out)) in enumerate(zip(layers, probs, outs)):
+            si = li % n_streams
+            st, wsi = streams[si], ws[si]
             if events is not None:
-                events[li][0].record(stream)
-            C.compresskv_score(p, lay["q_win"], lay["k"], lay["srh_mask"], scores, ws, stream)
+                events[li][0].record(st)
+            C.compresskv_compress_layer(p, lay["q_win"], lay["k"], lay["v"], lay["srh_mask"],
+                                        lay["budget"], idx, k_out, v_out, None, wsi, st)
             if events is not None:
-                events[li][1].record(stream)
-            C.compresskv_select(p, scores, lay["budget"], idx, None, stream)
-            C.compresskv_gather(p, lay["k"], lay["v"], idx, lay["budget"], k_out, v_out, stream)
+                events[li][1].record(st)
+        for st in streams[1:]:   # join
+            ev = torch.cuda.Event()
+            ev.record(st)
+            main.wait_event(ev)
 
     for i in range(args.warmup):
         step()
@@ -176,8 +192,20 @@ def main():
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     log(f"bench: {args.steps} timed steps in {elapsed * 1e3:.2f} ms")
-    score_ms = [e[0].elapsed_time(e[1]) for per_step in ev for e in per_step]
-    score_ms_avg = float(np.mean(score_ms))
+    layer_ms = [e[0].elapsed_time(e[1]) for per_step in ev for e in per_step]
+    layer_ms_avg = float(np.mean(layer_ms))
+
+    # Score phase alone (the kernels that stream K), one layer after another on
+    # the main stream, bracketed by events on that stream.
+    scores_buf = torch.empty((w.n_kv_heads, probs[0].total_tokens), dtype=torch.float32,
+                             device=dev)
+    sev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in layers]
+    for li, (lay, p) in enumerate(zip(layers, probs)):
+        sev[li][0].record(main)
+        C.compresskv_score(p, lay["q_win"], lay["k"], lay["srh_mask"], scores_buf, ws[0], main)
+        sev[li][1].record(main)
+    torch.cuda.synchronize()
+    score_ms_avg = float(np.mean([e[0].elapsed_time(e[1]) for e in sev]))
     score_bytes_avg = score_bytes_total / n_layers
     ms_per_step = elapsed * 1e3 / args.steps
     tokens = sum(lens)
@@ -201,7 +229,8 @@ def main():
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
                      "avg_ms": score_ms_avg, "bytes_per_launch": score_bytes_avg},
         "end_to_end": {"algorithmic_bytes_per_step": alg_bytes_total, "achieved_gbs": e2e_gbs,
-                       "frac": e2e_gbs / HBM_PEAK_GBS},
+                       "frac": e2e_gbs / HBM_PEAK_GBS, "streams": n_streams,
+                       "layer_ms_avg_in_stream": layer_ms_avg},
     }
     if not args.no_cpu_baseline:
         log("bench: timing the fp64 oracle on a bounded sample")

@@ -44,7 +44,7 @@ struct Plan {
   int rt_max = 0;      // max row tiles of a group
   int chunk1 = 0, max_chunks1 = 0;
   int chunk2 = 0, max_chunks2 = 0;
-  size_t scores_off = 0, stats_off = 0, total = 0;
+  size_t scores_off = 0, stats_off = 0, hist_off = 0, total = 0;
   std::vector<uint16_t> srh_off;
   std::vector<uint8_t> srh_head;
   uint32_t head_end_mask = 0;
@@ -157,18 +157,22 @@ void make_plan(const ckv_problem *p, Plan &pl) {
   pl.lmax = 0;
   for (int b = 0; b < p->batch; ++b)
     pl.lmax = std::max(pl.lmax, p->cu_seqlens_host[b + 1] - p->cu_seqlens_host[b]);
+  // Keys per workgroup: multiples of 512 (stats: 8 waves x 2-tile groups, at
+  // least two groups per wave) and 992 + 32 halo keys (column sums).
   int c1 = env_int("CKV_CHUNK1", 0), c2 = env_int("CKV_CHUNK2", 0);
-  if (c1 <= 0 || c1 % 64 != 0) c1 = pick_chunk(p, 256, 4096, 1024);
-  if (c2 <= 0 || c2 % 64 != 0 || c2 > 1024) c2 = pick_chunk(p, 512, 1024, 1024);
+  if (c1 <= 0 || c1 % 512 != 0) c1 = pick_chunk(p, 512, 4096, 256);
+  if (c2 <= 0 || (c2 + 32) % 256 != 0 || c2 > ckv::kMaxChunk2) c2 = 992;
   pl.chunk1 = c1;
   pl.chunk2 = c2;
   pl.max_chunks1 = std::max(1, (pl.lmax + c1 - 1) / c1);
   pl.max_chunks2 = std::max(1, (pl.lmax + c2 - 1) / c2);
   pl.scores_off = 0;
   pl.stats_off = round_up((size_t)p->n_kv_heads * pl.T * sizeof(float), 256);
-  pl.total = pl.stats_off + round_up((size_t)p->batch * p->n_kv_heads * pl.max_chunks1 *
-                                         (size_t)pl.rt_max * 16 * sizeof(float2),
-                                     256);
+  pl.hist_off = pl.stats_off + round_up((size_t)p->batch * p->n_kv_heads * pl.max_chunks1 *
+                                            (size_t)pl.rt_max * 16 * sizeof(float2),
+                                        256);
+  pl.total = pl.hist_off +
+             round_up((size_t)p->batch * p->n_kv_heads * ckv::kHistBins * sizeof(int), 256);
 }
 
 ckv::ScoreArgs score_args(const ckv_problem *p, const Plan &pl, const void *q, const void *k,
@@ -179,6 +183,7 @@ ckv::ScoreArgs score_args(const ckv_problem *p, const Plan &pl, const void *q, c
   a.cu = p->cu_seqlens;
   a.stats = reinterpret_cast<float2 *>(static_cast<char *>(ws) + pl.stats_off);
   a.scores = scores;
+  a.hist = reinterpret_cast<int *>(static_cast<char *>(ws) + pl.hist_off);
   a.k_stride_tok = p->k_stride_tok;
   a.k_stride_head = p->k_stride_head;
   a.T = (int32_t)pl.T;
@@ -232,9 +237,10 @@ int hip_status(hipError_t e, const char *what) {
 }
 
 ckv::SelectArgs select_args(const ckv_problem *p, const Plan &pl, const float *scores,
-                            int32_t budget, int32_t *idx) {
+                            const int *hist, int32_t budget, int32_t *idx) {
   ckv::SelectArgs s{};
   s.scores = scores;
+  s.hist = hist;
   s.cu = p->cu_seqlens;
   s.idx = idx;
   s.T = (int32_t)pl.T;
@@ -320,8 +326,8 @@ int compresskv_select(const ckv_problem *p, const float *scores, int32_t budget,
   if ((st = check_ptr(scores, "scores", 4)) || (st = check_ptr(idx, "idx", 4))) return st;
   Plan pl;
   pl.T = p->cu_seqlens_host[p->batch];
-  if ((st = hip_status(ckv::launch_select(select_args(p, pl, scores, budget, idx), p->batch,
-                                          (hipStream_t)stream),
+  if ((st = hip_status(ckv::launch_select(select_args(p, pl, scores, nullptr, budget, idx),
+                                          p->batch, (hipStream_t)stream),
                        "select")))
     return st;
   return ok();
@@ -368,8 +374,10 @@ int compresskv_compress_layer(const ckv_problem *p, const void *q_win, const voi
            ckv::launch_score(a, p->dtype == CKV_BF16, p->head_dim, pl.rt_max, p->batch, s),
            "score")))
     return st;
-  if ((st = hip_status(ckv::launch_select(select_args(p, pl, scores, budget, idx), p->batch, s),
-                       "select")))
+  const int *hist = reinterpret_cast<const int *>(static_cast<char *>(ws) + pl.hist_off);
+  if ((st = hip_status(
+           ckv::launch_select(select_args(p, pl, scores, hist, budget, idx), p->batch, s),
+           "select")))
     return st;
   if ((st = hip_status(
            ckv::launch_gather(gather_args(p, k, v, idx, budget, k_out, v_out), p->batch, s),

@@ -19,7 +19,12 @@ namespace ckv {
 constexpr int kMaxKvHeads = 128;
 constexpr int kMaxQHeads = 256;
 constexpr int kMaxPoolKernel = 31;   // pooling halo (k-1)/2 <= 15 fits one 16-key tile
-constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kMaxChunk2 = 1024;     // keys per column-sum workgroup (LDS column sums)
+constexpr int kHistBins = 2048;      // first radix digit of the selection: value bits 30..20
+
+// Scores are non-negative floats, ordered like their bit patterns; the first
+// selection digit is the exponent and the top three mantissa bits.
+__device__ __forceinline__ int hist_bin(uint32_t u) { return (int)((u >> 20) & 0x7FFu); }
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -31,6 +36,7 @@ struct ScoreArgs {
   const int32_t *cu;      // [batch+1] sequence offsets
   float2 *stats;          // [batch][Hkv][max_chunks1][row_slots] partial (ref, sum)
   float *scores;          // [Hkv][T]
+  int *hist;              // [batch][Hkv][kHistBins] counts of the first selection digit
   int64_t k_stride_tok, k_stride_head;
   int32_t T, batch, Hq, Hkv, W;
   int32_t th;             // 16-row tiles per SRH: ceil(W / 16)
@@ -46,6 +52,7 @@ struct ScoreArgs {
 
 struct SelectArgs {
   const float *scores;    // [Hkv][T]
+  const int *hist;        // [batch][Hkv][kHistBins] or NULL (then counted here)
   const int32_t *cu;
   int32_t *idx;           // [batch][Hkv][budget]
   int32_t T, Hkv, W, budget;

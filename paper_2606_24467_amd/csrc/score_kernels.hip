@@ -12,33 +12,90 @@
 //                  recomputes the logits of its chunk (plus a 16-key halo on
 //                  each side for pooling), sums the normalised probabilities
 //                  over the window rows of each SRH, pools along the token axis
-//                  in LDS and averages over the SRHs.
+//                  in LDS, averages over the SRHs, and adds the scores to a
+//                  2048-bin histogram of their top bits (first digit of the
+//                  radix selection, S5).
 //
 // Rows of a KV group: SRH h (in head order) owns th = ceil(W/16) row tiles of
 // 16 rows; row i < W of the tile set is window query i of that head, the
-// padding rows have zero queries and are ignored.
+// padding rows have zero queries and are ignored.  A workgroup (8 waves)
+// stages the group's window queries in LDS once; each wave keeps them in
+// registers when they fit (up to 4 row tiles) and otherwise reads them from
+// LDS per MFMA.  Each wave streams its key tiles through a two-deep pipeline
+// of 2-tile groups (8 KB each): loads are unconditional (key index clamped
+// into the sequence, extra tiles masked), so the compiler can wait for exactly
+// the group being consumed while the next one is still in flight.
 #include "ckv_device.h"
 
 namespace ckv {
 
-// Load one 16-row operand tile of window queries (rows = window positions of
-// one SRH) into per-lane slices.  Rows past W are zero.
 template <typename T, int D>
-__device__ __forceinline__ void load_q_tile(const ScoreArgs &a, int b, int head, int row0,
-                                            int c, int quad, uint4 (&out)[Slices<T, D>::n]) {
-  const int i = row0 + c;
-  if (i < a.W) {
-    const char *p = reinterpret_cast<const char *>(a.q) +
-                    ((((int64_t)b * a.W + i) * a.Hq + head) * D) * (int64_t)sizeof(T) + 16 * quad;
+struct QLayout {
+  static constexpr int NS = Slices<T, D>::n;   // 16-byte slices per row and quad
+  static constexpr int U4 = 4 * NS;            // 16-byte units per row
+  static constexpr int STRIDE = U4 + 1;        // padded row stride in LDS (bank spread)
+};
+
+constexpr int kWaves = 8;       // waves per scoring workgroup
+constexpr int kPair = 2;        // key tiles per load group; two groups in flight per wave
+
+// Row tiles kept in registers: all of them when they fit in 64 VGPRs, else none.
+template <typename T, int D, int RTM>
+struct RegTiles {
+  static constexpr int v = RTM * Slices<T, D>::n <= 16 ? RTM : 0;
+  static constexpr int n = v > 0 ? v : 1;   // array extent
+};
+
+// The group's SRH window queries (rt_n row tiles) staged in LDS in two
+// phases: q_load issues every global load (before the first key loads, so that
+// waiting for the queries never waits for keys), q_store writes them to LDS.
+// Rows past W and tiles past rt_n are zero.
+template <typename T, int D, int RTM, int NT>
+struct QStage {
+  static constexpr int U4 = QLayout<T, D>::U4;
+  static constexpr int n = (RTM * 16 * U4 + NT - 1) / NT;   // 16-byte units per thread
+};
+
+template <typename T, int D, int RTM, int NT>
+__device__ __forceinline__ void q_load(const ScoreArgs &a, int b, int off, int rt_n,
+                                       uint4 (&qv)[QStage<T, D, RTM, NT>::n]) {
+  constexpr int U4 = QLayout<T, D>::U4;
+  const char *qb = reinterpret_cast<const char *>(a.q);
 #pragma unroll
-    for (int s = 0; s < Slices<T, D>::n; ++s) out[s] = load16(p + 64 * s);
-  } else {
-#pragma unroll
-    for (int s = 0; s < Slices<T, D>::n; ++s) out[s] = make_uint4(0, 0, 0, 0);
+  for (int it = 0; it < QStage<T, D, RTM, NT>::n; ++it) {
+    const int idx = (int)threadIdx.x + it * NT;
+    const int row = idx / U4, u = idx - row * U4;
+    const int rt = row >> 4, c = row & 15;
+    qv[it] = make_uint4(0, 0, 0, 0);
+    if (rt < rt_n) {
+      const int i = (rt % a.th) * 16 + c;
+      if (i < a.W) {
+        const int head = a.srh_head[off + rt / a.th];
+        qv[it] = load16(qb + (((int64_t)b * a.W + i) * a.Hq + head) * (int64_t)(D * sizeof(T)) +
+                        16 * u);
+      }
+    }
   }
 }
 
-// Load the slices of one key row (key index clamped into the sequence).
+template <typename T, int D, int RTM, int NT>
+__device__ __forceinline__ void q_store(const uint4 (&qv)[QStage<T, D, RTM, NT>::n],
+                                        uint4 *q_lds) {
+  constexpr int U4 = QLayout<T, D>::U4, STRIDE = QLayout<T, D>::STRIDE;
+#pragma unroll
+  for (int it = 0; it < QStage<T, D, RTM, NT>::n; ++it) {
+    const int idx = (int)threadIdx.x + it * NT;
+    const int row = idx / U4, u = idx - row * U4;
+    if (row < RTM * 16) q_lds[row * STRIDE + u] = qv[it];
+  }
+}
+
+template <typename T, int D>
+__device__ __forceinline__ uint4 q_frag(const uint4 *q_lds, int rt, int s, int c, int quad) {
+  return q_lds[(rt * 16 + c) * QLayout<T, D>::STRIDE + 4 * s + quad];
+}
+
+// Slices of one key row (key index clamped into the sequence).
 template <typename T, int D>
 __device__ __forceinline__ void load_k_row(const ScoreArgs &a, int s0, int key, int g, int quad,
                                            uint4 (&out)[Slices<T, D>::n]) {
@@ -50,115 +107,166 @@ __device__ __forceinline__ void load_k_row(const ScoreArgs &a, int s0, int key, 
   for (int s = 0; s < Slices<T, D>::n; ++s) out[s] = load16(p + 64 * s);
 }
 
+// logits of row tile rt against one key tile; KEYS_AS_A selects the operand
+// order (true: lane holds 4 keys of one row; false: 4 rows of one key).
+template <typename T, int D, int RTM, bool KEYS_AS_A>
+__device__ __forceinline__ f32x4 tile_logits(const uint4 (&kf)[Slices<T, D>::n],
+                                             const uint4 (&qreg)[RegTiles<T, D, RTM>::n]
+                                                                [Slices<T, D>::n],
+                                             const uint4 *q_lds, int rt, int c, int quad) {
+  constexpr int NS = Slices<T, D>::n, RQ = RegTiles<T, D, RTM>::v;
+  f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    uint4 qv;
+    if (rt < RQ) {
+      qv = qreg[rt < RQ ? rt : 0][s];   // rt < RQ here; the clamp only keeps the index static
+    } else {
+      qv = q_frag<T, D>(q_lds, rt, s, c, quad);
+    }
+    acc = KEYS_AS_A ? mfma_slice<T>(kf[s], qv, acc) : mfma_slice<T>(qv, kf[s], acc);
+  }
+  return acc;
+}
+
+// Fold one key tile (logits acc[rt], keys base + 4*quad + r) into the running
+// (ref, sum) pairs of this lane's rows.  Keys past the sequence end and, inside
+// the window, after the row's own position (causal) are masked.
+template <int RTM>
+__device__ __forceinline__ void stats_update(const ScoreArgs &a, const f32x4 (&acc)[RTM],
+                                             float (&ref)[RTM], float (&sum)[RTM], int rt_n,
+                                             int base, int L, int P, int c, int quad) {
+  constexpr float kRescale = 30.f;   // rebase the reference when a term would exceed 2^30
+  const bool masked_tile = (base + 16 > P);
+  float d[RTM][4];
+  float dmax = -INFINITY;
+#pragma unroll
+  for (int rt = 0; rt < RTM; ++rt) {
+    if (rt >= rt_n) continue;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float x = __builtin_fmaf(acc[rt][r], a.c1, -ref[rt]);
+      if (masked_tile) {
+        const int i = (rt % a.th) * 16 + c;   // window index of this lane's row
+        const int j = base + 4 * quad + r;
+        const bool ok = (j < L) && (i >= a.W || j <= P + i);
+        x = ok ? x : -INFINITY;
+      }
+      d[rt][r] = x;
+      dmax = fmaxf(dmax, x);
+    }
+  }
+  if (__any(dmax > kRescale)) {
+    // Rebase a row's reference on the largest new value when a term would
+    // exceed 2^kRescale (always the case for the first key of a row).
+#pragma unroll
+    for (int rt = 0; rt < RTM; ++rt) {
+      if (rt >= rt_n) continue;
+      const float m = fmaxf(fmaxf(d[rt][0], d[rt][1]), fmaxf(d[rt][2], d[rt][3]));
+      if (m > kRescale) {
+        float best = -INFINITY;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (d[rt][r] != -INFINITY) best = fmaxf(best, acc[rt][r] * a.c1);
+        sum[rt] = (ref[rt] == -INFINITY) ? 0.f : sum[rt] * fast_exp2(ref[rt] - best);
+        ref[rt] = best;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          d[rt][r] = (d[rt][r] == -INFINITY) ? -INFINITY
+                                             : __builtin_fmaf(acc[rt][r], a.c1, -best);
+      }
+    }
+  }
+#pragma unroll
+  for (int rt = 0; rt < RTM; ++rt) {
+    if (rt >= rt_n) continue;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) sum[rt] += fast_exp2(d[rt][r]);
+  }
+}
+
 // ---------------------------------------------------------------------------
-// S1+S2 partial statistics.  Grid (max_chunks1, Hkv, batch), 256 threads.
+// S1+S2 partial statistics.  Grid (Hkv, max_chunks1, batch), 512 threads: the
+// groups of one key chunk are neighbours in launch order, so the workgroups in
+// flight read whole token rows of K ([T, Hkv, D]) rather than 1/Hkv of each.
 // MFMA operands: A = 16 keys, B = 16 window rows, so lane (quad, c) holds the
 // logits of row c against keys 4*quad .. 4*quad+3 of the tile and keeps one
-// running (ref, sum) pair per row tile.
+// running (ref, sum) pair per row tile.  Wave w handles the key tiles
+// w, w + 8, w + 16, ... of the chunk (chunk1 / 128 of them).
 // ---------------------------------------------------------------------------
 template <typename T, int D, int RTM>
-__global__ __launch_bounds__(256) void stats_kernel(const ScoreArgs a) {
-  constexpr int NS = Slices<T, D>::n;
-  constexpr float kRescale = 30.f;   // rebase the reference when a term would exceed 2^30
-  const int chunk = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+__global__ __launch_bounds__(64 * kWaves) void stats_kernel(const ScoreArgs a) {
+  constexpr int NS = Slices<T, D>::n, RQ = RegTiles<T, D, RTM>::v;
+  constexpr int NT = 64 * kWaves;
+  const int g = blockIdx.x, chunk = blockIdx.y, b = blockIdx.z;
   const int s0 = a.cu[b];
   const int L = a.cu[b + 1] - s0;
+  if (chunk == 0) {   // the column-sum kernel accumulates this histogram afterwards
+    int *h = a.hist + ((int64_t)b * a.Hkv + g) * kHistBins;
+    for (int i = threadIdx.x; i < kHistBins; i += NT) h[i] = 0;
+  }
   const int c0 = chunk * a.chunk1;
   if (c0 >= L) return;                       // uniform for the whole workgroup
-  const int c_end = min(L, c0 + a.chunk1);
   const int P = L - a.W;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int c = lane & 15, quad = lane >> 4;
   const int off = a.srh_off[g];
   const int rt_n = (a.srh_off[g + 1] - off) * a.th;
+  const int n_groups = a.chunk1 / (16 * kWaves * kPair);   // 2-tile groups per wave
+  // key row of this lane for tile index i of this wave, clamped into the chunk
+  // (the pipeline's reads past the last tile hit the same cached row)
+  const int k_last = min(L, c0 + a.chunk1) - 1;
+  auto key_of = [&](int i) { return min(c0 + 16 * (wave + kWaves * i) + c, k_last); };
 
-  uint4 qf[RTM][NS];
+  __shared__ uint4 q_lds[RTM * 16 * QLayout<T, D>::STRIDE];
+  __shared__ float2 part[kWaves][RTM * 16];
+
+  // Query loads first, then the first two key groups; the queries are written
+  // to LDS while the keys are still in flight.
+  uint4 qv[QStage<T, D, RTM, NT>::n];
+  q_load<T, D, RTM, NT>(a, b, off, rt_n, qv);
+  uint4 ka[kPair][NS], kb[kPair][NS];
 #pragma unroll
-  for (int rt = 0; rt < RTM; ++rt) {
-    if (rt < rt_n) {
-      load_q_tile<T, D>(a, b, a.srh_head[off + rt / a.th], (rt % a.th) * 16, c, quad, qf[rt]);
-    } else {
+  for (int p = 0; p < kPair; ++p) load_k_row<T, D>(a, s0, key_of(p), g, quad, ka[p]);
 #pragma unroll
-      for (int s = 0; s < NS; ++s) qf[rt][s] = make_uint4(0, 0, 0, 0);
-    }
-  }
-  // row held by this lane in row tile rt: rt*16 + c; its window index:
+  for (int p = 0; p < kPair; ++p) load_k_row<T, D>(a, s0, key_of(kPair + p), g, quad, kb[p]);
+  q_store<T, D, RTM, NT>(qv, q_lds);
+  __syncthreads();
+  uint4 qreg[RegTiles<T, D, RTM>::n][NS];
+#pragma unroll
+  for (int rt = 0; rt < RQ; ++rt)
+#pragma unroll
+    for (int s = 0; s < NS; ++s) qreg[rt][s] = q_frag<T, D>(q_lds, rt, s, c, quad);
+
   float ref[RTM], sum[RTM];
 #pragma unroll
   for (int rt = 0; rt < RTM; ++rt) {
     ref[rt] = -INFINITY;
     sum[rt] = 0.f;
   }
-
-  const int ntiles = (c_end - c0 + 15) >> 4;
-  uint4 kcur[NS], knext[NS];
-  int t = wave;
-  if (t < ntiles) load_k_row<T, D>(a, s0, min(c0 + 16 * t + c, L - 1), g, quad, kcur);
-  for (; t < ntiles; t += 4) {
-    const int base = c0 + 16 * t;
-    if (t + 4 < ntiles) load_k_row<T, D>(a, s0, min(base + 64 + c, L - 1), g, quad, knext);
-    f32x4 acc[RTM];
+  auto consume = [&](uint4 (&kf)[kPair][NS], int grp) {
 #pragma unroll
-    for (int rt = 0; rt < RTM; ++rt) {
-      acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      if (rt < rt_n) {
+    for (int p = 0; p < kPair; ++p) {
+      const int base = c0 + 16 * (wave + kWaves * (kPair * grp + p));
+      f32x4 acc[RTM];
 #pragma unroll
-        for (int s = 0; s < NS; ++s) acc[rt] = mfma_slice<T>(kcur[s], qf[rt][s], acc[rt]);
-      }
+      for (int rt = 0; rt < RTM; ++rt)
+        if (rt < rt_n) acc[rt] = tile_logits<T, D, RTM, true>(kf[p], qreg, q_lds, rt, c, quad);
+      stats_update<RTM>(a, acc, ref, sum, rt_n, base, L, P, c, quad);
     }
-    // keys of this lane: base + 4*quad + r; masked past the sequence end and,
-    // inside the window, after the row's own position (causal).
-    const bool masked_tile = (base + 16 > P);
-    float d[RTM][4];
-    float dmax = -INFINITY;
+  };
+  for (int grp = 0; grp < n_groups; grp += 2) {
+    consume(ka, grp);
 #pragma unroll
-    for (int rt = 0; rt < RTM; ++rt) {
-      if (rt >= rt_n) continue;
-      const int i = (rt % a.th) * 16 + c;   // window index of this lane's row
+    for (int p = 0; p < kPair; ++p)
+      load_k_row<T, D>(a, s0, key_of(kPair * (grp + 2) + p), g, quad, ka[p]);
+    if (grp + 1 < n_groups) consume(kb, grp + 1);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        float x = __builtin_fmaf(acc[rt][r], a.c1, -ref[rt]);
-        if (masked_tile) {
-          const int j = base + 4 * quad + r;
-          const bool ok = (j < L) && (i >= a.W || j <= P + i);
-          x = ok ? x : -INFINITY;
-        }
-        d[rt][r] = x;
-        dmax = fmaxf(dmax, x);
-      }
-    }
-    if (__any(dmax > kRescale)) {
-      // Rebase a row's reference on the largest new value when a term would
-      // exceed 2^kRescale (always the case for the first key of a row).
-#pragma unroll
-      for (int rt = 0; rt < RTM; ++rt) {
-        if (rt >= rt_n) continue;
-        const float m = fmaxf(fmaxf(d[rt][0], d[rt][1]), fmaxf(d[rt][2], d[rt][3]));
-        if (m > kRescale) {
-          float best = -INFINITY;
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (d[rt][r] != -INFINITY) best = fmaxf(best, acc[rt][r] * a.c1);
-          sum[rt] = (ref[rt] == -INFINITY) ? 0.f : sum[rt] * fast_exp2(ref[rt] - best);
-          ref[rt] = best;
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            d[rt][r] = (d[rt][r] == -INFINITY) ? -INFINITY
-                                               : __builtin_fmaf(acc[rt][r], a.c1, -best);
-        }
-      }
-    }
-#pragma unroll
-    for (int rt = 0; rt < RTM; ++rt) {
-      if (rt >= rt_n) continue;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) sum[rt] += fast_exp2(d[rt][r]);
-    }
-#pragma unroll
-    for (int s = 0; s < NS; ++s) kcur[s] = knext[s];
+    for (int p = 0; p < kPair; ++p)
+      load_k_row<T, D>(a, s0, key_of(kPair * (grp + 3) + p), g, quad, kb[p]);
   }
 
-  // merge the four quads (same row c, different keys), then the four waves
+  // merge the four quads (same row c, different keys), then the waves
 #pragma unroll
   for (int rt = 0; rt < RTM; ++rt) {
 #pragma unroll
@@ -168,7 +276,6 @@ __global__ __launch_bounds__(256) void stats_kernel(const ScoreArgs a) {
       merge_stats(ref[rt], sum[rt], ro, so);
     }
   }
-  __shared__ float2 part[4][RTM * 16];
   if (quad == 0) {
 #pragma unroll
     for (int rt = 0; rt < RTM; ++rt) part[wave][rt * 16 + c] = make_float2(ref[rt], sum[rt]);
@@ -178,23 +285,25 @@ __global__ __launch_bounds__(256) void stats_kernel(const ScoreArgs a) {
   if (tid < rt_n * 16) {
     float r0 = part[0][tid].x, s_0 = part[0][tid].y;
 #pragma unroll
-    for (int w = 1; w < 4; ++w) merge_stats(r0, s_0, part[w][tid].x, part[w][tid].y);
+    for (int w = 1; w < kWaves; ++w) merge_stats(r0, s_0, part[w][tid].x, part[w][tid].y);
     a.stats[(((int64_t)b * a.Hkv + g) * a.max_chunks1 + chunk) * a.row_slots + tid] =
         make_float2(r0, s_0);
   }
 }
 
 // ---------------------------------------------------------------------------
-// S2+S3+S4.  Grid (max_chunks2, Hkv, batch), 256 threads.
+// S2+S3+S4.  Grid (Hkv, max_chunks2, batch), 512 threads.
 // MFMA operands: A = 16 window rows, B = 16 keys, so lane (quad, c) holds
-// rows 4*quad .. 4*quad+3 of the tile against key c.
+// rows 4*quad .. 4*quad+3 of the tile against key c.  The tiles of a chunk
+// plus one halo tile on each side, e = -1 .. chunk2/16, go to the waves
+// round-robin (chunk2 + 32 keys = 16 * kWaves * kPair * n_groups).
 // ---------------------------------------------------------------------------
 template <typename T, int D, int RTM>
-__global__ __launch_bounds__(256) void colsum_kernel(const ScoreArgs a) {
-  constexpr int NS = Slices<T, D>::n;
-  constexpr int kMaxChunk2 = 1024;
+__global__ __launch_bounds__(64 * kWaves) void colsum_kernel(const ScoreArgs a) {
+  constexpr int NS = Slices<T, D>::n, RQ = RegTiles<T, D, RTM>::v;
+  constexpr int NT = 64 * kWaves;
   constexpr int kMaxSrh = RTM;   // th >= 1
-  const int chunk = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  const int g = blockIdx.x, chunk = blockIdx.y, b = blockIdx.z;
   const int s0 = a.cu[b];
   const int L = a.cu[b + 1] - s0;
   const int c0 = chunk * a.chunk2;
@@ -210,39 +319,65 @@ __global__ __launch_bounds__(256) void colsum_kernel(const ScoreArgs a) {
   float *out = a.scores + (int64_t)g * a.T + s0;
 
   // Window positions of this chunk are always kept: +inf.
-  for (int j = max(c0, P) + tid; j < c_end; j += 256) out[j] = INFINITY;
+  for (int j = max(c0, P) + tid; j < c_end; j += NT) out[j] = INFINITY;
   if (c0 >= P) return;                        // no prefix key in this chunk
   const int p_end = min(c_end, P);
+  const int ntiles = (p_end - c0 + 15) >> 4;        // tiles e = 0 .. ntiles-1
+  const int e_lo = (c0 > 0) ? -1 : 0;               // left halo tile
+  const int e_hi = (c0 + 16 * ntiles < P) ? ntiles : ntiles - 1;   // right halo tile
+  const int n_groups = (a.chunk2 + 32) / (16 * kWaves * kPair);
+  // tile index e of this wave's i-th tile, and its key row for this lane
+  auto tile_of = [&](int i) { return -1 + wave + kWaves * i; };
+  const int k_first = max(c0 - 16, 0), k_last = min(c0 + a.chunk2 + 16, L) - 1;
+  auto key_of = [&](int i) { return min(max(c0 + 16 * tile_of(i) + c, k_first), k_last); };
 
-  // Row normalisers: bias = ref + log2(sum) over all chunks of the statistics pass.
+  __shared__ uint4 q_lds[RTM * 16 * QLayout<T, D>::STRIDE];
   __shared__ float bias_s[RTM * 16];
-  if (tid < rt_n * 16) {
-    const int nc1 = (L + a.chunk1 - 1) / a.chunk1;
-    const float2 *st = a.stats + ((int64_t)b * a.Hkv + g) * a.max_chunks1 * a.row_slots + tid;
-    float m = -INFINITY;
-    for (int k = 0; k < nc1; ++k) m = fmaxf(m, st[(int64_t)k * a.row_slots].x);
-    float sm = 0.f;
-    for (int k = 0; k < nc1; ++k) {
-      float2 v = st[(int64_t)k * a.row_slots];
-      sm += v.y * fast_exp2(v.x - m);
-    }
-    const int i = (tid % (16 * a.th));
-    bias_s[tid] = (i < a.W) ? m + fast_log2(sm) : INFINITY;
-  } else if (tid < RTM * 16) {
-    bias_s[tid] = INFINITY;
-  }
+  __shared__ float cs[kMaxSrh][kMaxChunk2 + 32];
+  __shared__ int hist_s[kHistBins];
+  uint4 qv[QStage<T, D, RTM, NT>::n];
+  q_load<T, D, RTM, NT>(a, b, off, rt_n, qv);
+  uint4 ka[kPair][NS], kb[kPair][NS];
+#pragma unroll
+  for (int p = 0; p < kPair; ++p) load_k_row<T, D>(a, s0, key_of(p), g, quad, ka[p]);
+#pragma unroll
+  for (int p = 0; p < kPair; ++p) load_k_row<T, D>(a, s0, key_of(kPair + p), g, quad, kb[p]);
+  q_store<T, D, RTM, NT>(qv, q_lds);
+  for (int i = tid; i < kHistBins; i += NT) hist_s[i] = 0;
 
-  uint4 qf[RTM][NS];
-#pragma unroll
-  for (int rt = 0; rt < RTM; ++rt) {
-    if (rt < rt_n) {
-      load_q_tile<T, D>(a, b, a.srh_head[off + rt / a.th], (rt % a.th) * 16, c, quad, qf[rt]);
-    } else {
-#pragma unroll
-      for (int s = 0; s < NS; ++s) qf[rt][s] = make_uint4(0, 0, 0, 0);
+  // Row normalisers bias = ref + log2(sum), merged over every chunk of the
+  // statistics pass: tpr threads per row, fixed order, then a shuffle tree.
+  {
+    const int rows = rt_n * 16;
+    const int nc1 = (L + a.chunk1 - 1) / a.chunk1;
+    int tpr = 1;
+    while (tpr * 2 * rows <= NT && tpr < 32) tpr *= 2;
+    const int row = tid / tpr, sub = tid % tpr;
+    float m = -INFINITY, sm = 0.f;
+    if (row < rows) {
+      const float2 *st =
+          a.stats + ((int64_t)b * a.Hkv + g) * a.max_chunks1 * a.row_slots + row;
+      for (int k = sub; k < nc1; k += tpr) {
+        const float2 v = st[(int64_t)k * a.row_slots];
+        merge_stats(m, sm, v.x, v.y);
+      }
     }
+    for (int o = 1; o < tpr; o <<= 1) {
+      const float mo = __shfl_xor(m, o), so = __shfl_xor(sm, o);
+      merge_stats(m, sm, mo, so);
+    }
+    if (row < rows && sub == 0) {
+      const int i = row % (16 * a.th);
+      bias_s[row] = (i < a.W) ? m + fast_log2(sm) : INFINITY;
+    }
+    for (int r = rows + tid; r < RTM * 16; r += NT) bias_s[r] = INFINITY;
   }
   __syncthreads();
+  uint4 qreg[RegTiles<T, D, RTM>::n][NS];
+#pragma unroll
+  for (int rt = 0; rt < RQ; ++rt)
+#pragma unroll
+    for (int s = 0; s < NS; ++s) qreg[rt][s] = q_frag<T, D>(q_lds, rt, s, c, quad);
   float bias[RTM][4];
 #pragma unroll
   for (int rt = 0; rt < RTM; ++rt)
@@ -251,49 +386,50 @@ __global__ __launch_bounds__(256) void colsum_kernel(const ScoreArgs a) {
 
   // Column sums of the chunk plus one 16-key halo tile on each side.
   // cs[h][16 + x] holds the window sum of SRH h at key c0 + x.
-  __shared__ float cs[kMaxSrh][kMaxChunk2 + 32];
-  const int ntiles = (p_end - c0 + 15) >> 4;        // tiles e = 0 .. ntiles-1
-  const int e_lo = (c0 > 0) ? -1 : 0;
-  const int e_hi = (c0 + 16 * ntiles < P) ? ntiles : ntiles - 1;
-  for (int e = e_lo + wave; e <= e_hi; e += 4) {
-    const int base = c0 + 16 * e;
-    uint4 kf[NS];
-    load_k_row<T, D>(a, s0, min(base + c, L - 1), g, quad, kf);
-    f32x4 acc[RTM];
+  auto consume = [&](uint4 (&kf)[kPair][NS], int grp) {
 #pragma unroll
-    for (int rt = 0; rt < RTM; ++rt) {
-      acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      if (rt < rt_n) {
+    for (int p = 0; p < kPair; ++p) {
+      const int e = tile_of(kPair * grp + p);
+      const bool keep = (e >= e_lo && e <= e_hi);
+      // Sum the normalised probabilities over the window rows of each SRH:
+      // in-lane over the 4 rows and the SRH's row tiles, then across the quads.
+      int hh = 0;
+      float v = 0.f;
 #pragma unroll
-        for (int s = 0; s < NS; ++s) acc[rt] = mfma_slice<T>(qf[rt][s], kf[s], acc[rt]);
+      for (int rt = 0; rt < RTM; ++rt) {
+        if (rt >= rt_n) continue;
+        const f32x4 acc = tile_logits<T, D, RTM, false>(kf[p], qreg, q_lds, rt, c, quad);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v += fast_exp2(__builtin_fmaf(acc[r], a.c1, -bias[rt][r]));
+        if ((a.head_end_mask >> rt) & 1u) {
+          v += __shfl_xor(v, 16);
+          v += __shfl_xor(v, 32);
+          if (keep && quad == (hh & 3)) cs[hh][16 + 16 * e + c] = v;
+          v = 0.f;
+          ++hh;
+        }
       }
     }
-    // Sum the normalised probabilities over the window rows of each SRH:
-    // in-lane over the 4 rows and the SRH's row tiles, then across the quads.
-    int hh = 0;
-    float v = 0.f;
+  };
+  for (int grp = 0; grp < n_groups; grp += 2) {
+    consume(ka, grp);
 #pragma unroll
-    for (int rt = 0; rt < RTM; ++rt) {
-      if (rt >= rt_n) continue;
+    for (int p = 0; p < kPair; ++p)
+      load_k_row<T, D>(a, s0, key_of(kPair * (grp + 2) + p), g, quad, ka[p]);
+    if (grp + 1 < n_groups) consume(kb, grp + 1);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) v += fast_exp2(__builtin_fmaf(acc[rt][r], a.c1, -bias[rt][r]));
-      if ((a.head_end_mask >> rt) & 1u) {
-        v += __shfl_xor(v, 16);
-        v += __shfl_xor(v, 32);
-        if (quad == (hh & 3)) cs[hh][16 + 16 * e + c] = v;
-        v = 0.f;
-        ++hh;
-      }
-    }
+    for (int p = 0; p < kPair; ++p)
+      load_k_row<T, D>(a, s0, key_of(kPair * (grp + 3) + p), g, quad, kb[p]);
   }
   __syncthreads();
 
   // Pooling along the token axis (positions clipped to the prefix [0, P)),
-  // then the mean over the group's SRHs.
+  // then the mean over the group's SRHs; each score also lands in the
+  // histogram of its top 11 value bits.
   const int rp = (a.pool_kernel - 1) >> 1;
   const float inv_k = 1.f / (float)a.pool_kernel;
   const float inv_n = 1.f / (float)nh;
-  for (int j = c0 + tid; j < p_end; j += 256) {
+  for (int j = c0 + tid; j < p_end; j += NT) {
     const int lo = max(j - rp, 0) - c0 + 16;
     const int hi = min(j + rp, P - 1) - c0 + 16;
     float score;
@@ -331,6 +467,13 @@ __global__ __launch_bounds__(256) void colsum_kernel(const ScoreArgs a) {
       }
     }
     out[j] = score;
+    atomicAdd(&hist_s[hist_bin(__float_as_uint(score))], 1);
+  }
+  __syncthreads();
+  int *hg = a.hist + ((int64_t)b * a.Hkv + g) * kHistBins;
+  for (int i = tid; i < kHistBins; i += NT) {
+    const int n = hist_s[i];
+    if (n) atomicAdd(&hg[i], n);
   }
 }
 
@@ -339,22 +482,29 @@ __global__ __launch_bounds__(256) void colsum_kernel(const ScoreArgs a) {
 // ---------------------------------------------------------------------------
 template <typename T, int D, int RTM>
 static hipError_t launch_score_t(const ScoreArgs &a, int batch, hipStream_t stream) {
-  dim3 block(256);
-  hipLaunchKernelGGL((stats_kernel<T, D, RTM>), dim3(a.max_chunks1, a.Hkv, batch), block, 0,
+  dim3 block(64 * kWaves);
+  hipLaunchKernelGGL((stats_kernel<T, D, RTM>), dim3(a.Hkv, a.max_chunks1, batch), block, 0,
                      stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((colsum_kernel<T, D, RTM>), dim3(a.max_chunks2, a.Hkv, batch), block, 0,
+  hipLaunchKernelGGL((colsum_kernel<T, D, RTM>), dim3(a.Hkv, a.max_chunks2, batch), block, 0,
                      stream, a);
   return hipGetLastError();
 }
 
 template <typename T, int D>
 static hipError_t launch_score_d(const ScoreArgs &a, int rt_max, int batch, hipStream_t stream) {
-  if (rt_max <= 2) return launch_score_t<T, D, 2>(a, batch, stream);
-  if (rt_max <= 4) return launch_score_t<T, D, 4>(a, batch, stream);
-  if (rt_max <= 8) return launch_score_t<T, D, 8>(a, batch, stream);
-  return launch_score_t<T, D, 12>(a, batch, stream);
+  switch (rt_max) {
+    case 1: return launch_score_t<T, D, 1>(a, batch, stream);
+    case 2: return launch_score_t<T, D, 2>(a, batch, stream);
+    case 3: return launch_score_t<T, D, 3>(a, batch, stream);
+    case 4: return launch_score_t<T, D, 4>(a, batch, stream);
+    case 5:
+    case 6: return launch_score_t<T, D, 6>(a, batch, stream);
+    case 7:
+    case 8: return launch_score_t<T, D, 8>(a, batch, stream);
+    default: return launch_score_t<T, D, 12>(a, batch, stream);
+  }
 }
 
 hipError_t launch_score(const ScoreArgs &a, int dtype_bf16, int head_dim, int rt_max, int batch,

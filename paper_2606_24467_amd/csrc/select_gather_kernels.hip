@@ -1,13 +1,14 @@
-// Selection (S5) and eviction gather (S6) kernels of the CompressKV path.
-//
 // S5 keeps, per (sequence, KV group), the (budget - W) highest prefix scores
 // (section 3.3: the N best tokens keep their KV pairs) with ties going to the
 // lowest position, plus the W window positions, written in ascending order.
 // Scores are non-negative floats, so their bit patterns order like unsigned
-// integers: a three-digit radix select (11 + 11 + 10 bits) over LDS
-// histograms finds the exact bit pattern of the k-th largest score, and an
-// ordered compaction writes the kept positions.  Integer work only, so the
-// result does not depend on scheduling.
+// integers.  A three-digit radix select finds the exact bit pattern of the
+// k-th largest score: digit 1 (bits 30..20) comes from the histogram that the
+// column-sum kernel accumulated (or is counted here), the elements of the
+// chosen bucket are collected in LDS, and digits 2 (bits 19..9) and 3 (bits
+// 8..0) are resolved on that candidate list.  An ordered compaction then
+// writes the kept positions.  Integer work only, so the result does not
+// depend on scheduling.
 //
 // S6 copies the kept K and V rows (section 3.3: the retained KV pairs form the
 // compressed cache) with 16-byte lanes; rows whose index is -1 become zeros.
@@ -16,9 +17,12 @@
 namespace ckv {
 
 constexpr int kSelThreads = 1024;
+constexpr int kCandCap = 4096;               // candidates of the first-digit bucket kept in LDS
+constexpr int kEpt = 32;                     // scores per thread held in registers per round
+constexpr int kRound = kSelThreads * kEpt;   // scores per round
 
-// Inclusive prefix sum over the 1024 threads of the block.
-__device__ __forceinline__ int block_inclusive_scan(int x, int *lds_waves) {
+// Inclusive prefix sum over the 1024 threads of the block; *total gets the sum.
+__device__ __forceinline__ int block_inclusive_scan(int x, int *lds_waves, int *total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
@@ -38,8 +42,56 @@ __device__ __forceinline__ int block_inclusive_scan(int x, int *lds_waves) {
   }
   __syncthreads();
   const int before = (wave > 0) ? lds_waves[wave - 1] : 0;
+  *total = lds_waves[kSelThreads / 64 - 1];
   __syncthreads();   // lds_waves is reused by the next scan
   return x + before;
+}
+
+// LDS histogram increment; a wave whose active lanes share one bin issues a
+// single atomic (plateaus of equal scores are common after max pooling).
+// Must be reached by every lane of the wave.
+__device__ __forceinline__ void hist_add(int *h, int bin, bool active) {
+  const unsigned long long m = __ballot(active);
+  if (m == 0ull) return;
+  const int leader = __ffsll((unsigned long long)m) - 1;
+  const int first = __shfl(bin, leader);
+  if (__all(!active || bin == first)) {
+    if ((int)(threadIdx.x & 63) == leader) atomicAdd(&h[first], (int)__popcll(m));
+  } else if (active) {
+    atomicAdd(&h[bin], 1);
+  }
+}
+
+// Bucket of an nb-bin histogram (nb <= 2048) that holds the element of rank
+// `remain` counted from the top; writes the bucket and the rank inside it.
+__device__ __forceinline__ void find_bucket(const int *hist, int nb, int remain, int *scan_tmp,
+                                            int *bucket_out, int *remain_out) {
+  const int tid = threadIdx.x;
+  const int hi_b = nb - 1 - 2 * tid;     // thread t owns buckets nb-1-2t and nb-2-2t
+  const int c_hi = (hi_b >= 0) ? hist[hi_b] : 0;
+  const int c_lo = (hi_b - 1 >= 0) ? hist[hi_b - 1] : 0;
+  int total;
+  const int incl = block_inclusive_scan(c_hi + c_lo, scan_tmp, &total);
+  const int excl = incl - c_hi - c_lo;   // elements in buckets above hi_b
+  if (hi_b >= 0) {
+    if (excl < remain && remain <= excl + c_hi) {
+      *bucket_out = hi_b;
+      *remain_out = remain - excl;
+    } else if (hi_b - 1 >= 0 && excl + c_hi < remain && remain <= excl + c_hi + c_lo) {
+      *bucket_out = hi_b - 1;
+      *remain_out = remain - excl - c_hi;
+    }
+  }
+  __syncthreads();
+}
+
+// Scores [r0 + t*kEpt, r0 + (t+1)*kEpt) of thread t into registers (all loads
+// issued together); positions >= P read as 0 and are masked by the callers.
+__device__ __forceinline__ void load_round(const uint32_t *sc, int P, int r0,
+                                           uint32_t (&v)[kEpt]) {
+  const int j0 = r0 + (int)threadIdx.x * kEpt;
+#pragma unroll
+  for (int e = 0; e < kEpt; ++e) v[e] = (j0 + e < P) ? sc[j0 + e] : 0u;
 }
 
 // Grid (Hkv, batch), 1024 threads.
@@ -58,71 +110,125 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a)
   for (int w = tid; w < a.W; w += kSelThreads) out[k + w] = P + w;
   if (k == 0) return;
   const uint32_t *sc = reinterpret_cast<const uint32_t *>(a.scores + (int64_t)g * a.T + s0);
+  const int nrounds = (P + kRound - 1) / kRound;
+  const bool resident = (nrounds == 1);   // scores stay in registers for every pass
 
-  __shared__ int hist[2048];
+  __shared__ int hist[kHistBins];
   __shared__ int scan_tmp[kSelThreads / 64];
-  __shared__ int bucket_s, remain_s;
-  uint32_t prefix = 0, pmask = 0;
-  int remain = k;                   // rank of the target inside the current prefix
-  const int shifts[3] = {21, 10, 0};
-  const int widths[3] = {11, 11, 10};
-  for (int pass = 0; pass < 3; ++pass) {
+  __shared__ int bucket_s, remain_s, ncand_s;
+  __shared__ uint32_t cand_u[kCandCap];
+  __shared__ int cand_j[kCandCap];
+
+  uint32_t v[kEpt];
+  if (resident) load_round(sc, P, 0, v);
+
+  // Digit 1: bits 30..20.
+  if (a.hist) {
+    const int *hg = a.hist + ((int64_t)b * a.Hkv + g) * kHistBins;
+    for (int i = tid; i < kHistBins; i += kSelThreads) hist[i] = hg[i];
+  } else {
+    for (int i = tid; i < kHistBins; i += kSelThreads) hist[i] = 0;
+    __syncthreads();
+    for (int r = 0; r < nrounds; ++r) {
+      if (!resident) load_round(sc, P, r * kRound, v);
+      const int j0 = r * kRound + tid * kEpt;
+#pragma unroll
+      for (int e = 0; e < kEpt; ++e) hist_add(hist, hist_bin(v[e]), j0 + e < P);
+    }
+  }
+  if (tid == 0) ncand_s = 0;
+  __syncthreads();
+  find_bucket(hist, kHistBins, k, scan_tmp, &bucket_s, &remain_s);
+  uint32_t pmask = 0x7FFu << 20;
+  uint32_t prefix = (uint32_t)bucket_s << 20;
+  int remain = remain_s;
+
+  // Candidates: prefix elements whose first digit equals the chosen bucket.
+  for (int r = 0; r < nrounds; ++r) {
+    if (!resident) load_round(sc, P, r * kRound, v);
+    const int j0 = r * kRound + tid * kEpt;
+#pragma unroll
+    for (int e = 0; e < kEpt; ++e) {
+      if (j0 + e < P && (v[e] & pmask) == prefix) {
+        const int slot = atomicAdd(&ncand_s, 1);
+        if (slot < kCandCap) {
+          cand_u[slot] = v[e];
+          cand_j[slot] = j0 + e;
+        }
+      }
+    }
+  }
+  __syncthreads();
+  const int nc = ncand_s;
+  const bool in_lds = nc <= kCandCap;
+
+  // Digits 2 (bits 19..9) and 3 (bits 8..0) on the candidates (or, if they
+  // overflow the LDS list, on every prefix element that matches so far).
+  const int shifts[2] = {9, 0};
+  const int widths[2] = {11, 9};
+  for (int pass = 0; pass < 2; ++pass) {
     const int sh = shifts[pass];
     const uint32_t dmask = (1u << widths[pass]) - 1u;
-    const int nb = 1 << widths[pass];
-    for (int i = tid; i < 2048; i += kSelThreads) hist[i] = 0;
+    for (int i = tid; i < kHistBins; i += kSelThreads) hist[i] = 0;
     __syncthreads();
-    for (int j = tid; j < P; j += kSelThreads) {
-      const uint32_t u = sc[j];
-      if ((u & pmask) == prefix) atomicAdd(&hist[(u >> sh) & dmask], 1);
-    }
-    __syncthreads();
-    // Counts from the top bucket down: thread t owns buckets nb-1-2t and nb-2-2t.
-    const int hi_b = nb - 1 - 2 * tid;
-    int c_hi = 0, c_lo = 0;
-    if (hi_b >= 0) c_hi = hist[hi_b];
-    if (hi_b - 1 >= 0) c_lo = hist[hi_b - 1];
-    const int incl = block_inclusive_scan(c_hi + c_lo, scan_tmp);
-    const int excl = incl - c_hi - c_lo;   // elements in buckets above hi_b
-    if (hi_b >= 0) {
-      if (excl < remain && remain <= excl + c_hi) {
-        bucket_s = hi_b;
-        remain_s = remain - excl;
-      } else if (hi_b - 1 >= 0 && excl + c_hi < remain && remain <= excl + c_hi + c_lo) {
-        bucket_s = hi_b - 1;
-        remain_s = remain - excl - c_hi;
+    if (in_lds) {
+      for (int base = 0; base < nc; base += kSelThreads) {
+        const int i = base + tid;
+        const uint32_t u = (i < nc) ? cand_u[i] : 0u;
+        hist_add(hist, (int)((u >> sh) & dmask), i < nc && (u & pmask) == prefix);
+      }
+    } else {
+      for (int r = 0; r < nrounds; ++r) {
+        if (!resident) load_round(sc, P, r * kRound, v);
+        const int j0 = r * kRound + tid * kEpt;
+#pragma unroll
+        for (int e = 0; e < kEpt; ++e)
+          hist_add(hist, (int)((v[e] >> sh) & dmask), j0 + e < P && (v[e] & pmask) == prefix);
       }
     }
     __syncthreads();
+    find_bucket(hist, 1 << widths[pass], remain, scan_tmp, &bucket_s, &remain_s);
     prefix |= (uint32_t)bucket_s << sh;
     pmask |= dmask << sh;
     remain = remain_s;
     __syncthreads();
   }
+
   // prefix is the exact bit pattern of the k-th largest score; `remain` of the
   // positions holding it are kept (the lowest ones), plus every larger score.
+  // Ordered compaction, round by round: thread t owns a contiguous run.
   const uint32_t thr = prefix;
-  const int ept = (P + kSelThreads - 1) / kSelThreads;
-  const int j0 = min(P, tid * ept), j1 = min(P, j0 + ept);
-  int n_gt = 0, n_eq = 0;
-  for (int j = j0; j < j1; ++j) {
-    const uint32_t u = sc[j];
-    n_gt += (u > thr);
-    n_eq += (u == thr);
-  }
-  const int eq_before = block_inclusive_scan(n_eq, scan_tmp) - n_eq;
-  const int take_eq = max(0, min(n_eq, remain - eq_before));
-  const int n_sel = n_gt + take_eq;
-  int pos = block_inclusive_scan(n_sel, scan_tmp) - n_sel;
-  int eq_left = take_eq;
-  for (int j = j0; j < j1; ++j) {
-    const uint32_t u = sc[j];
-    bool keep = (u > thr);
-    if (u == thr && eq_left > 0) {
-      keep = true;
-      --eq_left;
+  int pos_base = 0, eq_base = 0;
+  for (int r = 0; r < nrounds; ++r) {
+    if (!resident) load_round(sc, P, r * kRound, v);
+    const int j0 = r * kRound + tid * kEpt;
+    int n_gt = 0, n_eq = 0;
+#pragma unroll
+    for (int e = 0; e < kEpt; ++e) {
+      const uint32_t u = v[e] & 0x7FFFFFFFu;
+      const bool ok = j0 + e < P;
+      n_gt += ok && (u > thr);
+      n_eq += ok && (u == thr);
     }
-    if (keep && pos < k) out[pos++] = j;   // bound holds for finite scores; guards NaN input
+    int eq_total, sel_total;
+    const int eq_before = eq_base + block_inclusive_scan(n_eq, scan_tmp, &eq_total) - n_eq;
+    const int take_eq = max(0, min(n_eq, remain - eq_before));
+    const int n_sel = n_gt + take_eq;
+    int pos = pos_base + block_inclusive_scan(n_sel, scan_tmp, &sel_total) - n_sel;
+    int eq_left = take_eq;
+#pragma unroll
+    for (int e = 0; e < kEpt; ++e) {
+      const uint32_t u = v[e] & 0x7FFFFFFFu;
+      const bool ok = j0 + e < P;
+      bool keep = ok && (u > thr);
+      if (ok && u == thr && eq_left > 0) {
+        keep = true;
+        --eq_left;
+      }
+      if (keep && pos < k) out[pos++] = j0 + e;   // bound holds for finite scores; guards NaN
+    }
+    eq_base += eq_total;
+    pos_base += sel_total;
   }
 }
 
@@ -137,10 +243,9 @@ __global__ __launch_bounds__(256) void gather_kernel(const GatherArgs a) {
   const int s0 = a.cu[b];
   const int L = a.cu[b + 1] - s0;
   const int64_t obase = ((int64_t)b * a.Hkv + g) * a.budget;
-  const int r_first = blockIdx.x * 4 * rows_per_pass;
-  for (int p = 0; p < 4; ++p) {
-    const int r = r_first + p * rows_per_pass + r_in;
-    if (r >= a.budget) break;
+  {
+    const int r = blockIdx.x * rows_per_pass + r_in;
+    if (r >= a.budget) return;
     const int j = a.idx[obase + r];
     uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
     if (j >= 0 && j < L) {   // anything else is a dropped slot: zeros
@@ -161,7 +266,7 @@ hipError_t launch_select(const SelectArgs &a, int batch, hipStream_t stream) {
 }
 
 hipError_t launch_gather(const GatherArgs &a, int batch, hipStream_t stream) {
-  const int rows_per_block = 4 * (256 / (a.row_bytes >> 4));
+  const int rows_per_block = 256 / (a.row_bytes >> 4);
   const int nblk = (a.budget + rows_per_block - 1) / rows_per_block;
   hipLaunchKernelGGL(gather_kernel, dim3(nblk, a.Hkv, batch), dim3(256), 0, stream, a);
   return hipGetLastError();
