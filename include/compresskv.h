@@ -131,6 +131,17 @@ int compresskv_compress_layer(const ckv_problem *p, const void *q_win, const voi
                               int32_t *idx, void *k_out, void *v_out, float *scores_or_null,
                               void *ws, size_t ws_bytes, void *stream);
 
+/*
+ * Which scoring implementation compresskv_score / _compress_layer will use for
+ * this problem: 2 = two passes over K (the default), 1 = single pass (each key
+ * read once from HBM), used when the environment variable CKV_PATH=single is
+ * set and the problem allows it (the units of every (sequence, group), 256
+ * keys each, fit in half of the workgroups the device can hold at once, and
+ * batch <= 64).  Negative on invalid arguments.  Queries the device
+ * (occupancy), so it needs a GPU.
+ */
+int compresskv_scoring_path(const ckv_problem *p, const uint8_t *srh_mask_host);
+
 /* Static text of a status code. */
 const char *compresskv_status_string(int status);
 

@@ -76,6 +76,8 @@ def lib() -> ctypes.CDLL:
     for f in ("compresskv_score", "compresskv_select", "compresskv_gather",
               "compresskv_compress_layer"):
         getattr(L, f).restype = ctypes.c_int
+    L.compresskv_scoring_path.argtypes = [P, u8p]
+    L.compresskv_scoring_path.restype = ctypes.c_int
     L.compresskv_status_string.argtypes = [ctypes.c_int]
     L.compresskv_status_string.restype = ctypes.c_char_p
     L.compresskv_last_error.argtypes = []
@@ -202,6 +204,15 @@ def compresskv_compress_layer(p: Problem, q_win, k, v, srh_mask, budget: int, id
         ctypes.byref(p.c), _ptr(q_win), _ptr(k), _ptr(v), m.ctypes.data, int(budget), _ptr(idx),
         _ptr(k_out), _ptr(v_out), _ptr(scores_or_null), _ptr(ws),
         ws.numel() if ws is not None else 0, _stream(stream)))
+
+
+def compresskv_scoring_path(p: Problem, srh_mask) -> int:
+    """1 = single-pass scoring kernel, 2 = two passes over K."""
+    m = _mask(srh_mask)
+    r = lib().compresskv_scoring_path(ctypes.byref(p.c), m.ctypes.data)
+    if r < 0:
+        raise CompressKVError("compresskv_scoring_path", -r)
+    return r
 
 
 # ------------------------------------------------------ tensor conveniences

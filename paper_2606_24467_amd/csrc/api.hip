@@ -44,10 +44,15 @@ struct Plan {
   int rt_max = 0;      // max row tiles of a group
   int chunk1 = 0, max_chunks1 = 0;
   int chunk2 = 0, max_chunks2 = 0;
-  size_t scores_off = 0, stats_off = 0, hist_off = 0, total = 0;
+  size_t scores_off = 0, stats_off = 0, counters_off = 0, hist_off = 0, total = 0;
+  bool fused = false;      // single-pass scoring kernel
+  int unit_tiles = 4;      // its key tiles per wave per unit
+  int n_units_max = 0;     // its units per (sequence, group), largest
+  int n_counters = 0;      // ints zeroed before it (ticket, fallbacks, arrivals, histograms)
   std::vector<uint16_t> srh_off;
   std::vector<uint8_t> srh_head;
   uint32_t head_end_mask = 0;
+  int max_parts = 0;       // partial-statistics slots per group in the workspace
 };
 
 int env_int(const char *name, int dflt) {
@@ -152,13 +157,43 @@ int check_mask(const ckv_problem *p, const uint8_t *mask, Plan &pl) {
   return CKV_OK;
 }
 
-void make_plan(const ckv_problem *p, Plan &pl) {
+// Keys per fused unit: 16 keys x 4 waves x unit_tiles.
+int fused_units(int L, int unit_tiles) { return (L + 64 * unit_tiles - 1) / (64 * unit_tiles); }
+
+// The two-kernel path is the default.  CKV_PATH=single selects the
+// single-pass kernel where it applies: every group's units must fit in half of
+// the workgroups that can be resident at once (its progress condition is that
+// one group per concurrently running launch fits; the margin covers two
+// launches on different streams) and the batch must fit its ticket table.
+void choose_path(const ckv_problem *p, Plan &pl) {
+  pl.fused = false;
+  const char *path = std::getenv("CKV_PATH");
+  if (!path || std::string(path) != "single") return;
+  if (p->batch > ckv::kFusedMaxBatch) return;
+  for (int ut : {4, 2}) {
+    const int resident = ckv::fused_resident_workgroups(p->dtype == CKV_BF16, p->head_dim,
+                                                        pl.rt_max, ut);
+    if (resident <= 0) continue;
+    int nmax = 0;
+    for (int b = 0; b < p->batch; ++b)
+      nmax = std::max(nmax, fused_units(p->cu_seqlens_host[b + 1] - p->cu_seqlens_host[b], ut));
+    if (2 * nmax <= resident) {
+      pl.fused = true;
+      pl.unit_tiles = ut;
+      pl.n_units_max = nmax;
+      return;
+    }
+  }
+}
+
+void make_plan(const ckv_problem *p, Plan &pl, bool decide_path) {
   pl.T = p->cu_seqlens_host[p->batch];
   pl.lmax = 0;
   for (int b = 0; b < p->batch; ++b)
     pl.lmax = std::max(pl.lmax, p->cu_seqlens_host[b + 1] - p->cu_seqlens_host[b]);
-  // Keys per workgroup: multiples of 512 (stats: 8 waves x 2-tile groups, at
-  // least two groups per wave) and 992 + 32 halo keys (column sums).
+  // Keys per workgroup of the two-kernel path: multiples of 512 (statistics:
+  // 8 waves x 2-tile groups, at least two groups per wave) and 992 + 32 halo
+  // keys (column sums).
   int c1 = env_int("CKV_CHUNK1", 0), c2 = env_int("CKV_CHUNK2", 0);
   if (c1 <= 0 || c1 % 512 != 0) c1 = pick_chunk(p, 512, 4096, 256);
   if (c2 <= 0 || (c2 + 32) % 256 != 0 || c2 > ckv::kMaxChunk2) c2 = 992;
@@ -166,13 +201,22 @@ void make_plan(const ckv_problem *p, Plan &pl) {
   pl.chunk2 = c2;
   pl.max_chunks1 = std::max(1, (pl.lmax + c1 - 1) / c1);
   pl.max_chunks2 = std::max(1, (pl.lmax + c2 - 1) / c2);
+  if (decide_path) choose_path(p, pl);
+  // partial row statistics: enough slots for either path's chunking, plus one
+  // per group for the published normalisers of the single-pass kernel
+  int parts = pl.max_chunks1;
+  for (int ut : {2, 4}) parts = std::max(parts, fused_units(pl.lmax, ut) + 1);
+  const size_t groups = (size_t)p->batch * p->n_kv_heads;
   pl.scores_off = 0;
   pl.stats_off = round_up((size_t)p->n_kv_heads * pl.T * sizeof(float), 256);
-  pl.hist_off = pl.stats_off + round_up((size_t)p->batch * p->n_kv_heads * pl.max_chunks1 *
-                                            (size_t)pl.rt_max * 16 * sizeof(float2),
-                                        256);
-  pl.total = pl.hist_off +
-             round_up((size_t)p->batch * p->n_kv_heads * ckv::kHistBins * sizeof(int), 256);
+  pl.counters_off = pl.stats_off +
+                    round_up(groups * parts * (size_t)pl.rt_max * 16 * sizeof(float2), 256);
+  // counters block: [0] ticket, [1] fallbacks, [64 ..) arrivals, ready flags,
+  // then the histograms
+  pl.hist_off = pl.counters_off + round_up((64 + 2 * groups) * sizeof(int), 256);
+  pl.n_counters = (int)((pl.hist_off - pl.counters_off) / sizeof(int) + groups * ckv::kHistBins);
+  pl.total = pl.hist_off + round_up(groups * ckv::kHistBins * sizeof(int), 256);
+  pl.max_parts = parts;
 }
 
 ckv::ScoreArgs score_args(const ckv_problem *p, const Plan &pl, const void *q, const void *k,
@@ -194,7 +238,7 @@ ckv::ScoreArgs score_args(const ckv_problem *p, const Plan &pl, const void *q, c
   a.th = pl.th;
   a.row_slots = pl.rt_max * 16;
   a.chunk1 = pl.chunk1;
-  a.max_chunks1 = pl.max_chunks1;
+  a.max_chunks1 = pl.max_parts;   // stride (in partials) between groups
   a.chunk2 = pl.chunk2;
   a.max_chunks2 = pl.max_chunks2;
   const double scale = p->scale > 0.f ? (double)p->scale : 1.0 / std::sqrt((double)p->head_dim);
@@ -270,6 +314,32 @@ ckv::GatherArgs gather_args(const ckv_problem *p, const void *k, const void *v, 
   return g;
 }
 
+// S1-S4 on the path the plan chose.
+hipError_t launch_scoring(const ckv_problem *p, const Plan &pl, const void *q, const void *k,
+                          float *scores, void *ws, hipStream_t stream) {
+  ckv::ScoreArgs a = score_args(p, pl, q, k, scores, ws);
+  if (!pl.fused)
+    return ckv::launch_score(a, p->dtype == CKV_BF16, p->head_dim, pl.rt_max, p->batch, stream);
+  ckv::FusedArgs f{};
+  f.s = a;
+  int *ctr = reinterpret_cast<int *>(static_cast<char *>(ws) + pl.counters_off);
+  f.ticket = ctr;
+  f.fallbacks = ctr + 1;
+  f.arrive = ctr + 64;
+  f.ready = ctr + 64 + p->batch * p->n_kv_heads;
+  f.bias_slot = pl.max_parts - 1;
+  int acc = 0;
+  for (int b = 0; b <= p->batch; ++b) {
+    f.seq_units[b] = acc;
+    if (b < p->batch)
+      acc += p->n_kv_heads *
+             fused_units(p->cu_seqlens_host[b + 1] - p->cu_seqlens_host[b], pl.unit_tiles);
+  }
+  f.n_units_total = acc;
+  return ckv::launch_fused_score(f, p->dtype == CKV_BF16, p->head_dim, pl.rt_max, pl.unit_tiles,
+                                 pl.n_counters, stream);
+}
+
 }  // namespace
 
 extern "C" {
@@ -287,11 +357,21 @@ const char *compresskv_status_string(int status) {
 
 const char *compresskv_last_error(void) { return g_last_error.c_str(); }
 
+int compresskv_scoring_path(const ckv_problem *p, const uint8_t *srh_mask_host) {
+  Plan pl;
+  int st;
+  if ((st = check_problem(p))) return -st;
+  if ((st = check_mask(p, srh_mask_host, pl))) return -st;
+  make_plan(p, pl, true);
+  ok();
+  return pl.fused ? 1 : 2;
+}
+
 size_t compresskv_workspace_bytes(const ckv_problem *p, const uint8_t *srh_mask_host,
                                   int32_t budget) {
   Plan pl;
   if (check_problem(p) || check_mask(p, srh_mask_host, pl) || check_budget(p, budget)) return 0;
-  make_plan(p, pl);
+  make_plan(p, pl, false);
   ok();
   return pl.total;
 }
@@ -306,11 +386,10 @@ int compresskv_score(const ckv_problem *p, const void *q_win, const void *k,
   if ((st = check_ptr(q_win, "q_win", 16)) || (st = check_ptr(k, "k", 16)) ||
       (st = check_ptr(scores, "scores", 4)))
     return st;
-  make_plan(p, pl);
+  make_plan(p, pl, false);
   if ((st = check_ws(pl, ws, ws_bytes))) return st;
-  ckv::ScoreArgs a = score_args(p, pl, q_win, k, scores, ws);
-  if ((st = hip_status(ckv::launch_score(a, p->dtype == CKV_BF16, p->head_dim, pl.rt_max,
-                                         p->batch, (hipStream_t)stream),
+  make_plan(p, pl, true);
+  if ((st = hip_status(launch_scoring(p, pl, q_win, k, scores, ws, (hipStream_t)stream),
                        "score")))
     return st;
   return ok();
@@ -363,17 +442,14 @@ int compresskv_compress_layer(const ckv_problem *p, const void *q_win, const voi
       (st = check_ptr(k_out, "k_out", 16)) || (st = check_ptr(v_out, "v_out", 16)))
     return st;
   if (scores_or_null && (st = check_ptr(scores_or_null, "scores", 4))) return st;
-  make_plan(p, pl);
+  make_plan(p, pl, false);
   if ((st = check_ws(pl, ws, ws_bytes))) return st;
+  make_plan(p, pl, true);
   float *scores = scores_or_null
                       ? scores_or_null
                       : reinterpret_cast<float *>(static_cast<char *>(ws) + pl.scores_off);
   hipStream_t s = (hipStream_t)stream;
-  ckv::ScoreArgs a = score_args(p, pl, q_win, k, scores, ws);
-  if ((st = hip_status(
-           ckv::launch_score(a, p->dtype == CKV_BF16, p->head_dim, pl.rt_max, p->batch, s),
-           "score")))
-    return st;
+  if ((st = hip_status(launch_scoring(p, pl, q_win, k, scores, ws, s), "score"))) return st;
   const int *hist = reinterpret_cast<const int *>(static_cast<char *>(ws) + pl.hist_off);
   if ((st = hip_status(
            ckv::launch_select(select_args(p, pl, scores, hist, budget, idx), p->batch, s),

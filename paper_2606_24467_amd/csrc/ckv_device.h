@@ -50,6 +50,18 @@ struct ScoreArgs {
   uint8_t srh_head[kMaxQHeads];        // query-head indices
 };
 
+// Arguments of the single-pass scoring kernel.
+struct FusedArgs {
+  ScoreArgs s;             // s.stats holds the published partials: [group][unit][row]
+  int *ticket;             // one counter
+  int *fallbacks;          // waits that hit their bound (diagnostic)
+  int *arrive;             // [batch * Hkv] units of each group that have published
+  int *ready;              // [batch * Hkv] the group's normalisers are published
+  int bias_slot;           // partial slot (per group) that holds the published normalisers
+  int n_units_total;
+  int seq_units[65];       // first ticket of sequence b (group-major numbering), b <= batch
+};
+
 struct SelectArgs {
   const float *scores;    // [Hkv][T]
   const int *hist;        // [batch][Hkv][kHistBins] or NULL (then counted here)

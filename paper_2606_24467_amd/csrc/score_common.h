@@ -1,0 +1,319 @@
+// Device building blocks shared by the scoring kernels (steps S1-S4):
+// query staging, key loads, MFMA tile logits, the running row statistics of
+// the window softmax, the merge of row-statistics partials, and the pooling
+// of window sums with the first-digit histogram of the selection.
+//
+// Rows of a KV group: SRH h (in head order) owns th = ceil(W/16) row tiles of
+// 16 rows; row i < W of the tile set is window query i of that head, the
+// padding rows have zero queries and are ignored.
+#pragma once
+
+#include "ckv_device.h"
+
+namespace ckv {
+
+template <typename T, int D>
+struct QLayout {
+  static constexpr int NS = Slices<T, D>::n;   // 16-byte slices per row and quad
+  static constexpr int U4 = 4 * NS;            // 16-byte units per row
+  static constexpr int STRIDE = U4 + 1;        // padded row stride in LDS (bank spread)
+};
+
+constexpr int kWaves = 8;       // waves per scoring workgroup
+constexpr int kPair = 2;        // key tiles per load group; two groups in flight per wave
+
+// Row tiles kept in registers: all of them when they fit in 64 VGPRs, else none.
+template <typename T, int D, int RTM>
+struct RegTiles {
+  static constexpr int v = RTM * Slices<T, D>::n <= 16 ? RTM : 0;
+  static constexpr int n = v > 0 ? v : 1;   // array extent
+};
+
+// The group's SRH window queries (rt_n row tiles) staged in LDS in two
+// phases: q_load issues every global load (before the first key loads, so that
+// waiting for the queries never waits for keys), q_store writes them to LDS.
+// Rows past W and tiles past rt_n are zero.
+template <typename T, int D, int RTM, int NT>
+struct QStage {
+  static constexpr int U4 = QLayout<T, D>::U4;
+  static constexpr int n = (RTM * 16 * U4 + NT - 1) / NT;   // 16-byte units per thread
+};
+
+template <typename T, int D, int RTM, int NT>
+__device__ __forceinline__ void q_load(const ScoreArgs &a, int b, int off, int rt_n,
+                                       uint4 (&qv)[QStage<T, D, RTM, NT>::n]) {
+  constexpr int U4 = QLayout<T, D>::U4;
+  const char *qb = reinterpret_cast<const char *>(a.q);
+#pragma unroll
+  for (int it = 0; it < QStage<T, D, RTM, NT>::n; ++it) {
+    const int idx = (int)threadIdx.x + it * NT;
+    const int row = idx / U4, u = idx - row * U4;
+    const int rt = row >> 4, c = row & 15;
+    qv[it] = make_uint4(0, 0, 0, 0);
+    if (rt < rt_n) {
+      const int i = (rt % a.th) * 16 + c;
+      if (i < a.W) {
+        const int head = a.srh_head[off + rt / a.th];
+        qv[it] = load16(qb + (((int64_t)b * a.W + i) * a.Hq + head) * (int64_t)(D * sizeof(T)) +
+                        16 * u);
+      }
+    }
+  }
+}
+
+template <typename T, int D, int RTM, int NT>
+__device__ __forceinline__ void q_store(const uint4 (&qv)[QStage<T, D, RTM, NT>::n],
+                                        uint4 *q_lds) {
+  constexpr int U4 = QLayout<T, D>::U4, STRIDE = QLayout<T, D>::STRIDE;
+#pragma unroll
+  for (int it = 0; it < QStage<T, D, RTM, NT>::n; ++it) {
+    const int idx = (int)threadIdx.x + it * NT;
+    const int row = idx / U4, u = idx - row * U4;
+    if (row < RTM * 16) q_lds[row * STRIDE + u] = qv[it];
+  }
+}
+
+template <typename T, int D>
+__device__ __forceinline__ uint4 q_frag(const uint4 *q_lds, int rt, int s, int c, int quad) {
+  return q_lds[(rt * 16 + c) * QLayout<T, D>::STRIDE + 4 * s + quad];
+}
+
+// Slices of one key row (key index clamped into the sequence).
+template <typename T, int D>
+__device__ __forceinline__ void load_k_row(const ScoreArgs &a, int s0, int key, int g, int quad,
+                                           uint4 (&out)[Slices<T, D>::n]) {
+  const char *p = reinterpret_cast<const char *>(a.k) +
+                  ((int64_t)(s0 + key) * a.k_stride_tok + (int64_t)g * a.k_stride_head) *
+                      (int64_t)sizeof(T) +
+                  16 * quad;
+#pragma unroll
+  for (int s = 0; s < Slices<T, D>::n; ++s) out[s] = load16(p + 64 * s);
+}
+
+// logits of row tile rt against one key tile; KEYS_AS_A selects the operand
+// order (true: lane holds 4 keys of one row; false: 4 rows of one key).
+template <typename T, int D, int RTM, bool KEYS_AS_A>
+__device__ __forceinline__ f32x4 tile_logits(const uint4 (&kf)[Slices<T, D>::n],
+                                             const uint4 (&qreg)[RegTiles<T, D, RTM>::n]
+                                                                [Slices<T, D>::n],
+                                             const uint4 *q_lds, int rt, int c, int quad) {
+  constexpr int NS = Slices<T, D>::n, RQ = RegTiles<T, D, RTM>::v;
+  f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    uint4 qv;
+    if (rt < RQ) {
+      qv = qreg[rt < RQ ? rt : 0][s];   // rt < RQ here; the clamp only keeps the index static
+    } else {
+      qv = q_frag<T, D>(q_lds, rt, s, c, quad);
+    }
+    acc = KEYS_AS_A ? mfma_slice<T>(kf[s], qv, acc) : mfma_slice<T>(qv, kf[s], acc);
+  }
+  return acc;
+}
+
+// Fold one key tile (logits acc[rt], keys base + 4*quad + r) into the running
+// (ref, sum) pairs of this lane's rows.  Keys past the sequence end and, inside
+// the window, after the row's own position (causal) are masked.
+template <int RTM>
+__device__ __forceinline__ void stats_update(const ScoreArgs &a, const f32x4 (&acc)[RTM],
+                                             float (&ref)[RTM], float (&sum)[RTM], int rt_n,
+                                             int base, int L, int P, int c, int quad) {
+  constexpr float kRescale = 30.f;   // rebase the reference when a term would exceed 2^30
+  const bool masked_tile = (base + 16 > P);
+  float d[RTM][4];
+  float dmax = -INFINITY;
+#pragma unroll
+  for (int rt = 0; rt < RTM; ++rt) {
+    if (rt >= rt_n) continue;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float x = __builtin_fmaf(acc[rt][r], a.c1, -ref[rt]);
+      if (masked_tile) {
+        const int i = (rt % a.th) * 16 + c;   // window index of this lane's row
+        const int j = base + 4 * quad + r;
+        const bool ok = (j < L) && (i >= a.W || j <= P + i);
+        x = ok ? x : -INFINITY;
+      }
+      d[rt][r] = x;
+      dmax = fmaxf(dmax, x);
+    }
+  }
+  if (__any(dmax > kRescale)) {
+    // Rebase a row's reference on the largest new value when a term would
+    // exceed 2^kRescale (always the case for the first key of a row).
+#pragma unroll
+    for (int rt = 0; rt < RTM; ++rt) {
+      if (rt >= rt_n) continue;
+      const float m = fmaxf(fmaxf(d[rt][0], d[rt][1]), fmaxf(d[rt][2], d[rt][3]));
+      if (m > kRescale) {
+        float best = -INFINITY;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (d[rt][r] != -INFINITY) best = fmaxf(best, acc[rt][r] * a.c1);
+        sum[rt] = (ref[rt] == -INFINITY) ? 0.f : sum[rt] * fast_exp2(ref[rt] - best);
+        ref[rt] = best;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          d[rt][r] = (d[rt][r] == -INFINITY) ? -INFINITY
+                                             : __builtin_fmaf(acc[rt][r], a.c1, -best);
+      }
+    }
+  }
+#pragma unroll
+  for (int rt = 0; rt < RTM; ++rt) {
+    if (rt >= rt_n) continue;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) sum[rt] += fast_exp2(d[rt][r]);
+  }
+}
+
+// A partial (ref, sum) pair read or written at agent scope: the access goes to
+// the device's coherence point instead of the per-XCD L2, so partials that
+// workgroups of the same kernel exchange need no cache-wide fences.
+__device__ __forceinline__ void store_partial_coherent(float2 *p, float2 v) {
+  __hip_atomic_store(reinterpret_cast<unsigned long long *>(p),
+                     __builtin_bit_cast(unsigned long long, v), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float2 load_partial_coherent(const float2 *p) {
+  return __builtin_bit_cast(float2, __hip_atomic_load(
+                                        reinterpret_cast<const unsigned long long *>(p),
+                                        __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+}
+
+// Row normalisers bias = ref + log2(sum) for the `rows` rows of one group,
+// merged from n_parts partial (ref, sum) pairs laid out parts[k * stride + row]
+// (fixed order per thread, then a shuffle tree over tpr threads per row).
+// Padding rows (window index >= W) and rows >= rows get +inf.  COHERENT reads
+// the partials at agent scope (they were written by this kernel).
+template <int NT, bool COHERENT = false>
+__device__ __forceinline__ void merge_row_bias(const ScoreArgs &a, const float2 *parts,
+                                               int64_t stride, int n_parts, int rows,
+                                               int rows_cap, float *bias_s) {
+  const int tid = threadIdx.x;
+  int tpr = 1;
+  while (tpr * 2 * rows <= NT && tpr < 32) tpr *= 2;
+  const int row = tid / tpr, sub = tid % tpr;
+  float m = -INFINITY, sm = 0.f;
+  if (row < rows) {
+    // batches of 8 loads in flight, merged in index order
+    constexpr int kBatch = 8;
+    for (int k0 = sub; k0 < n_parts; k0 += kBatch * tpr) {
+      float2 v[kBatch];
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) {
+        const int k = min(k0 + j * tpr, n_parts - 1);
+        v[j] = COHERENT ? load_partial_coherent(parts + (int64_t)k * stride + row)
+                        : parts[(int64_t)k * stride + row];
+      }
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j)
+        if (k0 + j * tpr < n_parts) merge_stats(m, sm, v[j].x, v[j].y);
+    }
+  }
+  for (int o = 1; o < tpr; o <<= 1) {
+    const float mo = __shfl_xor(m, o), so = __shfl_xor(sm, o);
+    merge_stats(m, sm, mo, so);
+  }
+  if (row < rows && sub == 0) {
+    const int i = row % (16 * a.th);
+    bias_s[row] = (i < a.W) ? m + fast_log2(sm) : INFINITY;
+  }
+  for (int r = rows + tid; r < rows_cap; r += NT) bias_s[r] = INFINITY;
+}
+
+// Window sums of one key tile for every SRH of the group (MFMA operands: A =
+// window rows, B = keys; lane (quad, c) holds rows 4*quad .. 4*quad+3 against
+// key c): in-lane over the 4 rows and the SRH's row tiles, then across the
+// quads.  cs[h][16 + 16*e + c] receives SRH h's sum for key c of tile e.
+template <typename T, int D, int RTM, int CSW>
+__device__ __forceinline__ void tile_window_sums(const ScoreArgs &a,
+                                                 const uint4 (&kf)[Slices<T, D>::n],
+                                                 const uint4 (&qreg)[RegTiles<T, D, RTM>::n]
+                                                                    [Slices<T, D>::n],
+                                                 const uint4 *q_lds, const float (&bias)[RTM][4],
+                                                 int rt_n, int e, bool keep, int c, int quad,
+                                                 float (*cs)[CSW]) {
+  int hh = 0;
+  float v = 0.f;
+#pragma unroll
+  for (int rt = 0; rt < RTM; ++rt) {
+    if (rt >= rt_n) continue;
+    const f32x4 acc = tile_logits<T, D, RTM, false>(kf, qreg, q_lds, rt, c, quad);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) v += fast_exp2(__builtin_fmaf(acc[r], a.c1, -bias[rt][r]));
+    if ((a.head_end_mask >> rt) & 1u) {
+      v += __shfl_xor(v, 16);
+      v += __shfl_xor(v, 32);
+      if (keep && quad == (hh & 3)) cs[hh][16 + 16 * e + c] = v;
+      v = 0.f;
+      ++hh;
+    }
+  }
+}
+
+// Pooling along the token axis (positions clipped to the prefix [0, P)), then
+// the mean over the group's nh SRHs, for positions [c0, p_end); cs[h][16 + x]
+// holds the window sum at key c0 + x (x from -16).  Each score goes to `out`
+// and to the LDS histogram of its top 11 value bits.
+template <int NT, int CSW>
+__device__ __forceinline__ void pool_scores(const ScoreArgs &a, const float (*cs)[CSW],
+                                            int nh, int c0, int p_end, int P, float *out,
+                                            int *hist_s) {
+  const int rp = (a.pool_kernel - 1) >> 1;
+  const float inv_k = 1.f / (float)a.pool_kernel;
+  const float inv_n = 1.f / (float)nh;
+  for (int j = c0 + (int)threadIdx.x; j < p_end; j += NT) {
+    const int lo = max(j - rp, 0) - c0 + 16;
+    const int hi = min(j + rp, P - 1) - c0 + 16;
+    float score;
+    if (a.reduce_order == 0) {      // pool each SRH, then average
+      score = 0.f;
+      for (int h = 0; h < nh; ++h) {
+        float v;
+        if (a.pool_type == 0) {
+          v = -INFINITY;
+          for (int x = lo; x <= hi; ++x) v = fmaxf(v, cs[h][x]);
+        } else {
+          v = 0.f;
+          for (int x = lo; x <= hi; ++x) v += cs[h][x];
+          v *= inv_k;
+        }
+        score += v;
+      }
+      score *= inv_n;
+    } else {                        // average the SRH sums, then pool
+      if (a.pool_type == 0) {
+        score = -INFINITY;
+        for (int x = lo; x <= hi; ++x) {
+          float m = 0.f;
+          for (int h = 0; h < nh; ++h) m += cs[h][x];
+          score = fmaxf(score, m * inv_n);
+        }
+      } else {
+        score = 0.f;
+        for (int x = lo; x <= hi; ++x) {
+          float m = 0.f;
+          for (int h = 0; h < nh; ++h) m += cs[h][x];
+          score += m * inv_n;
+        }
+        score *= inv_k;
+      }
+    }
+    out[j] = score;
+    atomicAdd(&hist_s[hist_bin(__float_as_uint(score))], 1);
+  }
+}
+
+// Add a workgroup's LDS histogram to the group's global one (integer atomics:
+// the result does not depend on their order).
+template <int NT>
+__device__ __forceinline__ void flush_hist(const int *hist_s, int *hg) {
+  for (int i = threadIdx.x; i < kHistBins; i += NT) {
+    const int n = hist_s[i];
+    if (n) atomicAdd(&hg[i], n);
+  }
+}
+
+}  // namespace ckv

@@ -25,165 +25,9 @@
 // of 2-tile groups (8 KB each): loads are unconditional (key index clamped
 // into the sequence, extra tiles masked), so the compiler can wait for exactly
 // the group being consumed while the next one is still in flight.
-#include "ckv_device.h"
+#include "score_common.h"
 
 namespace ckv {
-
-template <typename T, int D>
-struct QLayout {
-  static constexpr int NS = Slices<T, D>::n;   // 16-byte slices per row and quad
-  static constexpr int U4 = 4 * NS;            // 16-byte units per row
-  static constexpr int STRIDE = U4 + 1;        // padded row stride in LDS (bank spread)
-};
-
-constexpr int kWaves = 8;       // waves per scoring workgroup
-constexpr int kPair = 2;        // key tiles per load group; two groups in flight per wave
-
-// Row tiles kept in registers: all of them when they fit in 64 VGPRs, else none.
-template <typename T, int D, int RTM>
-struct RegTiles {
-  static constexpr int v = RTM * Slices<T, D>::n <= 16 ? RTM : 0;
-  static constexpr int n = v > 0 ? v : 1;   // array extent
-};
-
-// The group's SRH window queries (rt_n row tiles) staged in LDS in two
-// phases: q_load issues every global load (before the first key loads, so that
-// waiting for the queries never waits for keys), q_store writes them to LDS.
-// Rows past W and tiles past rt_n are zero.
-template <typename T, int D, int RTM, int NT>
-struct QStage {
-  static constexpr int U4 = QLayout<T, D>::U4;
-  static constexpr int n = (RTM * 16 * U4 + NT - 1) / NT;   // 16-byte units per thread
-};
-
-template <typename T, int D, int RTM, int NT>
-__device__ __forceinline__ void q_load(const ScoreArgs &a, int b, int off, int rt_n,
-                                       uint4 (&qv)[QStage<T, D, RTM, NT>::n]) {
-  constexpr int U4 = QLayout<T, D>::U4;
-  const char *qb = reinterpret_cast<const char *>(a.q);
-#pragma unroll
-  for (int it = 0; it < QStage<T, D, RTM, NT>::n; ++it) {
-    const int idx = (int)threadIdx.x + it * NT;
-    const int row = idx / U4, u = idx - row * U4;
-    const int rt = row >> 4, c = row & 15;
-    qv[it] = make_uint4(0, 0, 0, 0);
-    if (rt < rt_n) {
-      const int i = (rt % a.th) * 16 + c;
-      if (i < a.W) {
-        const int head = a.srh_head[off + rt / a.th];
-        qv[it] = load16(qb + (((int64_t)b * a.W + i) * a.Hq + head) * (int64_t)(D * sizeof(T)) +
-                        16 * u);
-      }
-    }
-  }
-}
-
-template <typename T, int D, int RTM, int NT>
-__device__ __forceinline__ void q_store(const uint4 (&qv)[QStage<T, D, RTM, NT>::n],
-                                        uint4 *q_lds) {
-  constexpr int U4 = QLayout<T, D>::U4, STRIDE = QLayout<T, D>::STRIDE;
-#pragma unroll
-  for (int it = 0; it < QStage<T, D, RTM, NT>::n; ++it) {
-    const int idx = (int)threadIdx.x + it * NT;
-    const int row = idx / U4, u = idx - row * U4;
-    if (row < RTM * 16) q_lds[row * STRIDE + u] = qv[it];
-  }
-}
-
-template <typename T, int D>
-__device__ __forceinline__ uint4 q_frag(const uint4 *q_lds, int rt, int s, int c, int quad) {
-  return q_lds[(rt * 16 + c) * QLayout<T, D>::STRIDE + 4 * s + quad];
-}
-
-// Slices of one key row (key index clamped into the sequence).
-template <typename T, int D>
-__device__ __forceinline__ void load_k_row(const ScoreArgs &a, int s0, int key, int g, int quad,
-                                           uint4 (&out)[Slices<T, D>::n]) {
-  const char *p = reinterpret_cast<const char *>(a.k) +
-                  ((int64_t)(s0 + key) * a.k_stride_tok + (int64_t)g * a.k_stride_head) *
-                      (int64_t)sizeof(T) +
-                  16 * quad;
-#pragma unroll
-  for (int s = 0; s < Slices<T, D>::n; ++s) out[s] = load16(p + 64 * s);
-}
-
-// logits of row tile rt against one key tile; KEYS_AS_A selects the operand
-// order (true: lane holds 4 keys of one row; false: 4 rows of one key).
-template <typename T, int D, int RTM, bool KEYS_AS_A>
-__device__ __forceinline__ f32x4 tile_logits(const uint4 (&kf)[Slices<T, D>::n],
-                                             const uint4 (&qreg)[RegTiles<T, D, RTM>::n]
-                                                                [Slices<T, D>::n],
-                                             const uint4 *q_lds, int rt, int c, int quad) {
-  constexpr int NS = Slices<T, D>::n, RQ = RegTiles<T, D, RTM>::v;
-  f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int s = 0; s < NS; ++s) {
-    uint4 qv;
-    if (rt < RQ) {
-      qv = qreg[rt < RQ ? rt : 0][s];   // rt < RQ here; the clamp only keeps the index static
-    } else {
-      qv = q_frag<T, D>(q_lds, rt, s, c, quad);
-    }
-    acc = KEYS_AS_A ? mfma_slice<T>(kf[s], qv, acc) : mfma_slice<T>(qv, kf[s], acc);
-  }
-  return acc;
-}
-
-// Fold one key tile (logits acc[rt], keys base + 4*quad + r) into the running
-// (ref, sum) pairs of this lane's rows.  Keys past the sequence end and, inside
-// the window, after the row's own position (causal) are masked.
-template <int RTM>
-__device__ __forceinline__ void stats_update(const ScoreArgs &a, const f32x4 (&acc)[RTM],
-                                             float (&ref)[RTM], float (&sum)[RTM], int rt_n,
-                                             int base, int L, int P, int c, int quad) {
-  constexpr float kRescale = 30.f;   // rebase the reference when a term would exceed 2^30
-  const bool masked_tile = (base + 16 > P);
-  float d[RTM][4];
-  float dmax = -INFINITY;
-#pragma unroll
-  for (int rt = 0; rt < RTM; ++rt) {
-    if (rt >= rt_n) continue;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      float x = __builtin_fmaf(acc[rt][r], a.c1, -ref[rt]);
-      if (masked_tile) {
-        const int i = (rt % a.th) * 16 + c;   // window index of this lane's row
-        const int j = base + 4 * quad + r;
-        const bool ok = (j < L) && (i >= a.W || j <= P + i);
-        x = ok ? x : -INFINITY;
-      }
-      d[rt][r] = x;
-      dmax = fmaxf(dmax, x);
-    }
-  }
-  if (__any(dmax > kRescale)) {
-    // Rebase a row's reference on the largest new value when a term would
-    // exceed 2^kRescale (always the case for the first key of a row).
-#pragma unroll
-    for (int rt = 0; rt < RTM; ++rt) {
-      if (rt >= rt_n) continue;
-      const float m = fmaxf(fmaxf(d[rt][0], d[rt][1]), fmaxf(d[rt][2], d[rt][3]));
-      if (m > kRescale) {
-        float best = -INFINITY;
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          if (d[rt][r] != -INFINITY) best = fmaxf(best, acc[rt][r] * a.c1);
-        sum[rt] = (ref[rt] == -INFINITY) ? 0.f : sum[rt] * fast_exp2(ref[rt] - best);
-        ref[rt] = best;
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          d[rt][r] = (d[rt][r] == -INFINITY) ? -INFINITY
-                                             : __builtin_fmaf(acc[rt][r], a.c1, -best);
-      }
-    }
-  }
-#pragma unroll
-  for (int rt = 0; rt < RTM; ++rt) {
-    if (rt >= rt_n) continue;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) sum[rt] += fast_exp2(d[rt][r]);
-  }
-}
 
 // ---------------------------------------------------------------------------
 // S1+S2 partial statistics.  Grid (Hkv, max_chunks1, batch), 512 threads: the
@@ -346,32 +190,9 @@ __global__ __launch_bounds__(64 * kWaves) void colsum_kernel(const ScoreArgs a) 
   for (int i = tid; i < kHistBins; i += NT) hist_s[i] = 0;
 
   // Row normalisers bias = ref + log2(sum), merged over every chunk of the
-  // statistics pass: tpr threads per row, fixed order, then a shuffle tree.
-  {
-    const int rows = rt_n * 16;
-    const int nc1 = (L + a.chunk1 - 1) / a.chunk1;
-    int tpr = 1;
-    while (tpr * 2 * rows <= NT && tpr < 32) tpr *= 2;
-    const int row = tid / tpr, sub = tid % tpr;
-    float m = -INFINITY, sm = 0.f;
-    if (row < rows) {
-      const float2 *st =
-          a.stats + ((int64_t)b * a.Hkv + g) * a.max_chunks1 * a.row_slots + row;
-      for (int k = sub; k < nc1; k += tpr) {
-        const float2 v = st[(int64_t)k * a.row_slots];
-        merge_stats(m, sm, v.x, v.y);
-      }
-    }
-    for (int o = 1; o < tpr; o <<= 1) {
-      const float mo = __shfl_xor(m, o), so = __shfl_xor(sm, o);
-      merge_stats(m, sm, mo, so);
-    }
-    if (row < rows && sub == 0) {
-      const int i = row % (16 * a.th);
-      bias_s[row] = (i < a.W) ? m + fast_log2(sm) : INFINITY;
-    }
-    for (int r = rows + tid; r < RTM * 16; r += NT) bias_s[r] = INFINITY;
-  }
+  // statistics pass.
+  merge_row_bias<NT>(a, a.stats + ((int64_t)b * a.Hkv + g) * a.max_chunks1 * a.row_slots,
+                     a.row_slots, (L + a.chunk1 - 1) / a.chunk1, rt_n * 16, RTM * 16, bias_s);
   __syncthreads();
   uint4 qreg[RegTiles<T, D, RTM>::n][NS];
 #pragma unroll
@@ -390,25 +211,8 @@ __global__ __launch_bounds__(64 * kWaves) void colsum_kernel(const ScoreArgs a) 
 #pragma unroll
     for (int p = 0; p < kPair; ++p) {
       const int e = tile_of(kPair * grp + p);
-      const bool keep = (e >= e_lo && e <= e_hi);
-      // Sum the normalised probabilities over the window rows of each SRH:
-      // in-lane over the 4 rows and the SRH's row tiles, then across the quads.
-      int hh = 0;
-      float v = 0.f;
-#pragma unroll
-      for (int rt = 0; rt < RTM; ++rt) {
-        if (rt >= rt_n) continue;
-        const f32x4 acc = tile_logits<T, D, RTM, false>(kf[p], qreg, q_lds, rt, c, quad);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) v += fast_exp2(__builtin_fmaf(acc[r], a.c1, -bias[rt][r]));
-        if ((a.head_end_mask >> rt) & 1u) {
-          v += __shfl_xor(v, 16);
-          v += __shfl_xor(v, 32);
-          if (keep && quad == (hh & 3)) cs[hh][16 + 16 * e + c] = v;
-          v = 0.f;
-          ++hh;
-        }
-      }
+      tile_window_sums<T, D, RTM, kMaxChunk2 + 32>(a, kf[p], qreg, q_lds, bias, rt_n, e, e >= e_lo && e <= e_hi,
+                                  c, quad, cs);
     }
   };
   for (int grp = 0; grp < n_groups; grp += 2) {
@@ -423,58 +227,9 @@ __global__ __launch_bounds__(64 * kWaves) void colsum_kernel(const ScoreArgs a) 
   }
   __syncthreads();
 
-  // Pooling along the token axis (positions clipped to the prefix [0, P)),
-  // then the mean over the group's SRHs; each score also lands in the
-  // histogram of its top 11 value bits.
-  const int rp = (a.pool_kernel - 1) >> 1;
-  const float inv_k = 1.f / (float)a.pool_kernel;
-  const float inv_n = 1.f / (float)nh;
-  for (int j = c0 + tid; j < p_end; j += NT) {
-    const int lo = max(j - rp, 0) - c0 + 16;
-    const int hi = min(j + rp, P - 1) - c0 + 16;
-    float score;
-    if (a.reduce_order == 0) {      // pool each SRH, then average
-      score = 0.f;
-      for (int h = 0; h < nh; ++h) {
-        float v;
-        if (a.pool_type == 0) {
-          v = -INFINITY;
-          for (int x = lo; x <= hi; ++x) v = fmaxf(v, cs[h][x]);
-        } else {
-          v = 0.f;
-          for (int x = lo; x <= hi; ++x) v += cs[h][x];
-          v *= inv_k;
-        }
-        score += v;
-      }
-      score *= inv_n;
-    } else {                        // average the SRH sums, then pool
-      if (a.pool_type == 0) {
-        score = -INFINITY;
-        for (int x = lo; x <= hi; ++x) {
-          float m = 0.f;
-          for (int h = 0; h < nh; ++h) m += cs[h][x];
-          score = fmaxf(score, m * inv_n);
-        }
-      } else {
-        score = 0.f;
-        for (int x = lo; x <= hi; ++x) {
-          float m = 0.f;
-          for (int h = 0; h < nh; ++h) m += cs[h][x];
-          score += m * inv_n;
-        }
-        score *= inv_k;
-      }
-    }
-    out[j] = score;
-    atomicAdd(&hist_s[hist_bin(__float_as_uint(score))], 1);
-  }
+  pool_scores<NT, kMaxChunk2 + 32>(a, cs, nh, c0, p_end, P, out, hist_s);
   __syncthreads();
-  int *hg = a.hist + ((int64_t)b * a.Hkv + g) * kHistBins;
-  for (int i = tid; i < kHistBins; i += NT) {
-    const int n = hist_s[i];
-    if (n) atomicAdd(&hg[i], n);
-  }
+  flush_hist<NT>(hist_s, a.hist + ((int64_t)b * a.Hkv + g) * kHistBins);
 }
 
 // ---------------------------------------------------------------------------

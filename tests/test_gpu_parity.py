@@ -14,6 +14,17 @@ from tests import parity_helpers as H
 pytestmark = pytest.mark.gpu
 
 
+@pytest.fixture(autouse=True, params=["two", "single"])
+def scoring_path(request, monkeypatch):
+    """Every case runs on the two-pass path (the default) and on the
+    single-pass kernel (where it applies)."""
+    if request.param == "single":
+        monkeypatch.setenv("CKV_PATH", "single")
+    else:
+        monkeypatch.delenv("CKV_PATH", raising=False)
+    return request.param
+
+
 def _say(*a):
     print(*a, file=sys.stderr, flush=True)
 
@@ -201,6 +212,20 @@ def test_deterministic_bits(gpu):
     r2, _ = run_case(x, gpu, check=False)
     for key in r1:
         assert np.array_equal(r1[key], r2[key]), key
+
+
+def test_scoring_path_choice_for_the_benchmark_shapes(gpu, scoring_path):
+    for name, kw in [("llama1", {}), ("llama32", {}), ("ragged8", {}), ("tiny", {}),
+                     ("qwen128k", dict(seq_len=65536))]:
+        w = wl.get(name, **kw)
+        lens = wl.seq_lengths(w)
+        cu = wl.cu_seqlens(lens)
+        q = torch.empty((w.batch, w.window, w.n_q_heads, w.head_dim), device=gpu,
+                        dtype=torch.bfloat16 if w.dtype == wl.BF16 else torch.float32)
+        k = torch.empty((16, w.n_kv_heads, w.head_dim), device=gpu, dtype=q.dtype)
+        p = C.Problem(q, k, k, torch.from_numpy(cu).to(gpu), cu_seqlens_host=cu)
+        path = C.compresskv_scoring_path(p, wl.srh_mask(w, 0))
+        assert path == (1 if scoring_path == "single" else 2), (name, path)
 
 
 def test_score_entry_point_alone(gpu):
