@@ -1,9 +1,9 @@
 #!/usr/bin/env python
 """Benchmark of the CompressKV prefill-time eviction path on one MI355X.
 
-A step compresses every layer of the workload once (compresskv_compress_layer
-per layer: score -> select -> gather) with inputs already resident in HBM;
-layers are independent, so they alternate over --streams streams.
+A step compresses every layer of the workload once (one compresskv_compress_layers
+call: score -> select -> gather for all layers) with inputs already resident in HBM;
+--mode per-layer instead calls compresskv_compress_layer per layer over --streams streams.
 The reported value is prompt tokens compressed per second per layer:
 sum_b L_b * n_layers / step_time.
 
@@ -47,11 +47,10 @@ def algorithmic_bytes(lens, Hkv, D, es, W, n_srh_total, budget):
     return k_bytes + q_bytes, gather
 
 
-def cpu_baseline(layer, w, seconds):
-    """The fp64 oracle on (sequence, group) units of one layer until about
-    `seconds` of CPU time, scaled to tokens per second per layer."""
+def cpu_baseline(layers, w, seconds):
+    """The fp64 oracle on (layer, sequence, KV group) units, layer after layer,
+    until about `seconds` of CPU time, scaled to tokens per second per layer."""
     import numpy as np
-    import torch
     import oracle as O
 
     try:
@@ -60,35 +59,40 @@ def cpu_baseline(layer, w, seconds):
                        if i.get("user_api") == "blas"] or [1])
     except Exception:
         threads = 1
-    cu = layer["cu_seqlens_host"]
     G = w.n_q_heads // w.n_kv_heads
-    units = [(b, g) for b in range(w.batch) for g in range(w.n_kv_heads)]
-    total_tokens = sum(int(cu[b + 1] - cu[b]) for b, _ in units)
-    done_tokens = 0
+    cu = layers[0]["cu_seqlens_host"]
+    tokens_layer = int(cu[-1])
+    done_tokens = 0          # group-tokens: a (sequence, group) unit of length L counts L
     t_total = 0.0
     n = 0
-    for b, g in units:
-        s0, s1 = int(cu[b]), int(cu[b + 1])
-        q = layer["q_win"][b:b + 1, :, g * G:(g + 1) * G, :].float().cpu().numpy()
-        k = layer["k"][s0:s1, g:g + 1, :].float().cpu().numpy()
-        v = layer["v"][s0:s1, g:g + 1, :].float().cpu().numpy()
-        mask = layer["srh_mask"][g * G:(g + 1) * G]
-        t0 = time.perf_counter()
-        O.compress_layer(q, k, v, np.array([0, s1 - s0]), mask, layer["budget"],
-                         w.pool_kernel, w.pool_type)
-        t_total += time.perf_counter() - t0
-        done_tokens += s1 - s0
-        n += 1
+    for lay in layers:
+        q_all = lay["q_win"].float().cpu().numpy()
+        for b in range(w.batch):
+            s0, s1 = int(cu[b]), int(cu[b + 1])
+            for g in range(w.n_kv_heads):
+                q = q_all[b:b + 1, :, g * G:(g + 1) * G, :]
+                k = lay["k"][s0:s1, g:g + 1, :].float().cpu().numpy()
+                v = lay["v"][s0:s1, g:g + 1, :].float().cpu().numpy()
+                mask = lay["srh_mask"][g * G:(g + 1) * G]
+                t0 = time.perf_counter()
+                O.compress_layer(q, k, v, np.array([0, s1 - s0]), mask, lay["budget"],
+                                 w.pool_kernel, w.pool_type)
+                t_total += time.perf_counter() - t0
+                done_tokens += s1 - s0
+                n += 1
+                if t_total >= seconds:
+                    break
+            if t_total >= seconds:
+                break
         if t_total >= seconds:
             break
-    t_layer = t_total * total_tokens / done_tokens
-    tokens_layer = sum(int(cu[b + 1] - cu[b]) for b in range(w.batch))
-    del torch
+    group_tokens_layer = tokens_layer * w.n_kv_heads
+    t_layer = t_total * group_tokens_layer / done_tokens
     return {"value": tokens_layer / t_layer, "unit": "tokens/s/layer", "cores": int(threads),
             "kind": "oracle",
-            "sample": f"layer 0, {n} of {len(units)} (sequence, KV group) units "
-                      f"({done_tokens} of {total_tokens} group-tokens), {t_total:.1f} s, "
-                      f"scaled to a whole layer"}
+            "sample": f"{n} (layer, sequence, KV group) units from layer 0 on "
+                      f"({done_tokens} group-tokens, {done_tokens / group_tokens_layer:.2f} "
+                      f"layers' worth), {t_total:.1f} s of oracle time, scaled to one layer"}
 
 
 def main():
@@ -100,10 +104,13 @@ def main():
                     help="tiny | llama1 | llama32 | qwen128k | ragged8")
     ap.add_argument("--layers", type=int, default=0, help="limit the layer count (0: all)")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--mode", default="layers", choices=["layers", "per-layer"],
+                    help="layers: one compresskv_compress_layers call per step (default); "
+                         "per-layer: one compresskv_compress_layer call per layer")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--streams", type=int, default=2,
-                    help="layers are independent: alternate them over this many streams")
+                    help="per-layer mode: alternate the layers over this many streams")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain elementwise copy of MIB MiB (3 times): the "
                          "reference point that scales the HBM byte counters")
@@ -134,20 +141,15 @@ def main():
         return
     w = wl.get(args.workload)
     n_layers = args.layers or w.n_layers
-    G = w.n_q_heads // w.n_kv_heads
     es = 2 if w.dtype == wl.BF16 else 4
     log(f"bench: workload {w.name}, {n_layers} layers, generating inputs on the GPU")
-    layers = []
-    for l in range(n_layers):
-        layers.append(wl.make_layer_device(w, l, args.seed, dev))
+    layers = [wl.make_layer_device(w, l, args.seed, dev) for l in range(n_layers)]
     torch.cuda.synchronize()
     lens = [int(x) for x in np.diff(layers[0]["cu_seqlens_host"])]
-    log(f"bench: inputs ready, lengths {lens[:8]}, budgets "
-        f"{[lay['budget'] for lay in layers][:8]}...")
+    budgets = [lay["budget"] for lay in layers]
+    log(f"bench: inputs ready, lengths {lens[:8]}, budgets {budgets[:8]}...")
 
-    # Per-layer problems, outputs and one shared workspace.
     probs, outs = [], []
-    ws_need = 0
     score_bytes_total = 0
     alg_bytes_total = 0
     for lay in layers:
@@ -155,7 +157,6 @@ def main():
                       cu_seqlens_host=lay["cu_seqlens_host"], pool_kernel=w.pool_kernel,
                       pool_type=w.pool_type)
         probs.append(p)
-        ws_need = max(ws_need, C.compresskv_workspace_bytes(p, lay["srh_mask"], lay["budget"]))
         B_l = lay["budget"]
         shape = (w.batch, w.n_kv_heads, B_l, w.head_dim)
         outs.append((torch.empty((w.batch, w.n_kv_heads, B_l), dtype=torch.int32, device=dev),
@@ -165,65 +166,71 @@ def main():
         sb, gb = algorithmic_bytes(lens, w.n_kv_heads, w.head_dim, es, w.window, n_srh, B_l)
         score_bytes_total += sb
         alg_bytes_total += sb + gb
-    # One workspace (row statistics, histogram, scores) per stream; every
-    # stream keeps the default priority.
-    n_streams = max(1, args.streams)
-    streams = [torch.cuda.current_stream()] + [torch.cuda.Stream() for _ in range(n_streams - 1)]
-    ws = [torch.empty(ws_need, dtype=torch.uint8, device=dev) for _ in streams]
-    main = streams[0]
+    q_l = [lay["q_win"] for lay in layers]
+    k_l = [lay["k"] for lay in layers]
+    v_l = [lay["v"] for lay in layers]
+    masks = np.stack([lay["srh_mask"] for lay in layers])
+    main = torch.cuda.current_stream()
 
-    def step(events=None):
-        # fork: every stream starts after the work already queued on the main stream
-        fork = torch.cuda.Event()
-        fork.record(main)
-        for st in streams[1:]:
-            st.wait_event(fork)
-        for li, (lay, p, (idx, k_out, v_out)) in enumerate(zip(layers, probs, outs)):
-            si = li % n_streams
-            st, wsi = streams[si], ws[si]
-            if events is not None:
-                events[li][0].record(st)
-            C.compresskv_compress_layer(p, lay["q_win"], lay["k"], lay["v"], lay["srh_mask"],
-                                        lay["budget"], idx, k_out, v_out, None, wsi, st)
-            if events is not None:
-                events[li][1].record(st)
-        for st in streams[1:]:   # join
-            ev = torch.cuda.Event()
-            ev.record(st)
-            main.wait_event(ev)
+    if args.mode == "layers":
+        ws_layers = C.layers_workspace(probs[0], masks, dev)
+        call = C.LayersCall(probs[0], q_l, k_l, v_l, masks, budgets, [o[0] for o in outs],
+                            [o[1] for o in outs], [o[2] for o in outs], None, ws_layers)
 
-    for i in range(args.warmup):
+        def step():
+            call(main)
+        n_streams = 1
+    else:
+        # One workspace per stream; every stream keeps the default priority.
+        n_streams = max(1, args.streams)
+        streams = [main] + [torch.cuda.Stream() for _ in range(n_streams - 1)]
+        ws_need = max(C.compresskv_workspace_bytes(p, lay["srh_mask"], lay["budget"])
+                      for p, lay in zip(probs, layers))
+        ws = [torch.empty(ws_need, dtype=torch.uint8, device=dev) for _ in streams]
+
+        def step():
+            fork = torch.cuda.Event()
+            fork.record(main)
+            for st in streams[1:]:
+                st.wait_event(fork)
+            for li, (lay, p, (idx, k_out, v_out)) in enumerate(zip(layers, probs, outs)):
+                si = li % n_streams
+                C.compresskv_compress_layer(p, lay["q_win"], lay["k"], lay["v"],
+                                            lay["srh_mask"], lay["budget"], idx, k_out, v_out,
+                                            None, ws[si], streams[si])
+            for st in streams[1:]:
+                ev = torch.cuda.Event()
+                ev.record(st)
+                main.wait_event(ev)
+
+    for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
     log(f"bench: {args.warmup} warmup steps done")
-    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in layers]
-          for _ in range(args.steps)]
-    torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for s in range(args.steps):
-        step(ev[s])
+    for _ in range(args.steps):
+        step()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     log(f"bench: {args.steps} timed steps in {elapsed * 1e3:.2f} ms")
-    layer_ms = [e[0].elapsed_time(e[1]) for per_step in ev for e in per_step]
-    layer_ms_avg = float(np.mean(layer_ms))
 
-    # Score phase alone (the kernels that stream K), one layer after another on
-    # the main stream, bracketed by events on that stream.
-    scores_buf = torch.empty((w.n_kv_heads, probs[0].total_tokens), dtype=torch.float32,
-                             device=dev)
-    sev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in layers]
-    for li, (lay, p) in enumerate(zip(layers, probs)):
-        sev[li][0].record(main)
-        C.compresskv_score(p, lay["q_win"], lay["k"], lay["srh_mask"], scores_buf, ws[0], main)
-        sev[li][1].record(main)
+    # Score phase alone (the two kernels that stream K), every layer in one
+    # multi-layer call, bracketed by events on the stream it runs on.
+    scores_all = torch.empty((n_layers, w.n_kv_heads, probs[0].total_tokens),
+                             dtype=torch.float32, device=dev)
+    ws_s = C.layers_workspace(probs[0], masks, dev)
+    reps = max(3, args.steps)
+    sev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(reps + 1)]
+    for r in range(reps + 1):          # the first repetition is a warm-up
+        sev[r][0].record(main)
+        C.compresskv_score_layers(probs[0], q_l, k_l, masks, scores_all, ws_s, main)
+        sev[r][1].record(main)
     torch.cuda.synchronize()
-    score_ms_avg = float(np.mean([e[0].elapsed_time(e[1]) for e in sev]))
-    score_bytes_avg = score_bytes_total / n_layers
+    score_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in sev[1:]]))
     ms_per_step = elapsed * 1e3 / args.steps
     tokens = sum(lens)
     value = tokens * n_layers / (ms_per_step / 1e3)
-    achieved = score_bytes_avg / (score_ms_avg / 1e3) / 1e9
+    achieved = score_bytes_total / (score_ms / 1e3) / 1e9
     e2e_gbs = alg_bytes_total / (ms_per_step / 1e3) / 1e9
 
     result = {
@@ -236,18 +243,19 @@ def main():
                                f"L={'ragged ' + str(w.ragged) if w.ragged else w.seq_len}, "
                                f"W={w.window}, maxpool {w.pool_kernel}",
                    "layers": n_layers, "batch": w.batch, "seq_lens": lens[:16],
-                   "budgets": [lay["budget"] for lay in layers]},
-        "roofline": {"bound": "hbm", "kernel": "score phase (compresskv_score: statistics + "
-                     "column-sum kernels)", "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
-                     "avg_ms": score_ms_avg, "bytes_per_launch": score_bytes_avg},
+                   "budgets": budgets, "mode": args.mode, "streams": n_streams},
+        "roofline": {"bound": "hbm",
+                     "kernel": f"score phase: stats_kernel + colsum_kernel over {n_layers} "
+                               f"layers (one compresskv_score_layers call)",
+                     "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "avg_ms": score_ms, "bytes_per_launch": score_bytes_total},
         "end_to_end": {"algorithmic_bytes_per_step": alg_bytes_total, "achieved_gbs": e2e_gbs,
-                       "frac": e2e_gbs / HBM_PEAK_GBS, "streams": n_streams,
-                       "layer_ms_avg_in_stream": layer_ms_avg},
+                       "frac": e2e_gbs / HBM_PEAK_GBS},
     }
     if not args.no_cpu_baseline:
         log("bench: timing the fp64 oracle on a bounded sample")
-        result["cpu_baseline"] = cpu_baseline(layers[0], w, args.cpu_seconds)
+        result["cpu_baseline"] = cpu_baseline(layers, w, args.cpu_seconds)
     print(json.dumps(result), flush=True)
 
 

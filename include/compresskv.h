@@ -17,7 +17,8 @@
  * sets from an offline calibration (section 3.2, equation 1); both are inputs.
  *
  * Conventions shared by every entry point:
- *   - Pointers are DEVICE pointers unless the name ends in _host.  The caller
+ *   - Pointers are DEVICE pointers unless the name ends in _host (host memory;
+ *     a _ptrs_host array holds device pointers).  The caller
  *     owns every buffer; the library never allocates, frees or synchronizes.
  *   - All work is enqueued on `stream` (a hipStream_t; NULL = default stream).
  *     CKV_OK means "enqueued"; kernel faults surface at the caller's next sync.
@@ -130,6 +131,49 @@ int compresskv_compress_layer(const ckv_problem *p, const void *q_win, const voi
                               const void *v, const uint8_t *srh_mask_host, int32_t budget,
                               int32_t *idx, void *k_out, void *v_out, float *scores_or_null,
                               void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Multi-layer calls.  A model's layers share one problem (shapes, cu_seqlens,
+ * strides, options) and differ in their operands, SRH masks and budgets
+ * (section 3.4 gives every layer its own budget; section 3.2 every layer its
+ * own SRHs).  Per-layer DEVICE pointers are passed in HOST arrays of n_layers
+ * entries (names ending in _ptrs_host); srh_masks_host is uint8
+ * [n_layers][n_q_heads] and budgets_host int32 [n_layers], both host memory.
+ * Every layer is validated before anything is enqueued; the work of all
+ * layers is enqueued as a few launches (each kernel covers every layer), so
+ * per-layer launch costs and the HBM ramp of a kernel are paid once per call.
+ * Results are bit-identical to per-layer compresskv_compress_layer calls.
+ * n_layers * batch <= 65535.
+ */
+
+/* Workspace bytes of the multi-layer calls for this problem and these masks
+ * (independent of the budgets).  0 on invalid arguments. */
+size_t compresskv_layers_workspace_bytes(const ckv_problem *p, int32_t n_layers,
+                                         const uint8_t *srh_masks_host);
+
+/*
+ * S1-S4 for n_layers layers: scores [n_layers][n_kv_heads][T] fp32 (device),
+ * layer l laid out as compresskv_score writes it.  Each layer's SRH groups
+ * obey compresskv_score's limit (ceil(W/16) * SRHs per group <= 12).
+ */
+int compresskv_score_layers(const ckv_problem *p, int32_t n_layers,
+                            const void *const *q_win_ptrs_host, const void *const *k_ptrs_host,
+                            const uint8_t *srh_masks_host, float *scores, void *ws,
+                            size_t ws_bytes, void *stream);
+
+/*
+ * S1-S6 for n_layers layers (the per-layer budget vector of the method): layer
+ * l reads q_win_ptrs_host[l], k_ptrs_host[l], v_ptrs_host[l] and writes
+ * idx_ptrs_host[l] [batch, n_kv_heads, budgets_host[l]] and k_out/v_out
+ * [batch, n_kv_heads, budgets_host[l], D] as compresskv_compress_layer does.
+ * scores_or_null: NULL or device [n_layers][n_kv_heads][T] fp32.
+ */
+int compresskv_compress_layers(const ckv_problem *p, int32_t n_layers,
+                               const void *const *q_win_ptrs_host, const void *const *k_ptrs_host,
+                               const void *const *v_ptrs_host, const uint8_t *srh_masks_host,
+                               const int32_t *budgets_host, int32_t *const *idx_ptrs_host,
+                               void *const *k_out_ptrs_host, void *const *v_out_ptrs_host,
+                               float *scores_or_null, void *ws, size_t ws_bytes, void *stream);
 
 /*
  * Which scoring implementation compresskv_score / _compress_layer will use for

@@ -15,7 +15,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIBDIR = os.path.join(HERE, "lib")
 LIBNAME = "libcompresskv.so"
-SOURCES = ["api.hip", "score_kernels.hip", "fused_score.hip", "select_gather_kernels.hip"]
+SOURCES = ["api.hip", "score_kernels.hip", "score_layers.hip", "fused_score.hip",
+           "select_gather_kernels.hip"]
 ARCH = "gfx950"
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",

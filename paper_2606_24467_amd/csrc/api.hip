@@ -35,24 +35,33 @@ bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) %
 
 int elem_size(const ckv_problem *p) { return p->dtype == CKV_BF16 ? 2 : 4; }
 
+// SRH lists of one layer, from its host mask.
+struct LayerSrh {
+  std::vector<uint16_t> off;   // [Hkv + 1]
+  std::vector<uint8_t> head;   // [n SRHs]
+  int nmax = 0;                // most SRHs in one group
+};
+
 // Everything derived from a validated problem.
 struct Plan {
   int64_t T = 0;
   int lmax = 0;
-  int64_t n_keys = 0;
+  int n_layers = 1;    // layers of a multi-layer call (1 otherwise)
   int th = 0;          // row tiles per SRH
-  int rt_max = 0;      // max row tiles of a group
+  int rt_max = 0;      // max row tiles of a group (over the layers)
   int chunk1 = 0, max_chunks1 = 0;
   int chunk2 = 0, max_chunks2 = 0;
-  size_t scores_off = 0, stats_off = 0, counters_off = 0, hist_off = 0, total = 0;
+  uint32_t head_end_mask = 0;
+  // single-layer workspace: scores | stats | counters | histograms
+  // multi-layer workspace:  table | scores | stats | histograms (all per layer)
+  size_t table_off = 0, scores_off = 0, stats_off = 0, counters_off = 0, hist_off = 0, total = 0;
+  int64_t stats_layer = 0, hist_layer = 0;   // elements per layer
   bool fused = false;      // single-pass scoring kernel
   int unit_tiles = 4;      // its key tiles per wave per unit
   int n_units_max = 0;     // its units per (sequence, group), largest
   int n_counters = 0;      // ints zeroed before it (ticket, fallbacks, arrivals, histograms)
-  std::vector<uint16_t> srh_off;
-  std::vector<uint8_t> srh_head;
-  uint32_t head_end_mask = 0;
   int max_parts = 0;       // partial-statistics slots per group in the workspace
+  LayerSrh srh;            // single-layer calls
 };
 
 int env_int(const char *name, int dflt) {
@@ -62,7 +71,9 @@ int env_int(const char *name, int dflt) {
 }
 
 // Keys per workgroup: the smallest power of two >= lo such that doubling it
-// would leave fewer than `target` workgroups, capped at hi.
+// would leave fewer than `target` workgroups for one layer, capped at hi.  It
+// depends on the layer's shape only: the chunking fixes the merge order of the
+// partial row statistics, so multi-layer calls reproduce single-layer bits.
 int pick_chunk(const ckv_problem *p, int lo, int hi, int target) {
   int c = lo;
   while (c < hi) {
@@ -126,26 +137,34 @@ int check_problem(const ckv_problem *p) {
   return CKV_OK;
 }
 
-// Per-group SRH lists from the host mask.
-int check_mask(const ckv_problem *p, const uint8_t *mask, Plan &pl) {
+// Per-group SRH lists of one layer from its host mask (`layer` only names it
+// in messages).
+int layer_srh(const ckv_problem *p, const uint8_t *mask, int layer, LayerSrh &ls) {
   if (!mask) return fail(CKV_INVALID_ARGUMENT, "srh_mask_host is NULL");
   const int G = p->n_q_heads / p->n_kv_heads;
-  pl.th = (p->window + 15) / 16;
-  pl.srh_off.assign(p->n_kv_heads + 1, 0);
-  pl.srh_head.clear();
-  int nmax = 0;
+  ls.off.assign(p->n_kv_heads + 1, 0);
+  ls.head.clear();
+  ls.nmax = 0;
   for (int g = 0; g < p->n_kv_heads; ++g) {
     int n = 0;
     for (int h = g * G; h < (g + 1) * G; ++h) {
       if (mask[h]) {
-        pl.srh_head.push_back((uint8_t)h);
+        ls.head.push_back((uint8_t)h);
         ++n;
       }
     }
-    if (n == 0) return fail(CKV_INVALID_ARGUMENT, "KV group %d has no Semantic Retrieval Head", g);
-    nmax = std::max(nmax, n);
-    pl.srh_off[g + 1] = (uint16_t)pl.srh_head.size();
+    if (n == 0)
+      return fail(CKV_INVALID_ARGUMENT, "layer %d: KV group %d has no Semantic Retrieval Head",
+                  layer, g);
+    ls.nmax = std::max(ls.nmax, n);
+    ls.off[g + 1] = (uint16_t)ls.head.size();
   }
+  return CKV_OK;
+}
+
+// Row tiles per SRH, the largest group, and the SRH-end bits of the row tiles.
+int set_row_tiles(const ckv_problem *p, int nmax, Plan &pl) {
+  pl.th = (p->window + 15) / 16;
   pl.rt_max = nmax * pl.th;
   if (pl.rt_max > 12)
     return fail(CKV_UNSUPPORTED,
@@ -155,6 +174,12 @@ int check_mask(const ckv_problem *p, const uint8_t *mask, Plan &pl) {
   for (int rt = 0; rt < 32; ++rt)
     if ((rt + 1) % pl.th == 0) pl.head_end_mask |= 1u << rt;
   return CKV_OK;
+}
+
+int check_mask(const ckv_problem *p, const uint8_t *mask, Plan &pl) {
+  int st;
+  if ((st = layer_srh(p, mask, 0, pl.srh))) return st;
+  return set_row_tiles(p, pl.srh.nmax, pl);
 }
 
 // Keys per fused unit: 16 keys x 4 waves x unit_tiles.
@@ -186,14 +211,14 @@ void choose_path(const ckv_problem *p, Plan &pl) {
   }
 }
 
-void make_plan(const ckv_problem *p, Plan &pl, bool decide_path) {
+// Chunk sizes of the two-kernel path: multiples of 512 keys (statistics: 8
+// waves x 2-tile groups, at least two groups per wave) and 992 + 32 halo keys
+// (column sums).
+void set_chunks(const ckv_problem *p, Plan &pl) {
   pl.T = p->cu_seqlens_host[p->batch];
   pl.lmax = 0;
   for (int b = 0; b < p->batch; ++b)
     pl.lmax = std::max(pl.lmax, p->cu_seqlens_host[b + 1] - p->cu_seqlens_host[b]);
-  // Keys per workgroup of the two-kernel path: multiples of 512 (statistics:
-  // 8 waves x 2-tile groups, at least two groups per wave) and 992 + 32 halo
-  // keys (column sums).
   int c1 = env_int("CKV_CHUNK1", 0), c2 = env_int("CKV_CHUNK2", 0);
   if (c1 <= 0 || c1 % 512 != 0) c1 = pick_chunk(p, 512, 4096, 256);
   if (c2 <= 0 || (c2 + 32) % 256 != 0 || c2 > ckv::kMaxChunk2) c2 = 992;
@@ -201,6 +226,11 @@ void make_plan(const ckv_problem *p, Plan &pl, bool decide_path) {
   pl.chunk2 = c2;
   pl.max_chunks1 = std::max(1, (pl.lmax + c1 - 1) / c1);
   pl.max_chunks2 = std::max(1, (pl.lmax + c2 - 1) / c2);
+}
+
+void make_plan(const ckv_problem *p, Plan &pl, bool decide_path) {
+  set_chunks(p, pl);
+  pl.n_layers = 1;
   if (decide_path) choose_path(p, pl);
   // partial row statistics: enough slots for either path's chunking, plus one
   // per group for the published normalisers of the single-pass kernel
@@ -217,17 +247,37 @@ void make_plan(const ckv_problem *p, Plan &pl, bool decide_path) {
   pl.n_counters = (int)((pl.hist_off - pl.counters_off) / sizeof(int) + groups * ckv::kHistBins);
   pl.total = pl.hist_off + round_up(groups * ckv::kHistBins * sizeof(int), 256);
   pl.max_parts = parts;
+  pl.stats_layer = 0;
+  pl.hist_layer = 0;
 }
 
-ckv::ScoreArgs score_args(const ckv_problem *p, const Plan &pl, const void *q, const void *k,
-                          float *scores, void *ws) {
+// Multi-layer workspace: the layer table, then per layer the scores, the
+// partial row statistics and the first-digit histograms.
+void make_plan_layers(const ckv_problem *p, int n_layers, Plan &pl) {
+  set_chunks(p, pl);
+  pl.n_layers = n_layers;
+  pl.fused = false;
+  pl.max_parts = pl.max_chunks1;
+  const size_t groups = (size_t)p->batch * p->n_kv_heads;
+  pl.stats_layer = (int64_t)(groups * pl.max_parts * (size_t)pl.rt_max * 16);
+  pl.hist_layer = (int64_t)(groups * ckv::kHistBins);
+  pl.table_off = 0;
+  pl.scores_off = round_up((size_t)n_layers * sizeof(ckv::LayerDesc), 256);
+  pl.stats_off = pl.scores_off +
+                 round_up((size_t)n_layers * p->n_kv_heads * pl.T * sizeof(float), 256);
+  pl.hist_off = pl.stats_off + round_up((size_t)n_layers * pl.stats_layer * sizeof(float2), 256);
+  pl.total = pl.hist_off + round_up((size_t)n_layers * pl.hist_layer * sizeof(int), 256);
+}
+
+// Fields of the scoring arguments shared by every layer.
+ckv::ScoreArgs score_args(const ckv_problem *p, const Plan &pl, void *ws) {
   ckv::ScoreArgs a{};
-  a.q = q;
-  a.k = k;
+  a.layers = nullptr;
   a.cu = p->cu_seqlens;
   a.stats = reinterpret_cast<float2 *>(static_cast<char *>(ws) + pl.stats_off);
-  a.scores = scores;
+  a.stats_layer = pl.stats_layer;
   a.hist = reinterpret_cast<int *>(static_cast<char *>(ws) + pl.hist_off);
+  a.hist_layer = pl.hist_layer;
   a.k_stride_tok = p->k_stride_tok;
   a.k_stride_head = p->k_stride_head;
   a.T = (int32_t)pl.T;
@@ -247,9 +297,26 @@ ckv::ScoreArgs score_args(const ckv_problem *p, const Plan &pl, const void *q, c
   a.pool_type = p->pool_type;
   a.reduce_order = p->reduce_order;
   a.head_end_mask = pl.head_end_mask;
-  for (size_t i = 0; i < pl.srh_off.size(); ++i) a.srh_off[i] = pl.srh_off[i];
-  for (size_t i = 0; i < pl.srh_head.size(); ++i) a.srh_head[i] = pl.srh_head[i];
   return a;
+}
+
+// The inline layer of a single-layer call.
+ckv::LayerDesc layer_desc(const LayerSrh *srh, const void *q, const void *k, const void *v,
+                          float *scores, int32_t *idx, void *k_out, void *v_out, int32_t budget) {
+  ckv::LayerDesc d{};
+  d.q = q;
+  d.k = k;
+  d.v = v;
+  d.scores = scores;
+  d.idx = idx;
+  d.k_out = k_out;
+  d.v_out = v_out;
+  d.budget = budget;
+  if (srh) {
+    for (size_t i = 0; i < srh->off.size(); ++i) d.srh_off[i] = srh->off[i];
+    for (size_t i = 0; i < srh->head.size(); ++i) d.srh_head[i] = srh->head[i];
+  }
+  return d;
 }
 
 int check_ptr(const void *ptr, const char *name, size_t align) {
@@ -280,44 +347,39 @@ int hip_status(hipError_t e, const char *what) {
   return CKV_OK;
 }
 
-ckv::SelectArgs select_args(const ckv_problem *p, const Plan &pl, const float *scores,
-                            const int *hist, int32_t budget, int32_t *idx) {
+ckv::SelectArgs select_args(const ckv_problem *p, const Plan &pl, const int *hist) {
   ckv::SelectArgs s{};
-  s.scores = scores;
+  s.layers = nullptr;
   s.hist = hist;
+  s.hist_layer = pl.hist_layer;
   s.cu = p->cu_seqlens;
-  s.idx = idx;
   s.T = (int32_t)pl.T;
   s.Hkv = p->n_kv_heads;
   s.W = p->window;
-  s.budget = budget;
+  s.batch = p->batch;
   return s;
 }
 
-ckv::GatherArgs gather_args(const ckv_problem *p, const void *k, const void *v, const int32_t *idx,
-                            int32_t budget, void *k_out, void *v_out) {
+ckv::GatherArgs gather_args(const ckv_problem *p) {
   const int es = elem_size(p);
   ckv::GatherArgs g{};
-  g.k = static_cast<const char *>(k);
-  g.v = static_cast<const char *>(v);
+  g.layers = nullptr;
   g.cu = p->cu_seqlens;
-  g.idx = idx;
-  g.k_out = static_cast<char *>(k_out);
-  g.v_out = static_cast<char *>(v_out);
   g.k_stride_tok = p->k_stride_tok * es;
   g.k_stride_head = p->k_stride_head * es;
   g.v_stride_tok = p->v_stride_tok * es;
   g.v_stride_head = p->v_stride_head * es;
   g.Hkv = p->n_kv_heads;
-  g.budget = budget;
+  g.batch = p->batch;
   g.row_bytes = p->head_dim * es;
   return g;
 }
 
-// S1-S4 on the path the plan chose.
+// S1-S4 of a single-layer call on the path the plan chose.
 hipError_t launch_scoring(const ckv_problem *p, const Plan &pl, const void *q, const void *k,
                           float *scores, void *ws, hipStream_t stream) {
-  ckv::ScoreArgs a = score_args(p, pl, q, k, scores, ws);
+  ckv::ScoreArgs a = score_args(p, pl, ws);
+  a.l0 = layer_desc(&pl.srh, q, k, nullptr, scores, nullptr, nullptr, nullptr, 0);
   if (!pl.fused)
     return ckv::launch_score(a, p->dtype == CKV_BF16, p->head_dim, pl.rt_max, p->batch, stream);
   ckv::FusedArgs f{};
@@ -338,6 +400,134 @@ hipError_t launch_scoring(const ckv_problem *p, const Plan &pl, const void *q, c
   f.n_units_total = acc;
   return ckv::launch_fused_score(f, p->dtype == CKV_BF16, p->head_dim, pl.rt_max, pl.unit_tiles,
                                  pl.n_counters, stream);
+}
+
+// Host-side arrays of a multi-layer call (entries may be NULL where the call
+// does not use them).
+struct LayerPtrs {
+  const void *const *q = nullptr, *const *k = nullptr, *const *v = nullptr;
+  int32_t *const *idx = nullptr;
+  void *const *k_out = nullptr, *const *v_out = nullptr;
+  const int32_t *budgets = nullptr;
+};
+
+// Validation of a multi-layer call: every layer's SRH mask (-> pl.rt_max) and,
+// where given, its budget and pointers.
+int check_layers(const ckv_problem *p, int n_layers, const uint8_t *masks, const LayerPtrs &lp,
+                 Plan &pl, std::vector<uint32_t> *bits) {
+  if (n_layers < 1) return fail(CKV_INVALID_ARGUMENT, "n_layers must be >= 1 (got %d)", n_layers);
+  if ((int64_t)n_layers * p->batch > 65535)
+    return fail(CKV_UNSUPPORTED, "n_layers * batch must be <= 65535");
+  if (!masks) return fail(CKV_INVALID_ARGUMENT, "srh_masks_host is NULL");
+  int nmax = 0, st;
+  LayerSrh ls;
+  if (bits) bits->assign((size_t)n_layers * (ckv::kMaxQHeads / 32), 0u);
+  for (int l = 0; l < n_layers; ++l) {
+    const uint8_t *m = masks + (size_t)l * p->n_q_heads;
+    if ((st = layer_srh(p, m, l, ls))) return st;
+    nmax = std::max(nmax, ls.nmax);
+    if (bits)
+      for (int h = 0; h < p->n_q_heads; ++h)
+        if (m[h]) (*bits)[(size_t)l * (ckv::kMaxQHeads / 32) + h / 32] |= 1u << (h % 32);
+  }
+  if ((st = set_row_tiles(p, nmax, pl))) return st;
+  char name[64];
+  for (int l = 0; l < n_layers; ++l) {
+    if (lp.budgets) {
+      if (lp.budgets[l] < p->window)
+        return fail(CKV_INVALID_ARGUMENT, "layer %d: budget (%d) must be >= window (%d)", l,
+                    lp.budgets[l], p->window);
+    }
+    struct {
+      const void *ptr;
+      const char *what;
+      size_t align;
+    } checks[] = {{lp.q ? lp.q[l] : nullptr, "q_win", 16}, {lp.k ? lp.k[l] : nullptr, "k", 16},
+                  {lp.v ? lp.v[l] : nullptr, "v", 16},     {lp.idx ? lp.idx[l] : nullptr, "idx", 4},
+                  {lp.k_out ? lp.k_out[l] : nullptr, "k_out", 16},
+                  {lp.v_out ? lp.v_out[l] : nullptr, "v_out", 16}};
+    const void *const *arrays[] = {(const void *const *)lp.q, (const void *const *)lp.k,
+                                   (const void *const *)lp.v, (const void *const *)lp.idx,
+                                   (const void *const *)lp.k_out, (const void *const *)lp.v_out};
+    for (int i = 0; i < 6; ++i) {
+      if (!arrays[i]) continue;   // not used by this call
+      snprintf(name, sizeof name, "layer %d: %s", l, checks[i].what);
+      if ((st = check_ptr(checks[i].ptr, name, checks[i].align))) return st;
+    }
+  }
+  return CKV_OK;
+}
+
+// Enqueue the table writes of a multi-layer call.
+hipError_t put_layers(const ckv_problem *p, const Plan &pl, int n_layers, const LayerPtrs &lp,
+                      const std::vector<uint32_t> &bits, float *scores, void *ws,
+                      hipStream_t stream) {
+  ckv::LayerDesc *table =
+      reinterpret_cast<ckv::LayerDesc *>(static_cast<char *>(ws) + pl.table_off);
+  const size_t per_layer_scores = (size_t)p->n_kv_heads * pl.T;
+  for (int first = 0; first < n_layers; first += ckv::kPutLayers) {
+    ckv::PutArgs a{};
+    a.table = table;
+    a.first = first;
+    a.count = std::min(ckv::kPutLayers, n_layers - first);
+    a.Hq = p->n_q_heads;
+    a.Hkv = p->n_kv_heads;
+    for (int i = 0; i < a.count; ++i) {
+      const int l = first + i;
+      ckv::PutEntry &e = a.e[i];
+      e.q = lp.q ? lp.q[l] : nullptr;
+      e.k = lp.k ? lp.k[l] : nullptr;
+      e.v = lp.v ? lp.v[l] : nullptr;
+      e.scores = scores + (size_t)l * per_layer_scores;
+      e.idx = lp.idx ? lp.idx[l] : nullptr;
+      e.k_out = lp.k_out ? lp.k_out[l] : nullptr;
+      e.v_out = lp.v_out ? lp.v_out[l] : nullptr;
+      e.budget = lp.budgets ? lp.budgets[l] : 0;
+      for (int w = 0; w < ckv::kMaxQHeads / 32; ++w)
+        e.srh_bits[w] = bits[(size_t)l * (ckv::kMaxQHeads / 32) + w];
+    }
+    hipError_t err = ckv::launch_put_layers(a, stream);
+    if (err != hipSuccess) return err;
+  }
+  return hipSuccess;
+}
+
+// S1-S4 (and, with budgets, S5-S6) of a multi-layer call.
+int run_layers(const ckv_problem *p, int n_layers, const LayerPtrs &lp, const uint8_t *masks,
+               float *scores_or_null, void *ws, size_t ws_bytes, void *stream, bool full) {
+  Plan pl;
+  std::vector<uint32_t> bits;
+  int st;
+  if ((st = check_problem(p))) return st;
+  if ((st = check_layers(p, n_layers, masks, lp, pl, &bits))) return st;
+  if (!full && (st = check_ptr(scores_or_null, "scores", 4))) return st;
+  if (scores_or_null && (st = check_ptr(scores_or_null, "scores", 4))) return st;
+  make_plan_layers(p, n_layers, pl);
+  if ((st = check_ws(pl, ws, ws_bytes))) return st;
+  float *scores = scores_or_null
+                      ? scores_or_null
+                      : reinterpret_cast<float *>(static_cast<char *>(ws) + pl.scores_off);
+  hipStream_t s = (hipStream_t)stream;
+  if ((st = hip_status(put_layers(p, pl, n_layers, lp, bits, scores, ws, s), "layer table")))
+    return st;
+  const ckv::LayerDesc *table =
+      reinterpret_cast<const ckv::LayerDesc *>(static_cast<char *>(ws) + pl.table_off);
+  ckv::ScoreArgs a = score_args(p, pl, ws);
+  a.layers = table;
+  if ((st = hip_status(ckv::launch_score_layers(a, p->dtype == CKV_BF16, p->head_dim, pl.rt_max,
+                                                p->batch, n_layers, s),
+                       "score")))
+    return st;
+  if (!full) return ok();
+  ckv::SelectArgs sa = select_args(p, pl, a.hist);
+  sa.layers = table;
+  if ((st = hip_status(ckv::launch_select(sa, n_layers, s), "select"))) return st;
+  ckv::GatherArgs ga = gather_args(p);
+  ga.layers = table;
+  int max_budget = 0;
+  for (int l = 0; l < n_layers; ++l) max_budget = std::max(max_budget, lp.budgets[l]);
+  if ((st = hip_status(ckv::launch_gather(ga, n_layers, max_budget, s), "gather"))) return st;
+  return ok();
 }
 
 }  // namespace
@@ -405,10 +595,10 @@ int compresskv_select(const ckv_problem *p, const float *scores, int32_t budget,
   if ((st = check_ptr(scores, "scores", 4)) || (st = check_ptr(idx, "idx", 4))) return st;
   Plan pl;
   pl.T = p->cu_seqlens_host[p->batch];
-  if ((st = hip_status(ckv::launch_select(select_args(p, pl, scores, nullptr, budget, idx),
-                                          p->batch, (hipStream_t)stream),
-                       "select")))
-    return st;
+  ckv::SelectArgs sa = select_args(p, pl, nullptr);
+  sa.l0 = layer_desc(nullptr, nullptr, nullptr, nullptr, const_cast<float *>(scores), idx,
+                     nullptr, nullptr, budget);
+  if ((st = hip_status(ckv::launch_select(sa, 0, (hipStream_t)stream), "select"))) return st;
   return ok();
 }
 
@@ -421,9 +611,10 @@ int compresskv_gather(const ckv_problem *p, const void *k, const void *v, const 
       (st = check_ptr(idx, "idx", 4)) || (st = check_ptr(k_out, "k_out", 16)) ||
       (st = check_ptr(v_out, "v_out", 16)))
     return st;
-  if ((st = hip_status(ckv::launch_gather(gather_args(p, k, v, idx, budget, k_out, v_out),
-                                          p->batch, (hipStream_t)stream),
-                       "gather")))
+  ckv::GatherArgs ga = gather_args(p);
+  ga.l0 = layer_desc(nullptr, nullptr, k, v, nullptr, const_cast<int32_t *>(idx), k_out, v_out,
+                     budget);
+  if ((st = hip_status(ckv::launch_gather(ga, 0, budget, (hipStream_t)stream), "gather")))
     return st;
   return ok();
 }
@@ -451,15 +642,55 @@ int compresskv_compress_layer(const ckv_problem *p, const void *q_win, const voi
   hipStream_t s = (hipStream_t)stream;
   if ((st = hip_status(launch_scoring(p, pl, q_win, k, scores, ws, s), "score"))) return st;
   const int *hist = reinterpret_cast<const int *>(static_cast<char *>(ws) + pl.hist_off);
-  if ((st = hip_status(
-           ckv::launch_select(select_args(p, pl, scores, hist, budget, idx), p->batch, s),
-           "select")))
-    return st;
-  if ((st = hip_status(
-           ckv::launch_gather(gather_args(p, k, v, idx, budget, k_out, v_out), p->batch, s),
-           "gather")))
-    return st;
+  ckv::SelectArgs sa = select_args(p, pl, hist);
+  sa.l0 = layer_desc(nullptr, nullptr, nullptr, nullptr, scores, idx, nullptr, nullptr, budget);
+  if ((st = hip_status(ckv::launch_select(sa, 0, s), "select"))) return st;
+  ckv::GatherArgs ga = gather_args(p);
+  ga.l0 = layer_desc(nullptr, nullptr, k, v, nullptr, idx, k_out, v_out, budget);
+  if ((st = hip_status(ckv::launch_gather(ga, 0, budget, s), "gather"))) return st;
   return ok();
+}
+
+size_t compresskv_layers_workspace_bytes(const ckv_problem *p, int32_t n_layers,
+                                         const uint8_t *srh_masks_host) {
+  Plan pl;
+  if (check_problem(p) || check_layers(p, n_layers, srh_masks_host, LayerPtrs{}, pl, nullptr))
+    return 0;
+  make_plan_layers(p, n_layers, pl);
+  ok();
+  return pl.total;
+}
+
+int compresskv_score_layers(const ckv_problem *p, int32_t n_layers,
+                            const void *const *q_win_ptrs_host, const void *const *k_ptrs_host,
+                            const uint8_t *srh_masks_host, float *scores, void *ws,
+                            size_t ws_bytes, void *stream) {
+  LayerPtrs lp;
+  if (!q_win_ptrs_host || !k_ptrs_host)
+    return fail(CKV_INVALID_ARGUMENT, "q_win_ptrs_host and k_ptrs_host are required");
+  lp.q = q_win_ptrs_host;
+  lp.k = k_ptrs_host;
+  return run_layers(p, n_layers, lp, srh_masks_host, scores, ws, ws_bytes, stream, false);
+}
+
+int compresskv_compress_layers(const ckv_problem *p, int32_t n_layers,
+                               const void *const *q_win_ptrs_host, const void *const *k_ptrs_host,
+                               const void *const *v_ptrs_host, const uint8_t *srh_masks_host,
+                               const int32_t *budgets_host, int32_t *const *idx_ptrs_host,
+                               void *const *k_out_ptrs_host, void *const *v_out_ptrs_host,
+                               float *scores_or_null, void *ws, size_t ws_bytes, void *stream) {
+  if (!q_win_ptrs_host || !k_ptrs_host || !v_ptrs_host || !budgets_host || !idx_ptrs_host ||
+      !k_out_ptrs_host || !v_out_ptrs_host)
+    return fail(CKV_INVALID_ARGUMENT, "every per-layer host array is required");
+  LayerPtrs lp;
+  lp.q = q_win_ptrs_host;
+  lp.k = k_ptrs_host;
+  lp.v = v_ptrs_host;
+  lp.idx = idx_ptrs_host;
+  lp.k_out = k_out_ptrs_host;
+  lp.v_out = v_out_ptrs_host;
+  lp.budgets = budgets_host;
+  return run_layers(p, n_layers, lp, srh_masks_host, scores_or_null, ws, ws_bytes, stream, true);
 }
 
 }  // extern "C"

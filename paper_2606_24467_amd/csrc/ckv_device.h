@@ -29,28 +29,53 @@ __device__ __forceinline__ int hist_bin(uint32_t u) { return (int)((u >> 20) & 0
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-// Arguments of the two scoring kernels (one layer).
-struct ScoreArgs {
+// Operands of one layer.  Single-layer calls pass one inline in the kernel
+// arguments; the multi-layer entry point keeps a table of them in device
+// memory (written by put_layers_kernel) and the kernels index it by layer.
+struct alignas(16) LayerDesc {
   const void *q;          // [batch, W, Hq, D]
-  const void *k;          // [T, Hkv, D] with strides below (elements)
-  const int32_t *cu;      // [batch+1] sequence offsets
-  float2 *stats;          // [batch][Hkv][max_chunks1][row_slots] partial (ref, sum)
+  const void *k, *v;      // [T, Hkv, D] with the problem's strides (elements)
   float *scores;          // [Hkv][T]
-  int *hist;              // [batch][Hkv][kHistBins] counts of the first selection digit
+  int32_t *idx;           // [batch][Hkv][budget]
+  void *k_out, *v_out;    // [batch][Hkv][budget][D]
+  int32_t budget;
+  int32_t reserved;
+  uint16_t srh_off[kMaxKvHeads + 1];   // SRHs of group g: srh_head[srh_off[g] .. srh_off[g+1])
+  uint8_t srh_head[kMaxQHeads];        // query-head indices, ascending within a group
+};
+
+// The layer a workgroup works on: the inline one, or entry `layer` of the table.
+template <bool ML, typename A>
+__device__ __forceinline__ const LayerDesc &layer_desc(const A &a, int layer) {
+  if constexpr (ML) {
+    return a.layers[layer];
+  } else {
+    (void)layer;
+    return a.l0;
+  }
+}
+
+// Arguments of the scoring kernels.
+struct ScoreArgs {
+  LayerDesc l0;            // single-layer calls
+  const LayerDesc *layers; // multi-layer calls: [n_layers]
+  const int32_t *cu;       // [batch+1] sequence offsets
+  float2 *stats;           // per layer: [batch][Hkv][max_chunks1][row_slots] partial (ref, sum)
+  int64_t stats_layer;     // float2 elements between layers
+  int *hist;               // per layer: [batch][Hkv][kHistBins] first selection digit counts
+  int64_t hist_layer;      // ints between layers
   int64_t k_stride_tok, k_stride_head;
   int32_t T, batch, Hq, Hkv, W;
   int32_t th;             // 16-row tiles per SRH: ceil(W / 16)
   int32_t row_slots;      // padded rows per (sequence, group, chunk) in stats
-  int32_t chunk1, max_chunks1;   // keys per workgroup in the statistics pass
+  int32_t chunk1, max_chunks1;   // keys per workgroup in the statistics pass, partial slots
   int32_t chunk2, max_chunks2;   // keys per workgroup in the column-sum pass
   float c1;               // softmax scale * log2(e): logits in base-2 units
   int32_t pool_kernel, pool_type, reduce_order;
   uint32_t head_end_mask;  // bit rt set if row tile rt is the last tile of an SRH
-  uint16_t srh_off[kMaxKvHeads + 1];   // SRHs of group g: srh_head[srh_off[g] .. srh_off[g+1])
-  uint8_t srh_head[kMaxQHeads];        // query-head indices
 };
 
-// Arguments of the single-pass scoring kernel.
+// Arguments of the single-pass scoring kernel (single-layer calls).
 struct FusedArgs {
   ScoreArgs s;             // s.stats holds the published partials: [group][unit][row]
   int *ticket;             // one counter
@@ -63,20 +88,37 @@ struct FusedArgs {
 };
 
 struct SelectArgs {
-  const float *scores;    // [Hkv][T]
-  const int *hist;        // [batch][Hkv][kHistBins] or NULL (then counted here)
+  LayerDesc l0;            // uses scores, idx, budget
+  const LayerDesc *layers;
+  const int *hist;         // per layer [batch][Hkv][kHistBins], or NULL (then counted here)
+  int64_t hist_layer;
   const int32_t *cu;
-  int32_t *idx;           // [batch][Hkv][budget]
-  int32_t T, Hkv, W, budget;
+  int32_t T, Hkv, W, batch;
 };
 
 struct GatherArgs {
-  const char *k, *v;
+  LayerDesc l0;            // uses k, v, idx, k_out, v_out, budget
+  const LayerDesc *layers;
   const int32_t *cu;
-  const int32_t *idx;
-  char *k_out, *v_out;
   int64_t k_stride_tok, k_stride_head, v_stride_tok, v_stride_head;  // bytes
-  int32_t Hkv, budget, row_bytes;
+  int32_t Hkv, batch, row_bytes;
+};
+
+// One layer of the table as the host hands it over (SRH mask as bits over the
+// query heads); put_layers_kernel expands the mask into per-group lists.
+constexpr int kPutLayers = 8;
+struct PutEntry {
+  const void *q, *k, *v;
+  float *scores;
+  int32_t *idx;
+  void *k_out, *v_out;
+  int32_t budget;
+  uint32_t srh_bits[kMaxQHeads / 32];
+};
+struct PutArgs {
+  LayerDesc *table;
+  int32_t first, count, Hq, Hkv;
+  PutEntry e[kPutLayers];
 };
 
 // 16-byte slices per row per quad: D * sizeof(T) / 64.

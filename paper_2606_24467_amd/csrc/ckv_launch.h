@@ -8,7 +8,14 @@ namespace ckv {
 // Enqueue the statistics and column-sum kernels; rt_max = max SRH row tiles of a group.
 hipError_t launch_score(const ScoreArgs &a, int dtype_bf16, int head_dim, int rt_max, int batch,
                         hipStream_t stream);
-hipError_t launch_select(const SelectArgs &a, int batch, hipStream_t stream);
+// Multi-layer scoring: grid z = batch * n_layers, operands from a.layers.
+hipError_t launch_score_layers(const ScoreArgs &a, int dtype_bf16, int head_dim, int rt_max,
+                               int batch, int n_layers, hipStream_t stream);
+// Selection and gather; n_layers > 0 reads the operands from the table
+// (a.layers), n_layers == 0 from a.l0.
+hipError_t launch_select(const SelectArgs &a, int n_layers, hipStream_t stream);
+// Writes table entries [first, first + count) from a.e (count <= kPutLayers).
+hipError_t launch_put_layers(const PutArgs &a, hipStream_t stream);
 
 // Single-pass scoring (fused_score.hip).
 struct FusedArgs;
@@ -16,6 +23,7 @@ constexpr int kFusedMaxBatch = 64;
 hipError_t launch_fused_score(const FusedArgs &f, int dtype_bf16, int head_dim, int rt_max,
                               int unit_tiles, int counters, hipStream_t stream);
 int fused_resident_workgroups(int dtype_bf16, int head_dim, int rt_max, int unit_tiles);
-hipError_t launch_gather(const GatherArgs &a, int batch, hipStream_t stream);
+// max_budget: the largest budget over the layers (sizes the grid).
+hipError_t launch_gather(const GatherArgs &a, int n_layers, int max_budget, hipStream_t stream);
 
 }  // namespace ckv

@@ -36,13 +36,13 @@ __global__ __launch_bounds__(256) void fill_kernel(int *p, int n) {
 
 // Keys of a unit: tile w + NW*i (i < UT) of wave w, clamped into [.., k_last].
 template <typename T, int D, int NW, int UT>
-__device__ __forceinline__ void load_unit(const ScoreArgs &a, int s0, int g, int u0, int k_last,
-                                          uint4 (&kf)[UT][Slices<T, D>::n]) {
+__device__ __forceinline__ void load_unit(const ScoreArgs &a, const char *kb, int s0, int g,
+                                          int u0, int k_last, uint4 (&kf)[UT][Slices<T, D>::n]) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int c = lane & 15, quad = lane >> 4;
 #pragma unroll
   for (int i = 0; i < UT; ++i)
-    load_k_row<T, D>(a, s0, min(u0 + 16 * (wave + NW * i) + c, k_last), g, quad, kf[i]);
+    load_k_row<T, D>(a, kb, s0, min(u0 + 16 * (wave + NW * i) + c, k_last), g, quad, kf[i]);
 }
 
 // Partial (ref, sum) statistics of every row over the keys of one unit held in
@@ -107,6 +107,8 @@ __global__ __launch_bounds__(64 * kFusedWaves) void fused_score_kernel(const Fus
   constexpr int kUnitKeys = 16 * NW * UT;
   constexpr int CSW = kUnitKeys + 32;
   const ScoreArgs &a = f.s;
+  const LayerDesc &ld = a.l0;
+  const char *kb = reinterpret_cast<const char *>(ld.k);
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int c = lane & 15, quad = lane >> 4;
@@ -132,21 +134,21 @@ __global__ __launch_bounds__(64 * kFusedWaves) void fused_score_kernel(const Fus
   const int gi = b * a.Hkv + g;
   const int u0 = u * kUnitKeys;
   const int P = L - a.W;
-  const int off = a.srh_off[g];
-  const int nh = a.srh_off[g + 1] - off;
+  const int off = ld.srh_off[g];
+  const int nh = ld.srh_off[g + 1] - off;
   const int rt_n = nh * a.th;
   const int rows = rt_n * 16;
 
   // Loads: queries, the unit's keys, then the pooling halo tiles (wave 0: the
   // tile before the unit, wave 1: the tile after it).
   uint4 qv[QStage<T, D, RTM, NT>::n];
-  q_load<T, D, RTM, NT>(a, b, off, rt_n, qv);
+  q_load<T, D, RTM, NT>(a, ld, b, off, rt_n, qv);
   uint4 kf[UT][NS];
-  load_unit<T, D, NW, UT>(a, s0, g, u0, min(L, u0 + kUnitKeys) - 1, kf);
+  load_unit<T, D, NW, UT>(a, kb, s0, g, u0, min(L, u0 + kUnitKeys) - 1, kf);
   const int halo_base = (wave == 0) ? u0 - 16 : u0 + kUnitKeys;
   const bool halo_ok = (wave < 2) && halo_base >= 0 && halo_base < P;
   uint4 kh[NS];
-  if (wave < 2) load_k_row<T, D>(a, s0, halo_ok ? min(halo_base + c, L - 1) : L - 1, g, quad, kh);
+  if (wave < 2) load_k_row<T, D>(a, kb, s0, halo_ok ? min(halo_base + c, L - 1) : L - 1, g, quad, kh);
   q_store<T, D, RTM, NT>(qv, q_lds);
   for (int i = tid; i < kHistBins; i += NT) hist_s[i] = 0;
   __syncthreads();
@@ -221,7 +223,7 @@ __global__ __launch_bounds__(64 * kFusedWaves) void fused_score_kernel(const Fus
   if (wave < 2)
     tile_window_sums<T, D, RTM, CSW>(a, kh, qreg, q_lds, bias, rt_n,
                                      (wave == 0) ? -1 : kUnitKeys / 16, halo_ok, c, quad, cs);
-  float *out = a.scores + (int64_t)g * a.T + s0;
+  float *out = ld.scores + (int64_t)g * a.T + s0;
   // Window positions of the unit are always kept: +inf.
   for (int j = max(u0, P) + tid; j < min(L, u0 + kUnitKeys); j += NT) out[j] = INFINITY;
   __syncthreads();

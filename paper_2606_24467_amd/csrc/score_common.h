@@ -40,10 +40,10 @@ struct QStage {
 };
 
 template <typename T, int D, int RTM, int NT>
-__device__ __forceinline__ void q_load(const ScoreArgs &a, int b, int off, int rt_n,
-                                       uint4 (&qv)[QStage<T, D, RTM, NT>::n]) {
+__device__ __forceinline__ void q_load(const ScoreArgs &a, const LayerDesc &ld, int b, int off,
+                                       int rt_n, uint4 (&qv)[QStage<T, D, RTM, NT>::n]) {
   constexpr int U4 = QLayout<T, D>::U4;
-  const char *qb = reinterpret_cast<const char *>(a.q);
+  const char *qb = reinterpret_cast<const char *>(ld.q);
 #pragma unroll
   for (int it = 0; it < QStage<T, D, RTM, NT>::n; ++it) {
     const int idx = (int)threadIdx.x + it * NT;
@@ -53,7 +53,7 @@ __device__ __forceinline__ void q_load(const ScoreArgs &a, int b, int off, int r
     if (rt < rt_n) {
       const int i = (rt % a.th) * 16 + c;
       if (i < a.W) {
-        const int head = a.srh_head[off + rt / a.th];
+        const int head = ld.srh_head[off + rt / a.th];
         qv[it] = load16(qb + (((int64_t)b * a.W + i) * a.Hq + head) * (int64_t)(D * sizeof(T)) +
                         16 * u);
       }
@@ -78,11 +78,12 @@ __device__ __forceinline__ uint4 q_frag(const uint4 *q_lds, int rt, int s, int c
   return q_lds[(rt * 16 + c) * QLayout<T, D>::STRIDE + 4 * s + quad];
 }
 
-// Slices of one key row (key index clamped into the sequence).
+// Slices of one key row of the layer's K at kb (key index clamped into the
+// sequence by the callers).
 template <typename T, int D>
-__device__ __forceinline__ void load_k_row(const ScoreArgs &a, int s0, int key, int g, int quad,
-                                           uint4 (&out)[Slices<T, D>::n]) {
-  const char *p = reinterpret_cast<const char *>(a.k) +
+__device__ __forceinline__ void load_k_row(const ScoreArgs &a, const char *kb, int s0, int key,
+                                           int g, int quad, uint4 (&out)[Slices<T, D>::n]) {
+  const char *p = kb +
                   ((int64_t)(s0 + key) * a.k_stride_tok + (int64_t)g * a.k_stride_head) *
                       (int64_t)sizeof(T) +
                   16 * quad;

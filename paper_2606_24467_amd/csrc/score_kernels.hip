@@ -1,275 +1,12 @@
-// Scoring kernels of the CompressKV eviction path (steps S1-S4) for gfx950.
-//
-// The window softmax (section 3.3, SnapKV-style window of section 4) needs each
-// window row's statistics over the whole sequence before any column can be
-// normalised, so scoring runs in two kernels over K:
-//
-//   stats_kernel   S1+S2: per (sequence, KV group, key chunk) it computes the
-//                  logits of all SRH window rows against the chunk's keys on
-//                  MFMA and reduces them to a per-row partial (ref, sum) with
-//                  sum = sum_j exp2(y_j - ref), y = logit * log2(e).
-//   colsum_kernel  S2+S3+S4: merges the partials into each row's normaliser,
-//                  recomputes the logits of its chunk (plus a 16-key halo on
-//                  each side for pooling), sums the normalised probabilities
-//                  over the window rows of each SRH, pools along the token axis
-//                  in LDS, averages over the SRHs, and adds the scores to a
-//                  2048-bin histogram of their top bits (first digit of the
-//                  radix selection, S5).
-//
-// Rows of a KV group: SRH h (in head order) owns th = ceil(W/16) row tiles of
-// 16 rows; row i < W of the tile set is window query i of that head, the
-// padding rows have zero queries and are ignored.  A workgroup (8 waves)
-// stages the group's window queries in LDS once; each wave keeps them in
-// registers when they fit (up to 4 row tiles) and otherwise reads them from
-// LDS per MFMA.  Each wave streams its key tiles through a two-deep pipeline
-// of 2-tile groups (8 KB each): loads are unconditional (key index clamped
-// into the sequence, extra tiles masked), so the compiler can wait for exactly
-// the group being consumed while the next one is still in flight.
-#include "score_common.h"
+// Scoring kernels (S1-S4) for single-layer calls: operands in the arguments.
+#include "ckv_launch.h"
+#include "score_kernels.h"
 
 namespace ckv {
 
-// ---------------------------------------------------------------------------
-// S1+S2 partial statistics.  Grid (Hkv, max_chunks1, batch), 512 threads: the
-// groups of one key chunk are neighbours in launch order, so the workgroups in
-// flight read whole token rows of K ([T, Hkv, D]) rather than 1/Hkv of each.
-// MFMA operands: A = 16 keys, B = 16 window rows, so lane (quad, c) holds the
-// logits of row c against keys 4*quad .. 4*quad+3 of the tile and keeps one
-// running (ref, sum) pair per row tile.  Wave w handles the key tiles
-// w, w + 8, w + 16, ... of the chunk (chunk1 / 128 of them).
-// ---------------------------------------------------------------------------
-template <typename T, int D, int RTM>
-__global__ __launch_bounds__(64 * kWaves) void stats_kernel(const ScoreArgs a) {
-  constexpr int NS = Slices<T, D>::n, RQ = RegTiles<T, D, RTM>::v;
-  constexpr int NT = 64 * kWaves;
-  const int g = blockIdx.x, chunk = blockIdx.y, b = blockIdx.z;
-  const int s0 = a.cu[b];
-  const int L = a.cu[b + 1] - s0;
-  if (chunk == 0) {   // the column-sum kernel accumulates this histogram afterwards
-    int *h = a.hist + ((int64_t)b * a.Hkv + g) * kHistBins;
-    for (int i = threadIdx.x; i < kHistBins; i += NT) h[i] = 0;
-  }
-  const int c0 = chunk * a.chunk1;
-  if (c0 >= L) return;                       // uniform for the whole workgroup
-  const int P = L - a.W;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int c = lane & 15, quad = lane >> 4;
-  const int off = a.srh_off[g];
-  const int rt_n = (a.srh_off[g + 1] - off) * a.th;
-  const int n_groups = a.chunk1 / (16 * kWaves * kPair);   // 2-tile groups per wave
-  // key row of this lane for tile index i of this wave, clamped into the chunk
-  // (the pipeline's reads past the last tile hit the same cached row)
-  const int k_last = min(L, c0 + a.chunk1) - 1;
-  auto key_of = [&](int i) { return min(c0 + 16 * (wave + kWaves * i) + c, k_last); };
-
-  __shared__ uint4 q_lds[RTM * 16 * QLayout<T, D>::STRIDE];
-  __shared__ float2 part[kWaves][RTM * 16];
-
-  // Query loads first, then the first two key groups; the queries are written
-  // to LDS while the keys are still in flight.
-  uint4 qv[QStage<T, D, RTM, NT>::n];
-  q_load<T, D, RTM, NT>(a, b, off, rt_n, qv);
-  uint4 ka[kPair][NS], kb[kPair][NS];
-#pragma unroll
-  for (int p = 0; p < kPair; ++p) load_k_row<T, D>(a, s0, key_of(p), g, quad, ka[p]);
-#pragma unroll
-  for (int p = 0; p < kPair; ++p) load_k_row<T, D>(a, s0, key_of(kPair + p), g, quad, kb[p]);
-  q_store<T, D, RTM, NT>(qv, q_lds);
-  __syncthreads();
-  uint4 qreg[RegTiles<T, D, RTM>::n][NS];
-#pragma unroll
-  for (int rt = 0; rt < RQ; ++rt)
-#pragma unroll
-    for (int s = 0; s < NS; ++s) qreg[rt][s] = q_frag<T, D>(q_lds, rt, s, c, quad);
-
-  float ref[RTM], sum[RTM];
-#pragma unroll
-  for (int rt = 0; rt < RTM; ++rt) {
-    ref[rt] = -INFINITY;
-    sum[rt] = 0.f;
-  }
-  auto consume = [&](uint4 (&kf)[kPair][NS], int grp) {
-#pragma unroll
-    for (int p = 0; p < kPair; ++p) {
-      const int base = c0 + 16 * (wave + kWaves * (kPair * grp + p));
-      f32x4 acc[RTM];
-#pragma unroll
-      for (int rt = 0; rt < RTM; ++rt)
-        if (rt < rt_n) acc[rt] = tile_logits<T, D, RTM, true>(kf[p], qreg, q_lds, rt, c, quad);
-      stats_update<RTM>(a, acc, ref, sum, rt_n, base, L, P, c, quad);
-    }
-  };
-  for (int grp = 0; grp < n_groups; grp += 2) {
-    consume(ka, grp);
-#pragma unroll
-    for (int p = 0; p < kPair; ++p)
-      load_k_row<T, D>(a, s0, key_of(kPair * (grp + 2) + p), g, quad, ka[p]);
-    if (grp + 1 < n_groups) consume(kb, grp + 1);
-#pragma unroll
-    for (int p = 0; p < kPair; ++p)
-      load_k_row<T, D>(a, s0, key_of(kPair * (grp + 3) + p), g, quad, kb[p]);
-  }
-
-  // merge the four quads (same row c, different keys), then the waves
-#pragma unroll
-  for (int rt = 0; rt < RTM; ++rt) {
-#pragma unroll
-    for (int o = 16; o <= 32; o <<= 1) {
-      float ro = __shfl_xor(ref[rt], o);
-      float so = __shfl_xor(sum[rt], o);
-      merge_stats(ref[rt], sum[rt], ro, so);
-    }
-  }
-  if (quad == 0) {
-#pragma unroll
-    for (int rt = 0; rt < RTM; ++rt) part[wave][rt * 16 + c] = make_float2(ref[rt], sum[rt]);
-  }
-  __syncthreads();
-  const int tid = threadIdx.x;
-  if (tid < rt_n * 16) {
-    float r0 = part[0][tid].x, s_0 = part[0][tid].y;
-#pragma unroll
-    for (int w = 1; w < kWaves; ++w) merge_stats(r0, s_0, part[w][tid].x, part[w][tid].y);
-    a.stats[(((int64_t)b * a.Hkv + g) * a.max_chunks1 + chunk) * a.row_slots + tid] =
-        make_float2(r0, s_0);
-  }
-}
-
-// ---------------------------------------------------------------------------
-// S2+S3+S4.  Grid (Hkv, max_chunks2, batch), 512 threads.
-// MFMA operands: A = 16 window rows, B = 16 keys, so lane (quad, c) holds
-// rows 4*quad .. 4*quad+3 of the tile against key c.  The tiles of a chunk
-// plus one halo tile on each side, e = -1 .. chunk2/16, go to the waves
-// round-robin (chunk2 + 32 keys = 16 * kWaves * kPair * n_groups).
-// ---------------------------------------------------------------------------
-template <typename T, int D, int RTM>
-__global__ __launch_bounds__(64 * kWaves) void colsum_kernel(const ScoreArgs a) {
-  constexpr int NS = Slices<T, D>::n, RQ = RegTiles<T, D, RTM>::v;
-  constexpr int NT = 64 * kWaves;
-  constexpr int kMaxSrh = RTM;   // th >= 1
-  const int g = blockIdx.x, chunk = blockIdx.y, b = blockIdx.z;
-  const int s0 = a.cu[b];
-  const int L = a.cu[b + 1] - s0;
-  const int c0 = chunk * a.chunk2;
-  if (c0 >= L) return;
-  const int c_end = min(L, c0 + a.chunk2);
-  const int P = L - a.W;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int c = lane & 15, quad = lane >> 4;
-  const int tid = threadIdx.x;
-  const int off = a.srh_off[g];
-  const int nh = a.srh_off[g + 1] - off;
-  const int rt_n = nh * a.th;
-  float *out = a.scores + (int64_t)g * a.T + s0;
-
-  // Window positions of this chunk are always kept: +inf.
-  for (int j = max(c0, P) + tid; j < c_end; j += NT) out[j] = INFINITY;
-  if (c0 >= P) return;                        // no prefix key in this chunk
-  const int p_end = min(c_end, P);
-  const int ntiles = (p_end - c0 + 15) >> 4;        // tiles e = 0 .. ntiles-1
-  const int e_lo = (c0 > 0) ? -1 : 0;               // left halo tile
-  const int e_hi = (c0 + 16 * ntiles < P) ? ntiles : ntiles - 1;   // right halo tile
-  const int n_groups = (a.chunk2 + 32) / (16 * kWaves * kPair);
-  // tile index e of this wave's i-th tile, and its key row for this lane
-  auto tile_of = [&](int i) { return -1 + wave + kWaves * i; };
-  const int k_first = max(c0 - 16, 0), k_last = min(c0 + a.chunk2 + 16, L) - 1;
-  auto key_of = [&](int i) { return min(max(c0 + 16 * tile_of(i) + c, k_first), k_last); };
-
-  __shared__ uint4 q_lds[RTM * 16 * QLayout<T, D>::STRIDE];
-  __shared__ float bias_s[RTM * 16];
-  __shared__ float cs[kMaxSrh][kMaxChunk2 + 32];
-  __shared__ int hist_s[kHistBins];
-  uint4 qv[QStage<T, D, RTM, NT>::n];
-  q_load<T, D, RTM, NT>(a, b, off, rt_n, qv);
-  uint4 ka[kPair][NS], kb[kPair][NS];
-#pragma unroll
-  for (int p = 0; p < kPair; ++p) load_k_row<T, D>(a, s0, key_of(p), g, quad, ka[p]);
-#pragma unroll
-  for (int p = 0; p < kPair; ++p) load_k_row<T, D>(a, s0, key_of(kPair + p), g, quad, kb[p]);
-  q_store<T, D, RTM, NT>(qv, q_lds);
-  for (int i = tid; i < kHistBins; i += NT) hist_s[i] = 0;
-
-  // Row normalisers bias = ref + log2(sum), merged over every chunk of the
-  // statistics pass.
-  merge_row_bias<NT>(a, a.stats + ((int64_t)b * a.Hkv + g) * a.max_chunks1 * a.row_slots,
-                     a.row_slots, (L + a.chunk1 - 1) / a.chunk1, rt_n * 16, RTM * 16, bias_s);
-  __syncthreads();
-  uint4 qreg[RegTiles<T, D, RTM>::n][NS];
-#pragma unroll
-  for (int rt = 0; rt < RQ; ++rt)
-#pragma unroll
-    for (int s = 0; s < NS; ++s) qreg[rt][s] = q_frag<T, D>(q_lds, rt, s, c, quad);
-  float bias[RTM][4];
-#pragma unroll
-  for (int rt = 0; rt < RTM; ++rt)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) bias[rt][r] = bias_s[rt * 16 + 4 * quad + r];
-
-  // Column sums of the chunk plus one 16-key halo tile on each side.
-  // cs[h][16 + x] holds the window sum of SRH h at key c0 + x.
-  auto consume = [&](uint4 (&kf)[kPair][NS], int grp) {
-#pragma unroll
-    for (int p = 0; p < kPair; ++p) {
-      const int e = tile_of(kPair * grp + p);
-      tile_window_sums<T, D, RTM, kMaxChunk2 + 32>(a, kf[p], qreg, q_lds, bias, rt_n, e, e >= e_lo && e <= e_hi,
-                                  c, quad, cs);
-    }
-  };
-  for (int grp = 0; grp < n_groups; grp += 2) {
-    consume(ka, grp);
-#pragma unroll
-    for (int p = 0; p < kPair; ++p)
-      load_k_row<T, D>(a, s0, key_of(kPair * (grp + 2) + p), g, quad, ka[p]);
-    if (grp + 1 < n_groups) consume(kb, grp + 1);
-#pragma unroll
-    for (int p = 0; p < kPair; ++p)
-      load_k_row<T, D>(a, s0, key_of(kPair * (grp + 3) + p), g, quad, kb[p]);
-  }
-  __syncthreads();
-
-  pool_scores<NT, kMaxChunk2 + 32>(a, cs, nh, c0, p_end, P, out, hist_s);
-  __syncthreads();
-  flush_hist<NT>(hist_s, a.hist + ((int64_t)b * a.Hkv + g) * kHistBins);
-}
-
-// ---------------------------------------------------------------------------
-// Host-side launchers (called by the C ABI after validation).
-// ---------------------------------------------------------------------------
-template <typename T, int D, int RTM>
-static hipError_t launch_score_t(const ScoreArgs &a, int batch, hipStream_t stream) {
-  dim3 block(64 * kWaves);
-  hipLaunchKernelGGL((stats_kernel<T, D, RTM>), dim3(a.Hkv, a.max_chunks1, batch), block, 0,
-                     stream, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((colsum_kernel<T, D, RTM>), dim3(a.Hkv, a.max_chunks2, batch), block, 0,
-                     stream, a);
-  return hipGetLastError();
-}
-
-template <typename T, int D>
-static hipError_t launch_score_d(const ScoreArgs &a, int rt_max, int batch, hipStream_t stream) {
-  switch (rt_max) {
-    case 1: return launch_score_t<T, D, 1>(a, batch, stream);
-    case 2: return launch_score_t<T, D, 2>(a, batch, stream);
-    case 3: return launch_score_t<T, D, 3>(a, batch, stream);
-    case 4: return launch_score_t<T, D, 4>(a, batch, stream);
-    case 5:
-    case 6: return launch_score_t<T, D, 6>(a, batch, stream);
-    case 7:
-    case 8: return launch_score_t<T, D, 8>(a, batch, stream);
-    default: return launch_score_t<T, D, 12>(a, batch, stream);
-  }
-}
-
 hipError_t launch_score(const ScoreArgs &a, int dtype_bf16, int head_dim, int rt_max, int batch,
                         hipStream_t stream) {
-  if (dtype_bf16) {
-    return head_dim == 64 ? launch_score_d<__bf16, 64>(a, rt_max, batch, stream)
-                          : launch_score_d<__bf16, 128>(a, rt_max, batch, stream);
-  }
-  return head_dim == 64 ? launch_score_d<float, 64>(a, rt_max, batch, stream)
-                        : launch_score_d<float, 128>(a, rt_max, batch, stream);
+  return launch_score_any<false>(a, dtype_bf16, head_dim, rt_max, batch, stream);
 }
 
 }  // namespace ckv

@@ -12,7 +12,10 @@
 //
 // S6 copies the kept K and V rows (section 3.3: the retained KV pairs form the
 // compressed cache) with 16-byte lanes; rows whose index is -1 become zeros.
-#include "ckv_device.h"
+//
+// ML (multi-layer): the grid's last dimension runs over (layer, sequence)
+// pairs, layer-major, and each layer's operands and budget come from the table.
+#include "ckv_launch.h"
 
 namespace ckv {
 
@@ -94,22 +97,27 @@ __device__ __forceinline__ void load_round(const uint32_t *sc, int P, int r0,
   for (int e = 0; e < kEpt; ++e) v[e] = (j0 + e < P) ? sc[j0 + e] : 0u;
 }
 
-// Grid (Hkv, batch), 1024 threads.
+// Grid (Hkv, batch [x layers]), 1024 threads.
+template <bool ML>
 __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a) {
-  const int g = blockIdx.x, b = blockIdx.y;
+  const int g = blockIdx.x;
+  const int layer = ML ? (int)blockIdx.y / a.batch : 0;
+  const int b = (int)blockIdx.y - layer * a.batch;
+  const LayerDesc &ld = layer_desc<ML>(a, layer);
+  const int budget = ld.budget;
   const int tid = threadIdx.x;
   const int s0 = a.cu[b];
   const int L = a.cu[b + 1] - s0;
-  int32_t *out = a.idx + ((int64_t)b * a.Hkv + g) * a.budget;
-  if (L <= a.budget) {
-    for (int j = tid; j < a.budget; j += kSelThreads) out[j] = (j < L) ? j : -1;
+  int32_t *out = ld.idx + ((int64_t)b * a.Hkv + g) * budget;
+  if (L <= budget) {
+    for (int j = tid; j < budget; j += kSelThreads) out[j] = (j < L) ? j : -1;
     return;
   }
   const int P = L - a.W;
-  const int k = a.budget - a.W;     // prefix tokens to keep, 0 <= k < P
+  const int k = budget - a.W;       // prefix tokens to keep, 0 <= k < P
   for (int w = tid; w < a.W; w += kSelThreads) out[k + w] = P + w;
   if (k == 0) return;
-  const uint32_t *sc = reinterpret_cast<const uint32_t *>(a.scores + (int64_t)g * a.T + s0);
+  const uint32_t *sc = reinterpret_cast<const uint32_t *>(ld.scores + (int64_t)g * a.T + s0);
   const int nrounds = (P + kRound - 1) / kRound;
   const bool resident = (nrounds == 1);   // scores stay in registers for every pass
 
@@ -124,7 +132,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a)
 
   // Digit 1: bits 30..20.
   if (a.hist) {
-    const int *hg = a.hist + ((int64_t)b * a.Hkv + g) * kHistBins;
+    const int *hg = a.hist + layer * a.hist_layer + ((int64_t)b * a.Hkv + g) * kHistBins;
     for (int i = tid; i < kHistBins; i += kSelThreads) hist[i] = hg[i];
   } else {
     for (int i = tid; i < kHistBins; i += kSelThreads) hist[i] = 0;
@@ -232,43 +240,96 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a)
   }
 }
 
-// Grid (ceil(budget / rows_per_block), Hkv, batch), 256 threads; each lane
-// moves 16 bytes, a row is row_bytes / 16 lanes.
+// Grid (ceil(max budget / rows_per_block), Hkv, batch [x layers]), 256
+// threads; each lane moves 16 bytes, a row is row_bytes / 16 lanes.
+template <bool ML>
 __global__ __launch_bounds__(256) void gather_kernel(const GatherArgs a) {
-  const int g = blockIdx.y, b = blockIdx.z;
+  const int g = blockIdx.y;
+  const int layer = ML ? (int)blockIdx.z / a.batch : 0;
+  const int b = (int)blockIdx.z - layer * a.batch;
+  const LayerDesc &ld = layer_desc<ML>(a, layer);
+  const int budget = ld.budget;
+  const char *kb = reinterpret_cast<const char *>(ld.k);
+  const char *vb = reinterpret_cast<const char *>(ld.v);
   const int lanes_per_row = a.row_bytes >> 4;
   const int rows_per_pass = 256 / lanes_per_row;
   const int sub = threadIdx.x % lanes_per_row;
   const int r_in = threadIdx.x / lanes_per_row;
   const int s0 = a.cu[b];
   const int L = a.cu[b + 1] - s0;
-  const int64_t obase = ((int64_t)b * a.Hkv + g) * a.budget;
+  const int64_t obase = ((int64_t)b * a.Hkv + g) * budget;
   {
     const int r = blockIdx.x * rows_per_pass + r_in;
-    if (r >= a.budget) return;
-    const int j = a.idx[obase + r];
+    if (r >= budget) return;
+    const int j = ld.idx[obase + r];
     uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
     if (j >= 0 && j < L) {   // anything else is a dropped slot: zeros
-      kv = load16(a.k + (int64_t)(s0 + j) * a.k_stride_tok + (int64_t)g * a.k_stride_head +
+      kv = load16(kb + (int64_t)(s0 + j) * a.k_stride_tok + (int64_t)g * a.k_stride_head +
                   16 * sub);
-      vv = load16(a.v + (int64_t)(s0 + j) * a.v_stride_tok + (int64_t)g * a.v_stride_head +
+      vv = load16(vb + (int64_t)(s0 + j) * a.v_stride_tok + (int64_t)g * a.v_stride_head +
                   16 * sub);
     }
     const int64_t o = (obase + r) * a.row_bytes + 16 * sub;
-    *reinterpret_cast<uint4 *>(a.k_out + o) = kv;
-    *reinterpret_cast<uint4 *>(a.v_out + o) = vv;
+    *reinterpret_cast<uint4 *>(static_cast<char *>(ld.k_out) + o) = kv;
+    *reinterpret_cast<uint4 *>(static_cast<char *>(ld.v_out) + o) = vv;
   }
 }
 
-hipError_t launch_select(const SelectArgs &a, int batch, hipStream_t stream) {
-  hipLaunchKernelGGL(select_kernel, dim3(a.Hkv, batch), dim3(kSelThreads), 0, stream, a);
+// Layer table entries from the host's compact form: pointers and budget as
+// given, the SRH bit mask expanded into per-group head lists.  Grid (count),
+// 256 threads.
+__global__ __launch_bounds__(256) void put_layers_kernel(const PutArgs a) {
+  const PutEntry &e = a.e[blockIdx.x];
+  LayerDesc &d = a.table[a.first + blockIdx.x];
+  const int tid = threadIdx.x;
+  if (tid == 0) {
+    d.q = e.q;
+    d.k = e.k;
+    d.v = e.v;
+    d.scores = e.scores;
+    d.idx = e.idx;
+    d.k_out = e.k_out;
+    d.v_out = e.v_out;
+    d.budget = e.budget;
+    d.reserved = 0;
+  }
+  // number of SRHs among query heads 0 .. x-1
+  auto below = [&](int x) {
+    int n = 0;
+    for (int w = 0; w < (x >> 5); ++w) n += __popc(e.srh_bits[w]);
+    if (x & 31) n += __popc(e.srh_bits[x >> 5] & ((1u << (x & 31)) - 1u));
+    return n;
+  };
+  for (int h = tid; h < a.Hq; h += 256)
+    if ((e.srh_bits[h >> 5] >> (h & 31)) & 1u) d.srh_head[below(h)] = (uint8_t)h;
+  const int G = a.Hq / a.Hkv;
+  for (int g = tid; g <= a.Hkv; g += 256) d.srh_off[g] = (uint16_t)below(g * G);
+}
+
+hipError_t launch_put_layers(const PutArgs &a, hipStream_t stream) {
+  hipLaunchKernelGGL(put_layers_kernel, dim3(a.count), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 
-hipError_t launch_gather(const GatherArgs &a, int batch, hipStream_t stream) {
+hipError_t launch_select(const SelectArgs &a, int n_layers, hipStream_t stream) {
+  if (n_layers > 0)
+    hipLaunchKernelGGL(select_kernel<true>, dim3(a.Hkv, a.batch * n_layers), dim3(kSelThreads),
+                       0, stream, a);
+  else
+    hipLaunchKernelGGL(select_kernel<false>, dim3(a.Hkv, a.batch), dim3(kSelThreads), 0, stream,
+                       a);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather(const GatherArgs &a, int n_layers, int max_budget, hipStream_t stream) {
   const int rows_per_block = 256 / (a.row_bytes >> 4);
-  const int nblk = (a.budget + rows_per_block - 1) / rows_per_block;
-  hipLaunchKernelGGL(gather_kernel, dim3(nblk, a.Hkv, batch), dim3(256), 0, stream, a);
+  const int nblk = (max_budget + rows_per_block - 1) / rows_per_block;
+  if (n_layers > 0)
+    hipLaunchKernelGGL(gather_kernel<true>, dim3(nblk, a.Hkv, a.batch * n_layers), dim3(256), 0,
+                       stream, a);
+  else
+    hipLaunchKernelGGL(gather_kernel<false>, dim3(nblk, a.Hkv, a.batch), dim3(256), 0, stream,
+                       a);
   return hipGetLastError();
 }
 

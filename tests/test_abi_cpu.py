@@ -155,3 +155,85 @@ def test_budget_pointer_and_workspace_rules(L):
     assert c.compress(L, ws_bytes=need - 1) == C.WORKSPACE_TOO_SMALL
     assert c.score(L, ws_bytes=need - 1) == C.WORKSPACE_TOO_SMALL
     assert c.compress(L, ws=FAKE + 16) == C.UNSUPPORTED            # 256-byte alignment
+
+
+class LayersCase(Case):
+    """A valid multi-layer call: n_layers copies of the problem's operands."""
+
+    def __init__(self, n_layers=3, **kw):
+        super().__init__(**kw)
+        self.n = n_layers
+        self.masks = np.ascontiguousarray(np.tile(self.mask, (n_layers, 1)))
+        self.budgets = np.full(n_layers, 64, dtype=np.int32)
+        self.arrays = {name: (ctypes.c_void_p * n_layers)(*([FAKE] * n_layers))
+                       for name in ("q", "k", "v", "idx", "k_out", "v_out")}
+
+    def addr(self, name):
+        return ctypes.cast(self.arrays[name], ctypes.c_void_p).value
+
+    def ws_bytes(self, L, budget=64):
+        return L.compresskv_layers_workspace_bytes(ctypes.byref(self.p), self.n,
+                                                   self.masks.ctypes.data)
+
+    def compress_layers(self, L, ws_bytes=1 << 40, ws=FAKE, n=None):
+        return L.compresskv_compress_layers(
+            ctypes.byref(self.p), self.n if n is None else n, self.addr("q"), self.addr("k"),
+            self.addr("v"), self.masks.ctypes.data, self.budgets.ctypes.data, self.addr("idx"),
+            self.addr("k_out"), self.addr("v_out"), None, ws, ws_bytes, None)
+
+    def score_layers(self, L, scores=FAKE, ws_bytes=1 << 40):
+        return L.compresskv_score_layers(ctypes.byref(self.p), self.n, self.addr("q"),
+                                         self.addr("k"), self.masks.ctypes.data, scores, FAKE,
+                                         ws_bytes, None)
+
+
+@pytest.mark.parametrize("name,fields,status", INVALID, ids=[c[0] for c in INVALID])
+def test_invalid_problem_is_rejected_by_multi_layer_calls(L, name, fields, status):
+    c = _mutate(LayersCase(), **fields)
+    assert c.compress_layers(L) == status, L.compresskv_last_error()
+    c = _mutate(LayersCase(), **fields)
+    assert c.score_layers(L) == status, L.compresskv_last_error()
+    c = _mutate(LayersCase(), **fields)
+    assert c.ws_bytes(L) == 0
+
+
+def test_multi_layer_workspace_grows_with_layers(L):
+    one, four = LayersCase(n_layers=1), LayersCase(n_layers=4)
+    n1, n4 = one.ws_bytes(L), four.ws_bytes(L)
+    assert n1 > 0 and n4 > 0 and n1 % 256 == 0 and n4 % 256 == 0
+    T = int(one.cu[-1])
+    assert n4 - n1 >= 3 * 2 * T * 4                # three more layers of scores at least
+    assert n4 < 4 * n1 + 4 * 1024
+
+
+def test_multi_layer_rules_name_the_layer(L):
+    c = LayersCase(n_layers=4)
+    c.masks[2, :] = 0
+    c.masks[2, 0] = 1                               # layer 2, group 1: no SRH
+    assert c.compress_layers(L) == C.INVALID_ARGUMENT
+    assert "layer 2" in L.compresskv_last_error().decode()
+    c = LayersCase(n_layers=4)
+    c.budgets[1] = 15                               # < W
+    assert c.compress_layers(L) == C.INVALID_ARGUMENT
+    assert "layer 1" in L.compresskv_last_error().decode()
+    c = LayersCase(n_layers=4)
+    c.arrays["k_out"][3] = None
+    assert c.compress_layers(L) == C.INVALID_ARGUMENT
+    assert "layer 3: k_out" in L.compresskv_last_error().decode()
+    c = LayersCase(n_layers=4)
+    c.arrays["v"][0] = FAKE + 8                     # 16-byte alignment
+    assert c.compress_layers(L) == C.UNSUPPORTED
+    c = LayersCase(n_layers=4)
+    assert c.compress_layers(L, n=0) == C.INVALID_ARGUMENT
+    need = c.ws_bytes(L)
+    assert c.compress_layers(L, ws_bytes=need - 1) == C.WORKSPACE_TOO_SMALL
+    assert c.compress_layers(L, ws=FAKE + 16) == C.UNSUPPORTED
+    assert c.score_layers(L, scores=0) == C.INVALID_ARGUMENT
+    assert c.score_layers(L, ws_bytes=need - 1) == C.WORKSPACE_TOO_SMALL
+
+
+def test_multi_layer_row_tile_limit_uses_the_largest_layer(L):
+    c = LayersCase(n_layers=2, W=64, Hq=32, Hkv=4)
+    c.masks[1, :] = 1                               # layer 1: 8 SRHs x 4 row tiles > 12
+    assert c.compress_layers(L) == C.UNSUPPORTED
+    assert c.ws_bytes(L) == 0
