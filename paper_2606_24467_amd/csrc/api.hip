@@ -51,6 +51,7 @@ struct Plan {
   int rt_max = 0;      // max row tiles of a group (over the layers)
   int chunk1 = 0, max_chunks1 = 0;
   int chunk2 = 0, max_chunks2 = 0;
+  int cpw1 = 1, cpw2 = 1;  // consecutive chunks per scoring workgroup
   uint32_t head_end_mask = 0;
   // single-layer workspace: scores | stats | counters | histograms
   // multi-layer workspace:  table | scores | stats | histograms (all per layer)
@@ -211,9 +212,9 @@ void choose_path(const ckv_problem *p, Plan &pl) {
   }
 }
 
-// Chunk sizes of the two-kernel path: multiples of 512 keys (statistics: 8
-// waves x 2-tile groups, at least two groups per wave) and 992 + 32 halo keys
-// (column sums).
+// Chunk sizes of the two-kernel path: multiples of 512 keys (statistics: an
+// even number of 2-tile groups for each of the 4 waves) and 992 + 32 halo keys
+// (column sums: an even number of 2-tile groups for each of the 8 waves).
 void set_chunks(const ckv_problem *p, Plan &pl) {
   pl.T = p->cu_seqlens_host[p->batch];
   pl.lmax = 0;
@@ -221,7 +222,7 @@ void set_chunks(const ckv_problem *p, Plan &pl) {
     pl.lmax = std::max(pl.lmax, p->cu_seqlens_host[b + 1] - p->cu_seqlens_host[b]);
   int c1 = env_int("CKV_CHUNK1", 0), c2 = env_int("CKV_CHUNK2", 0);
   if (c1 <= 0 || c1 % 512 != 0) c1 = pick_chunk(p, 512, 4096, 256);
-  if (c2 <= 0 || (c2 + 32) % 256 != 0 || c2 > ckv::kMaxChunk2) c2 = 992;
+  if (c2 <= 0 || (c2 + 32) % 512 != 0 || c2 > ckv::kMaxChunk2) c2 = 992;   // even groups per chunk
   pl.chunk1 = c1;
   pl.chunk2 = c2;
   pl.max_chunks1 = std::max(1, (pl.lmax + c1 - 1) / c1);
@@ -256,6 +257,16 @@ void make_plan(const ckv_problem *p, Plan &pl, bool decide_path) {
 void make_plan_layers(const ckv_problem *p, int n_layers, Plan &pl) {
   set_chunks(p, pl);
   pl.n_layers = n_layers;
+  // Longer workgroups once there are enough of them: a few rounds of the
+  // resident workgroups keep the tail short, and every round keeps its key
+  // stream going across chunk boundaries.
+  const int64_t units1 = (int64_t)p->batch * p->n_kv_heads * n_layers * pl.max_chunks1;
+  const int64_t units2 = (int64_t)p->batch * p->n_kv_heads * n_layers * pl.max_chunks2;
+  pl.cpw1 = (int)std::max<int64_t>(1, std::min<int64_t>(8, units1 / 3072));
+  pl.cpw2 = (int)std::max<int64_t>(1, std::min<int64_t>(8, units2 / 2048));
+  const int e1 = env_int("CKV_CPW1", 0), e2 = env_int("CKV_CPW2", 0);
+  if (e1 > 0) pl.cpw1 = std::min(e1, 64);
+  if (e2 > 0) pl.cpw2 = std::min(e2, 64);
   pl.fused = false;
   pl.max_parts = pl.max_chunks1;
   const size_t groups = (size_t)p->batch * p->n_kv_heads;
@@ -288,7 +299,10 @@ ckv::ScoreArgs score_args(const ckv_problem *p, const Plan &pl, void *ws) {
   a.th = pl.th;
   a.row_slots = pl.rt_max * 16;
   a.chunk1 = pl.chunk1;
-  a.max_chunks1 = pl.max_parts;   // stride (in partials) between groups
+  a.max_chunks1 = pl.max_chunks1;
+  a.parts_stride = pl.max_parts;   // partial slots between groups
+  a.cpw1 = pl.cpw1;
+  a.cpw2 = pl.cpw2;
   a.chunk2 = pl.chunk2;
   a.max_chunks2 = pl.max_chunks2;
   const double scale = p->scale > 0.f ? (double)p->scale : 1.0 / std::sqrt((double)p->head_dim);

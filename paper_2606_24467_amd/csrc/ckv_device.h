@@ -44,15 +44,60 @@ struct alignas(16) LayerDesc {
   uint8_t srh_head[kMaxQHeads];        // query-head indices, ascending within a group
 };
 
+// Pointers into global memory.  Pointers read from the layer table have no
+// address space the compiler can infer; generic (flat) accesses would share
+// the wait counter of the LDS reads and serialise every key load with them.
+template <typename T>
+using gptr = __attribute__((address_space(1))) T *;
+template <typename T>
+__device__ __forceinline__ gptr<T> to_global(T *p) {
+  return (gptr<T>)p;
+}
+
+// What a workgroup uses of its layer, as global pointers; off / nsrh describe
+// the SRHs of group g (srh_head[off .. off + nsrh)).
+struct LayerView {
+  gptr<const char> q, k, v;
+  gptr<float> scores;
+  gptr<int32_t> idx;
+  gptr<char> k_out, v_out;
+  gptr<const uint8_t> srh_head;
+  int budget, off, nsrh;
+};
+
 // The layer a workgroup works on: the inline one, or entry `layer` of the table.
 template <bool ML, typename A>
-__device__ __forceinline__ const LayerDesc &layer_desc(const A &a, int layer) {
+__device__ __forceinline__ LayerView layer_view(const A &a, int layer, int g) {
+  LayerView v;
   if constexpr (ML) {
-    return a.layers[layer];
+    gptr<const LayerDesc> d = to_global(a.layers) + layer;
+    v.q = to_global(static_cast<const char *>(d->q));
+    v.k = to_global(static_cast<const char *>(d->k));
+    v.v = to_global(static_cast<const char *>(d->v));
+    v.scores = to_global(d->scores);
+    v.idx = to_global(d->idx);
+    v.k_out = to_global(static_cast<char *>(d->k_out));
+    v.v_out = to_global(static_cast<char *>(d->v_out));
+    v.srh_head = &d->srh_head[0];
+    v.budget = d->budget;
+    v.off = d->srh_off[g];
+    v.nsrh = d->srh_off[g + 1] - v.off;
   } else {
     (void)layer;
-    return a.l0;
+    const LayerDesc &d = a.l0;
+    v.q = to_global(static_cast<const char *>(d.q));
+    v.k = to_global(static_cast<const char *>(d.k));
+    v.v = to_global(static_cast<const char *>(d.v));
+    v.scores = to_global(d.scores);
+    v.idx = to_global(d.idx);
+    v.k_out = to_global(static_cast<char *>(d.k_out));
+    v.v_out = to_global(static_cast<char *>(d.v_out));
+    v.srh_head = to_global(&d.srh_head[0]);
+    v.budget = d.budget;
+    v.off = d.srh_off[g];
+    v.nsrh = d.srh_off[g + 1] - v.off;
   }
+  return v;
 }
 
 // Arguments of the scoring kernels.
@@ -60,7 +105,7 @@ struct ScoreArgs {
   LayerDesc l0;            // single-layer calls
   const LayerDesc *layers; // multi-layer calls: [n_layers]
   const int32_t *cu;       // [batch+1] sequence offsets
-  float2 *stats;           // per layer: [batch][Hkv][max_chunks1][row_slots] partial (ref, sum)
+  float2 *stats;           // per layer: [batch][Hkv][parts_stride][row_slots] partial (ref, sum)
   int64_t stats_layer;     // float2 elements between layers
   int *hist;               // per layer: [batch][Hkv][kHistBins] first selection digit counts
   int64_t hist_layer;      // ints between layers
@@ -68,8 +113,10 @@ struct ScoreArgs {
   int32_t T, batch, Hq, Hkv, W;
   int32_t th;             // 16-row tiles per SRH: ceil(W / 16)
   int32_t row_slots;      // padded rows per (sequence, group, chunk) in stats
-  int32_t chunk1, max_chunks1;   // keys per workgroup in the statistics pass, partial slots
-  int32_t chunk2, max_chunks2;   // keys per workgroup in the column-sum pass
+  int32_t chunk1, max_chunks1;   // keys per statistics chunk, chunks of the longest sequence
+  int32_t parts_stride;          // partial slots per (sequence, group) in stats
+  int32_t chunk2, max_chunks2;   // keys per column-sum chunk, chunks of the longest sequence
+  int32_t cpw1, cpw2;            // consecutive chunks per workgroup (statistics, column sums)
   float c1;               // softmax scale * log2(e): logits in base-2 units
   int32_t pool_kernel, pool_type, reduce_order;
   uint32_t head_end_mask;  // bit rt set if row tile rt is the last tile of an SRH
@@ -127,8 +174,14 @@ struct Slices {
   static constexpr int n = D * (int)sizeof(T) / 64;
 };
 
-__device__ __forceinline__ uint4 load16(const char *p) {
-  return *reinterpret_cast<const uint4 *>(p);
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint4 load16(gptr<const char> p) {
+  return __builtin_bit_cast(uint4, *reinterpret_cast<gptr<const u32x4>>(p));
+}
+
+__device__ __forceinline__ void store16(gptr<char> p, uint4 v) {
+  *reinterpret_cast<gptr<u32x4>>(p) = __builtin_bit_cast(u32x4, v);
 }
 
 // acc += A_tile * B_tile^T over one 16-byte slice of each row.

@@ -36,7 +36,7 @@ __global__ __launch_bounds__(256) void fill_kernel(int *p, int n) {
 
 // Keys of a unit: tile w + NW*i (i < UT) of wave w, clamped into [.., k_last].
 template <typename T, int D, int NW, int UT>
-__device__ __forceinline__ void load_unit(const ScoreArgs &a, const char *kb, int s0, int g,
+__device__ __forceinline__ void load_unit(const ScoreArgs &a, gptr<const char> kb, int s0, int g,
                                           int u0, int k_last, uint4 (&kf)[UT][Slices<T, D>::n]) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int c = lane & 15, quad = lane >> 4;
@@ -107,8 +107,6 @@ __global__ __launch_bounds__(64 * kFusedWaves) void fused_score_kernel(const Fus
   constexpr int kUnitKeys = 16 * NW * UT;
   constexpr int CSW = kUnitKeys + 32;
   const ScoreArgs &a = f.s;
-  const LayerDesc &ld = a.l0;
-  const char *kb = reinterpret_cast<const char *>(ld.k);
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int c = lane & 15, quad = lane >> 4;
@@ -134,15 +132,16 @@ __global__ __launch_bounds__(64 * kFusedWaves) void fused_score_kernel(const Fus
   const int gi = b * a.Hkv + g;
   const int u0 = u * kUnitKeys;
   const int P = L - a.W;
-  const int off = ld.srh_off[g];
-  const int nh = ld.srh_off[g + 1] - off;
+  const LayerView lv = layer_view<false>(a, 0, g);
+  const gptr<const char> kb = lv.k;
+  const int nh = lv.nsrh;
   const int rt_n = nh * a.th;
   const int rows = rt_n * 16;
 
   // Loads: queries, the unit's keys, then the pooling halo tiles (wave 0: the
   // tile before the unit, wave 1: the tile after it).
   uint4 qv[QStage<T, D, RTM, NT>::n];
-  q_load<T, D, RTM, NT>(a, ld, b, off, rt_n, qv);
+  q_load<T, D, RTM, NT>(a, lv, b, rt_n, qv);
   uint4 kf[UT][NS];
   load_unit<T, D, NW, UT>(a, kb, s0, g, u0, min(L, u0 + kUnitKeys) - 1, kf);
   const int halo_base = (wave == 0) ? u0 - 16 : u0 + kUnitKeys;
@@ -159,7 +158,7 @@ __global__ __launch_bounds__(64 * kFusedWaves) void fused_score_kernel(const Fus
     for (int s = 0; s < NS; ++s) qreg[rt][s] = q_frag<T, D>(q_lds, rt, s, c, quad);
 
   // S1+S2: this unit's partial row statistics, published for the group.
-  float2 *gparts = a.stats + (int64_t)gi * a.max_chunks1 * a.row_slots;
+  float2 *gparts = a.stats + (int64_t)gi * a.parts_stride * a.row_slots;
   const float2 mine = unit_stats<T, D, RTM, NW, UT>(a, kf, qreg, q_lds, part, rt_n, u0, L, P);
   if (tid < rows) store_partial_coherent(gparts + (int64_t)u * a.row_slots + tid, mine);
   // Every thread's partial store has reached the coherence point before the
@@ -223,7 +222,7 @@ __global__ __launch_bounds__(64 * kFusedWaves) void fused_score_kernel(const Fus
   if (wave < 2)
     tile_window_sums<T, D, RTM, CSW>(a, kh, qreg, q_lds, bias, rt_n,
                                      (wave == 0) ? -1 : kUnitKeys / 16, halo_ok, c, quad, cs);
-  float *out = ld.scores + (int64_t)g * a.T + s0;
+  const gptr<float> out = lv.scores + (int64_t)g * a.T + s0;
   // Window positions of the unit are always kept: +inf.
   for (int j = max(u0, P) + tid; j < min(L, u0 + kUnitKeys); j += NT) out[j] = INFINITY;
   __syncthreads();

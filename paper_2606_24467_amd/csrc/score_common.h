@@ -40,10 +40,10 @@ struct QStage {
 };
 
 template <typename T, int D, int RTM, int NT>
-__device__ __forceinline__ void q_load(const ScoreArgs &a, const LayerDesc &ld, int b, int off,
-                                       int rt_n, uint4 (&qv)[QStage<T, D, RTM, NT>::n]) {
+__device__ __forceinline__ void q_load(const ScoreArgs &a, const LayerView &lv, int b, int rt_n,
+                                       uint4 (&qv)[QStage<T, D, RTM, NT>::n]) {
   constexpr int U4 = QLayout<T, D>::U4;
-  const char *qb = reinterpret_cast<const char *>(ld.q);
+  const gptr<const char> qb = lv.q;
 #pragma unroll
   for (int it = 0; it < QStage<T, D, RTM, NT>::n; ++it) {
     const int idx = (int)threadIdx.x + it * NT;
@@ -53,7 +53,7 @@ __device__ __forceinline__ void q_load(const ScoreArgs &a, const LayerDesc &ld, 
     if (rt < rt_n) {
       const int i = (rt % a.th) * 16 + c;
       if (i < a.W) {
-        const int head = ld.srh_head[off + rt / a.th];
+        const int head = lv.srh_head[lv.off + rt / a.th];
         qv[it] = load16(qb + (((int64_t)b * a.W + i) * a.Hq + head) * (int64_t)(D * sizeof(T)) +
                         16 * u);
       }
@@ -81,9 +81,10 @@ __device__ __forceinline__ uint4 q_frag(const uint4 *q_lds, int rt, int s, int c
 // Slices of one key row of the layer's K at kb (key index clamped into the
 // sequence by the callers).
 template <typename T, int D>
-__device__ __forceinline__ void load_k_row(const ScoreArgs &a, const char *kb, int s0, int key,
-                                           int g, int quad, uint4 (&out)[Slices<T, D>::n]) {
-  const char *p = kb +
+__device__ __forceinline__ void load_k_row(const ScoreArgs &a, gptr<const char> kb, int s0,
+                                           int key, int g, int quad,
+                                           uint4 (&out)[Slices<T, D>::n]) {
+  const gptr<const char> p = kb +
                   ((int64_t)(s0 + key) * a.k_stride_tok + (int64_t)g * a.k_stride_head) *
                       (int64_t)sizeof(T) +
                   16 * quad;
@@ -121,23 +122,30 @@ __device__ __forceinline__ void stats_update(const ScoreArgs &a, const f32x4 (&a
                                              float (&ref)[RTM], float (&sum)[RTM], int rt_n,
                                              int base, int L, int P, int c, int quad) {
   constexpr float kRescale = 30.f;   // rebase the reference when a term would exceed 2^30
-  const bool masked_tile = (base + 16 > P);
   float d[RTM][4];
   float dmax = -INFINITY;
+  if (base + 16 <= P) {   // prefix keys only (uniform): nothing is masked
 #pragma unroll
-  for (int rt = 0; rt < RTM; ++rt) {
-    if (rt >= rt_n) continue;
+    for (int rt = 0; rt < RTM; ++rt) {
+      if (rt >= rt_n) continue;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      float x = __builtin_fmaf(acc[rt][r], a.c1, -ref[rt]);
-      if (masked_tile) {
+      for (int r = 0; r < 4; ++r) {
+        d[rt][r] = __builtin_fmaf(acc[rt][r], a.c1, -ref[rt]);
+        dmax = fmaxf(dmax, d[rt][r]);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int rt = 0; rt < RTM; ++rt) {
+      if (rt >= rt_n) continue;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
         const int i = (rt % a.th) * 16 + c;   // window index of this lane's row
         const int j = base + 4 * quad + r;
         const bool ok = (j < L) && (i >= a.W || j <= P + i);
-        x = ok ? x : -INFINITY;
+        d[rt][r] = ok ? __builtin_fmaf(acc[rt][r], a.c1, -ref[rt]) : -INFINITY;
+        dmax = fmaxf(dmax, d[rt][r]);
       }
-      d[rt][r] = x;
-      dmax = fmaxf(dmax, x);
     }
   }
   if (__any(dmax > kRescale)) {
@@ -260,7 +268,7 @@ __device__ __forceinline__ void tile_window_sums(const ScoreArgs &a,
 // and to the LDS histogram of its top 11 value bits.
 template <int NT, int CSW>
 __device__ __forceinline__ void pool_scores(const ScoreArgs &a, const float (*cs)[CSW],
-                                            int nh, int c0, int p_end, int P, float *out,
+                                            int nh, int c0, int p_end, int P, gptr<float> out,
                                             int *hist_s) {
   const int rp = (a.pool_kernel - 1) >> 1;
   const float inv_k = 1.f / (float)a.pool_kernel;

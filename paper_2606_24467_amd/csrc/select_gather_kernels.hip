@@ -90,7 +90,7 @@ __device__ __forceinline__ void find_bucket(const int *hist, int nb, int remain,
 
 // Scores [r0 + t*kEpt, r0 + (t+1)*kEpt) of thread t into registers (all loads
 // issued together); positions >= P read as 0 and are masked by the callers.
-__device__ __forceinline__ void load_round(const uint32_t *sc, int P, int r0,
+__device__ __forceinline__ void load_round(gptr<const uint32_t> sc, int P, int r0,
                                            uint32_t (&v)[kEpt]) {
   const int j0 = r0 + (int)threadIdx.x * kEpt;
 #pragma unroll
@@ -103,12 +103,12 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a)
   const int g = blockIdx.x;
   const int layer = ML ? (int)blockIdx.y / a.batch : 0;
   const int b = (int)blockIdx.y - layer * a.batch;
-  const LayerDesc &ld = layer_desc<ML>(a, layer);
-  const int budget = ld.budget;
+  const LayerView lv = layer_view<ML>(a, layer, 0);
+  const int budget = lv.budget;
   const int tid = threadIdx.x;
   const int s0 = a.cu[b];
   const int L = a.cu[b + 1] - s0;
-  int32_t *out = ld.idx + ((int64_t)b * a.Hkv + g) * budget;
+  const gptr<int32_t> out = lv.idx + ((int64_t)b * a.Hkv + g) * budget;
   if (L <= budget) {
     for (int j = tid; j < budget; j += kSelThreads) out[j] = (j < L) ? j : -1;
     return;
@@ -117,7 +117,8 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a)
   const int k = budget - a.W;       // prefix tokens to keep, 0 <= k < P
   for (int w = tid; w < a.W; w += kSelThreads) out[k + w] = P + w;
   if (k == 0) return;
-  const uint32_t *sc = reinterpret_cast<const uint32_t *>(ld.scores + (int64_t)g * a.T + s0);
+  const gptr<const uint32_t> sc =
+      reinterpret_cast<gptr<const uint32_t>>(lv.scores + (int64_t)g * a.T + s0);
   const int nrounds = (P + kRound - 1) / kRound;
   const bool resident = (nrounds == 1);   // scores stay in registers for every pass
 
@@ -247,10 +248,10 @@ __global__ __launch_bounds__(256) void gather_kernel(const GatherArgs a) {
   const int g = blockIdx.y;
   const int layer = ML ? (int)blockIdx.z / a.batch : 0;
   const int b = (int)blockIdx.z - layer * a.batch;
-  const LayerDesc &ld = layer_desc<ML>(a, layer);
-  const int budget = ld.budget;
-  const char *kb = reinterpret_cast<const char *>(ld.k);
-  const char *vb = reinterpret_cast<const char *>(ld.v);
+  const LayerView lv = layer_view<ML>(a, layer, 0);
+  const int budget = lv.budget;
+  const gptr<const char> kb = lv.k;
+  const gptr<const char> vb = lv.v;
   const int lanes_per_row = a.row_bytes >> 4;
   const int rows_per_pass = 256 / lanes_per_row;
   const int sub = threadIdx.x % lanes_per_row;
@@ -261,7 +262,7 @@ __global__ __launch_bounds__(256) void gather_kernel(const GatherArgs a) {
   {
     const int r = blockIdx.x * rows_per_pass + r_in;
     if (r >= budget) return;
-    const int j = ld.idx[obase + r];
+    const int j = lv.idx[obase + r];
     uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
     if (j >= 0 && j < L) {   // anything else is a dropped slot: zeros
       kv = load16(kb + (int64_t)(s0 + j) * a.k_stride_tok + (int64_t)g * a.k_stride_head +
@@ -270,8 +271,8 @@ __global__ __launch_bounds__(256) void gather_kernel(const GatherArgs a) {
                   16 * sub);
     }
     const int64_t o = (obase + r) * a.row_bytes + 16 * sub;
-    *reinterpret_cast<uint4 *>(static_cast<char *>(ld.k_out) + o) = kv;
-    *reinterpret_cast<uint4 *>(static_cast<char *>(ld.v_out) + o) = vv;
+    store16(lv.k_out + o, kv);
+    store16(lv.v_out + o, vv);
   }
 }
 
