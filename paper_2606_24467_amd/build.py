@@ -19,7 +19,7 @@ SOURCES = ["api.hip", "score_kernels.hip", "score_layers.hip", "fused_score.hip"
            "select_gather_kernels.hip"]
 ARCH = "gfx950"
 FLAGS = [
-    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
+    f"--offload-arch={ARCH}", "-O3", "-std=c++20", "-fPIC",
     # packed fp32 VALU instructions stay off in every kernel of this library
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-result",
@@ -37,8 +37,17 @@ def _hipcc() -> str:
     return p
 
 
+# Per-source additions.  The two-pass scoring kernels keep MFMA results in
+# VGPRs, where the softmax arithmetic reads them (the single-pass kernel is
+# left to the default heuristics: this compiler fails on it with the option).
+EXTRA = {
+    "score_kernels.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+    "score_layers.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+}
+
+
 def _compile(src: str, obj: str) -> None:
-    cmd = [_hipcc(), *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [_hipcc(), *FLAGS, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     err = "\n".join(l for l in r.stderr.splitlines() if "packed-fp32-ops" not in l)
     if r.returncode != 0:

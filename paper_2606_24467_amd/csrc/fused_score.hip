@@ -58,6 +58,7 @@ __device__ __forceinline__ float2 unit_stats(const ScoreArgs &a,
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int c = lane & 15, quad = lane >> 4;
   float ref[RTM], sum[RTM];
+  bool ready = false;
 #pragma unroll
   for (int rt = 0; rt < RTM; ++rt) {
     ref[rt] = -INFINITY;
@@ -68,8 +69,8 @@ __device__ __forceinline__ float2 unit_stats(const ScoreArgs &a,
     f32x4 acc[RTM];
 #pragma unroll
     for (int rt = 0; rt < RTM; ++rt)
-      if (rt < rt_n) acc[rt] = tile_logits<T, D, RTM, true>(kf[i], qreg, q_lds, rt, c, quad);
-    stats_update<RTM>(a, acc, ref, sum, rt_n, u0 + 16 * (wave + NW * i), L, P, c, quad);
+      acc[rt] = tile_logits<T, D, RTM, true>(kf[i], qreg, q_lds, rt, c, quad);
+    stats_update<RTM>(a, acc, ref, sum, ready, u0 + 16 * (wave + NW * i), L, P, c, quad);
   }
 #pragma unroll
   for (int rt = 0; rt < RTM; ++rt) {
@@ -216,12 +217,12 @@ __global__ __launch_bounds__(64 * kFusedWaves) void fused_score_kernel(const Fus
 #pragma unroll
   for (int i = 0; i < UT; ++i) {
     const int e = wave + NW * i;
-    tile_window_sums<T, D, RTM, CSW>(a, kf[i], qreg, q_lds, bias, rt_n, e, u0 + 16 * e < P, c,
-                                     quad, cs);
+    tile_window_sums<T, D, RTM, CSW>(a, kf[i], qreg, q_lds, bias, e, u0 + 16 * e < P, c, quad,
+                                     cs);
   }
   if (wave < 2)
-    tile_window_sums<T, D, RTM, CSW>(a, kh, qreg, q_lds, bias, rt_n,
-                                     (wave == 0) ? -1 : kUnitKeys / 16, halo_ok, c, quad, cs);
+    tile_window_sums<T, D, RTM, CSW>(a, kh, qreg, q_lds, bias, (wave == 0) ? -1 : kUnitKeys / 16,
+                                     halo_ok, c, quad, cs);
   const gptr<float> out = lv.scores + (int64_t)g * a.T + s0;
   // Window positions of the unit are always kept: +inf.
   for (int j = max(u0, P) + tid; j < min(L, u0 + kUnitKeys); j += NT) out[j] = INFINITY;

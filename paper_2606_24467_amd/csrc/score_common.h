@@ -19,8 +19,9 @@ struct QLayout {
   static constexpr int STRIDE = U4 + 1;        // padded row stride in LDS (bank spread)
 };
 
-constexpr int kWaves = 8;       // waves per scoring workgroup
-constexpr int kPair = 2;        // key tiles per load group; two groups in flight per wave
+constexpr int kWaves = 8;       // waves per column-sum workgroup
+constexpr int kRing = 4;        // key tiles per wave in the load ring: kRing - 1 in flight
+                                // while one is consumed
 
 // Row tiles kept in registers: all of them when they fit in 64 VGPRs, else none.
 template <typename T, int D, int RTM>
@@ -114,46 +115,73 @@ __device__ __forceinline__ f32x4 tile_logits(const uint4 (&kf)[Slices<T, D>::n],
   return acc;
 }
 
+// Row-tile counts the scoring loops are compiled for: a group with rt_n row
+// tiles runs the smallest of them that is >= rt_n; the extra tiles hold zero
+// queries (their rows are never read back), so every loop over row tiles has
+// a compile-time bound and no branch.
+__host__ __device__ constexpr int rt_class(int rt_n) {
+  return rt_n <= 4 ? rt_n : rt_n <= 6 ? 6 : rt_n <= 8 ? 8 : 12;
+}
+
+// Sum of v over the four quads (lanes c, c + 16, c + 32, c + 48) in every lane,
+// with the gfx950 lane-swap instructions (no LDS round trip).
+__device__ __forceinline__ float quad_sum(float v) {
+  const auto s32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v),
+                                                    false, false);
+  v = __uint_as_float(s32[0]) + __uint_as_float(s32[1]);
+  const auto s16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v),
+                                                    false, false);
+  return __uint_as_float(s16[0]) + __uint_as_float(s16[1]);
+}
+
 // Fold one key tile (logits acc[rt], keys base + 4*quad + r) into the running
-// (ref, sum) pairs of this lane's rows.  Keys past the sequence end and, inside
-// the window, after the row's own position (causal) are masked.
-template <int RTM>
-__device__ __forceinline__ void stats_update(const ScoreArgs &a, const f32x4 (&acc)[RTM],
-                                             float (&ref)[RTM], float (&sum)[RTM], int rt_n,
+// (ref, sum) pairs of this lane's rows, sum = sum_j exp2(y_j - ref).  A row's
+// reference stays fixed while its sum stays below 2^64, so on the common path
+// (every key of the tile is a prefix key and the references are set: `ready`)
+// a logit costs one fma, one exp2 and one add.  The first tile, masked tiles
+// (keys past the sequence end, or after the row's own position inside the
+// window: causal) and a tile that would push a sum past 2^64 take the general
+// path, which rebases a row on its largest new value when a term would exceed
+// 2^30 (always the case for the first key of a row).
+template <int RT>
+__device__ __forceinline__ void stats_update(const ScoreArgs &a, const f32x4 (&acc)[RT],
+                                             float (&ref)[RT], float (&sum)[RT], bool &ready,
                                              int base, int L, int P, int c, int quad) {
-  constexpr float kRescale = 30.f;   // rebase the reference when a term would exceed 2^30
-  float d[RTM][4];
-  float dmax = -INFINITY;
-  if (base + 16 <= P) {   // prefix keys only (uniform): nothing is masked
+  constexpr float kRescale = 30.f;
+  const bool unmasked = (base + 16 <= P);   // uniform
+  if (ready && unmasked) {
+    float s_new[RT];
+    bool over = false;
 #pragma unroll
-    for (int rt = 0; rt < RTM; ++rt) {
-      if (rt >= rt_n) continue;
+    for (int rt = 0; rt < RT; ++rt) {
+      float t = 0.f;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        d[rt][r] = __builtin_fmaf(acc[rt][r], a.c1, -ref[rt]);
-        dmax = fmaxf(dmax, d[rt][r]);
-      }
+      for (int r = 0; r < 4; ++r) t += fast_exp2(__builtin_fmaf(acc[rt][r], a.c1, -ref[rt]));
+      s_new[rt] = sum[rt] + t;
+      over |= !(s_new[rt] <= 0x1p64f);   // also true for inf and nan
     }
-  } else {
+    if (!__any(over)) {
 #pragma unroll
-    for (int rt = 0; rt < RTM; ++rt) {
-      if (rt >= rt_n) continue;
+      for (int rt = 0; rt < RT; ++rt) sum[rt] = s_new[rt];
+      return;
+    }
+  }
+  float d[RT][4];
+  float dmax = -INFINITY;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int i = (rt % a.th) * 16 + c;   // window index of this lane's row
-        const int j = base + 4 * quad + r;
-        const bool ok = (j < L) && (i >= a.W || j <= P + i);
-        d[rt][r] = ok ? __builtin_fmaf(acc[rt][r], a.c1, -ref[rt]) : -INFINITY;
-        dmax = fmaxf(dmax, d[rt][r]);
-      }
+  for (int rt = 0; rt < RT; ++rt) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int i = (rt % a.th) * 16 + c;   // window index of this lane's row
+      const int j = base + 4 * quad + r;
+      const bool ok = unmasked || ((j < L) && (i >= a.W || j <= P + i));
+      d[rt][r] = ok ? __builtin_fmaf(acc[rt][r], a.c1, -ref[rt]) : -INFINITY;
+      dmax = fmaxf(dmax, d[rt][r]);
     }
   }
   if (__any(dmax > kRescale)) {
-    // Rebase a row's reference on the largest new value when a term would
-    // exceed 2^kRescale (always the case for the first key of a row).
 #pragma unroll
-    for (int rt = 0; rt < RTM; ++rt) {
-      if (rt >= rt_n) continue;
+    for (int rt = 0; rt < RT; ++rt) {
       const float m = fmaxf(fmaxf(d[rt][0], d[rt][1]), fmaxf(d[rt][2], d[rt][3]));
       if (m > kRescale) {
         float best = -INFINITY;
@@ -170,11 +198,12 @@ __device__ __forceinline__ void stats_update(const ScoreArgs &a, const f32x4 (&a
     }
   }
 #pragma unroll
-  for (int rt = 0; rt < RTM; ++rt) {
-    if (rt >= rt_n) continue;
+  for (int rt = 0; rt < RT; ++rt) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) sum[rt] += fast_exp2(d[rt][r]);
   }
+  // after an unmasked tile every row has a finite reference
+  ready = ready || unmasked;
 }
 
 // A partial (ref, sum) pair read or written at agent scope: the access goes to
@@ -235,26 +264,33 @@ __device__ __forceinline__ void merge_row_bias(const ScoreArgs &a, const float2 
 // Window sums of one key tile for every SRH of the group (MFMA operands: A =
 // window rows, B = keys; lane (quad, c) holds rows 4*quad .. 4*quad+3 against
 // key c): in-lane over the 4 rows and the SRH's row tiles, then across the
-// quads.  cs[h][16 + 16*e + c] receives SRH h's sum for key c of tile e.
-template <typename T, int D, int RTM, int CSW>
+// quads.  cs[h][16 + 16*e + c] receives SRH h's sum for key c of tile e.  Row
+// tiles past the group's own (zero queries) have bias +inf and add nothing.
+template <typename T, int D, int RT, int CSW>
 __device__ __forceinline__ void tile_window_sums(const ScoreArgs &a,
                                                  const uint4 (&kf)[Slices<T, D>::n],
-                                                 const uint4 (&qreg)[RegTiles<T, D, RTM>::n]
+                                                 const uint4 (&qreg)[RegTiles<T, D, RT>::n]
                                                                     [Slices<T, D>::n],
-                                                 const uint4 *q_lds, const float (&bias)[RTM][4],
-                                                 int rt_n, int e, bool keep, int c, int quad,
+                                                 const uint4 *q_lds, const float (&bias)[RT][4],
+                                                 int e, bool keep, int c, int quad,
                                                  float (*cs)[CSW]) {
+  // per row tile: the lane's 4 rows (no branch between the row tiles)
+  float vt[RT];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    const f32x4 acc = tile_logits<T, D, RT, false>(kf, qreg, q_lds, rt, c, quad);
+    vt[rt] = 0.f;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) vt[rt] += fast_exp2(__builtin_fmaf(acc[r], a.c1, -bias[rt][r]));
+  }
+  // per SRH: its row tiles, then the quads
   int hh = 0;
   float v = 0.f;
 #pragma unroll
-  for (int rt = 0; rt < RTM; ++rt) {
-    if (rt >= rt_n) continue;
-    const f32x4 acc = tile_logits<T, D, RTM, false>(kf, qreg, q_lds, rt, c, quad);
-#pragma unroll
-    for (int r = 0; r < 4; ++r) v += fast_exp2(__builtin_fmaf(acc[r], a.c1, -bias[rt][r]));
+  for (int rt = 0; rt < RT; ++rt) {
+    v += vt[rt];
     if ((a.head_end_mask >> rt) & 1u) {
-      v += __shfl_xor(v, 16);
-      v += __shfl_xor(v, 32);
+      v = quad_sum(v);
       if (keep && quad == (hh & 3)) cs[hh][16 + 16 * e + c] = v;
       v = 0.f;
       ++hh;
@@ -313,6 +349,105 @@ __device__ __forceinline__ void pool_scores(const ScoreArgs &a, const float (*cs
     out[j] = score;
     atomicAdd(&hist_s[hist_bin(__float_as_uint(score))], 1);
   }
+}
+
+// Pooling with a compile-time radius RP (kernel 2 RP + 1): each thread pools
+// PPT consecutive positions of [c0, p_end) from one register window of
+// PPT + 2 RP window sums per SRH (independent LDS reads, positions outside
+// the prefix [0, P) padded: -inf for max, 0 for average).  Same arithmetic, in
+// the same order, as pool_scores.  The scores go to stage[j - c0] (LDS; the
+// caller writes them out with whole-line stores), and runs of equal histogram
+// bins (plateaus of max pooling) are added with one atomic.
+template <int RP, int NT, int CSW>
+__device__ __forceinline__ void pool_scores_r(const ScoreArgs &a, const float (*cs)[CSW],
+                                              int nh, int c0, int p_end, int P, float *stage,
+                                              int *hist_s) {
+  constexpr int PPT = 4;
+  constexpr int NV = PPT + 2 * RP;
+  const bool is_max = (a.pool_type == 0);
+  const float pad = is_max ? -INFINITY : 0.f;
+  const float inv_k = 1.f / (float)a.pool_kernel;
+  const float inv_n = 1.f / (float)nh;
+  for (int j0 = c0 + PPT * (int)threadIdx.x; j0 < p_end; j0 += PPT * NT) {
+    float score[PPT];
+    if (a.reduce_order == 0) {      // pool each SRH, then average
+#pragma unroll
+      for (int p = 0; p < PPT; ++p) score[p] = 0.f;
+      for (int h = 0; h < nh; ++h) {
+        float v[NV];
+#pragma unroll
+        for (int k = 0; k < NV; ++k) {
+          const int x = j0 - RP + k;
+          v[k] = (x >= 0 && x < P) ? cs[h][16 + x - c0] : pad;
+        }
+#pragma unroll
+        for (int p = 0; p < PPT; ++p) {
+          float m = v[p];
+#pragma unroll
+          for (int d = 1; d <= 2 * RP; ++d) m = is_max ? fmaxf(m, v[p + d]) : m + v[p + d];
+          score[p] += is_max ? m : m * inv_k;
+        }
+      }
+#pragma unroll
+      for (int p = 0; p < PPT; ++p) score[p] *= inv_n;
+    } else {                        // average the SRH sums, then pool
+      float v[NV];
+#pragma unroll
+      for (int k = 0; k < NV; ++k) {
+        const int x = j0 - RP + k;
+        if (x >= 0 && x < P) {
+          float m = 0.f;
+          for (int h = 0; h < nh; ++h) m += cs[h][16 + x - c0];
+          v[k] = m * inv_n;
+        } else {
+          v[k] = pad;
+        }
+      }
+#pragma unroll
+      for (int p = 0; p < PPT; ++p) {
+        float m = v[p];
+#pragma unroll
+        for (int d = 1; d <= 2 * RP; ++d) m = is_max ? fmaxf(m, v[p + d]) : m + v[p + d];
+        score[p] = is_max ? m : m * inv_k;
+      }
+    }
+    int run_bin = -1, run_n = 0;
+#pragma unroll
+    for (int p = 0; p < PPT; ++p) {
+      if (j0 + p >= p_end) break;
+      stage[j0 + p - c0] = score[p];
+      const int bin = hist_bin(__float_as_uint(score[p]));
+      if (bin != run_bin) {
+        if (run_n) atomicAdd(&hist_s[run_bin], run_n);
+        run_bin = bin;
+        run_n = 0;
+      }
+      ++run_n;
+    }
+    if (run_n) atomicAdd(&hist_s[run_bin], run_n);
+  }
+}
+
+// S4 for one chunk: the compiled radius for the usual kernels (scores staged
+// in LDS, then stored a line at a time), the general loop otherwise (or when
+// there is no staging buffer).
+template <int NT, int CSW>
+__device__ __forceinline__ void pool_chunk(const ScoreArgs &a, const float (*cs)[CSW], int nh,
+                                           int c0, int p_end, int P, gptr<float> out,
+                                           float *stage, int *hist_s) {
+  const int rp = (a.pool_kernel - 1) >> 1;
+  if (rp > 3 || stage == nullptr) {
+    pool_scores<NT, CSW>(a, cs, nh, c0, p_end, P, out, hist_s);
+    return;
+  }
+  switch (rp) {
+    case 0: pool_scores_r<0, NT, CSW>(a, cs, nh, c0, p_end, P, stage, hist_s); break;
+    case 1: pool_scores_r<1, NT, CSW>(a, cs, nh, c0, p_end, P, stage, hist_s); break;
+    case 2: pool_scores_r<2, NT, CSW>(a, cs, nh, c0, p_end, P, stage, hist_s); break;
+    default: pool_scores_r<3, NT, CSW>(a, cs, nh, c0, p_end, P, stage, hist_s); break;
+  }
+  __syncthreads();
+  for (int j = c0 + (int)threadIdx.x; j < p_end; j += NT) out[j] = stage[j - c0];
 }
 
 // Add a workgroup's LDS histogram to the group's global one (integer atomics:

@@ -20,13 +20,13 @@
 //
 // Rows of a KV group: SRH h (in head order) owns th = ceil(W/16) row tiles of
 // 16 rows; row i < W of the tile set is window query i of that head, the
-// padding rows have zero queries and are ignored.  A workgroup (8 waves)
-// stages the group's window queries in LDS once; each wave keeps them in
-// registers when they fit (up to 4 row tiles) and otherwise reads them from
-// LDS per MFMA.  Each wave streams its key tiles through a two-deep pipeline
-// of 2-tile groups (8 KB each): loads are unconditional (key index clamped
-// into the sequence, extra tiles masked), so the compiler can wait for exactly
-// the group being consumed while the next one is still in flight.
+// padding rows have zero queries and are ignored.  A workgroup stages the
+// group's window queries in LDS once; each wave keeps them in registers when
+// they fit (up to 4 row tiles) and otherwise reads them from LDS per MFMA.
+// Each wave streams its key tiles through a ring of kRing one-tile buffers
+// (4 KB each): while it works on one tile, the next kRing - 1 are in flight.
+// The loads are unconditional (key index clamped into the range, extra tiles
+// masked), so the compiler waits for exactly the tile being consumed.
 //
 // ML (multi-layer): grid z runs over (layer, sequence) pairs, layer-major, and
 // the layer's operands come from the table; otherwise from the arguments.
@@ -35,6 +35,27 @@
 #include "score_common.h"
 
 namespace ckv {
+
+// What a scoring workgroup knows before it specialises on its row-tile count.
+struct Work {
+  LayerView lv;
+  gptr<const char> kbase;
+  int layer, b, g, s0, L, P, c0, n_chunks, rt_n;
+};
+
+// Calls body.template operator()<RT>() with RT = rt_class(rt_n) (<= RTM).
+template <int RTM, typename F>
+__device__ __forceinline__ void dispatch_rt(int rt_n, F &&body) {
+  switch (rt_class(rt_n)) {
+    case 1: if constexpr (RTM >= 1) body.template operator()<1>(); break;
+    case 2: if constexpr (RTM >= 2) body.template operator()<2>(); break;
+    case 3: if constexpr (RTM >= 3) body.template operator()<3>(); break;
+    case 4: if constexpr (RTM >= 4) body.template operator()<4>(); break;
+    case 6: if constexpr (RTM >= 6) body.template operator()<6>(); break;
+    case 8: if constexpr (RTM >= 8) body.template operator()<8>(); break;
+    default: if constexpr (RTM >= 12) body.template operator()<12>(); break;
+  }
+}
 
 // ---------------------------------------------------------------------------
 // S1+S2 partial statistics.  Grid (Hkv, ceil(max_chunks1 / cpw1), batch
@@ -46,88 +67,64 @@ namespace ckv {
 // logits of row c against keys 4*quad .. 4*quad+3 of the tile and keeps one
 // running (ref, sum) pair per row tile.  Wave w handles the key tiles
 // w, w + NW, w + 2 NW, ... of the workgroup's range; a chunk (chunk1 keys) is
-// a whole number of 2-tile groups of every wave, so its partial is the same
+// a whole number of ring turns of every wave, so its partial is the same
 // whichever workgroup size covers it.
 // ---------------------------------------------------------------------------
 constexpr int kStatsWaves = 4;
 
-template <typename T, int D, int RTM, bool ML>
-__global__ __launch_bounds__(64 * kStatsWaves) void stats_kernel(const ScoreArgs a) {
+template <typename T, int D, int RT>
+__device__ __forceinline__ void stats_body(const ScoreArgs &a, const Work &w, uint4 *q_lds,
+                                           float2 (*part)[16 * 12]) {
   constexpr int NW = kStatsWaves;
-  constexpr int NS = Slices<T, D>::n, RQ = RegTiles<T, D, RTM>::v;
+  constexpr int NS = Slices<T, D>::n, RQ = RegTiles<T, D, RT>::v;
   constexpr int NT = 64 * NW;
-  const int g = blockIdx.x;
-  const int layer = ML ? (int)blockIdx.z / a.batch : 0;
-  const int b = (int)blockIdx.z - layer * a.batch;
-  const LayerView lv = layer_view<ML>(a, layer, g);
-  const gptr<const char> kbase = lv.k;
-  const int s0 = a.cu[b];
-  const int L = a.cu[b + 1] - s0;
-  const int chunk0 = (int)blockIdx.y * a.cpw1;
-  if (chunk0 == 0) {   // the column-sum kernel accumulates this histogram afterwards
-    int *h = a.hist + layer * a.hist_layer + ((int64_t)b * a.Hkv + g) * kHistBins;
-    for (int i = threadIdx.x; i < kHistBins; i += NT) h[i] = 0;
-  }
-  const int c0 = chunk0 * a.chunk1;
-  if (c0 >= L) return;                       // uniform for the whole workgroup
-  const int n_chunks = min(a.cpw1, (L - c0 + a.chunk1 - 1) / a.chunk1);
-  const int P = L - a.W;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int c = lane & 15, quad = lane >> 4;
   const int tid = threadIdx.x;
-  const int rt_n = lv.nsrh * a.th;
-  const int gpc = a.chunk1 / (16 * NW * kPair);   // 2-tile groups per wave and chunk (even)
-  const int n_groups = gpc * n_chunks;
+  const int c0 = w.c0, L = w.L, P = w.P, s0 = w.s0, g = w.g;
+  const int tpc = a.chunk1 / (16 * NW);   // key tiles per wave and chunk (a multiple of kRing)
+  const int n_tiles = tpc * w.n_chunks;
   // key row of this lane for tile index i of this wave, clamped into the range
-  // (the pipeline's reads past the last tile hit the same cached row)
-  const int k_last = min(L, c0 + n_chunks * a.chunk1) - 1;
+  // (the ring's reads past the last tile hit the same cached row)
+  const int k_last = min(L, c0 + w.n_chunks * a.chunk1) - 1;
   auto key_of = [&](int i) { return min(c0 + 16 * (wave + NW * i) + c, k_last); };
-  float2 *parts = a.stats + layer * a.stats_layer +
-                  ((int64_t)b * a.Hkv + g) * a.parts_stride * a.row_slots;
+  float2 *parts = a.stats + w.layer * a.stats_layer +
+                  ((int64_t)w.b * a.Hkv + g) * a.parts_stride * a.row_slots;
 
-  __shared__ uint4 q_lds[RTM * 16 * QLayout<T, D>::STRIDE];
-  __shared__ float2 part[NW][RTM * 16];
-
-  // Query loads first, then the first two key groups; the queries are written
+  // Query loads first, then the first kRing key tiles; the queries are written
   // to LDS while the keys are still in flight.
-  uint4 qv[QStage<T, D, RTM, NT>::n];
-  q_load<T, D, RTM, NT>(a, lv, b, rt_n, qv);
-  uint4 ka[kPair][NS], kb[kPair][NS];
+  uint4 qv[QStage<T, D, RT, NT>::n];
+  q_load<T, D, RT, NT>(a, w.lv, w.b, w.rt_n, qv);
+  uint4 kr[kRing][NS];
 #pragma unroll
-  for (int p = 0; p < kPair; ++p) load_k_row<T, D>(a, kbase, s0, key_of(p), g, quad, ka[p]);
-#pragma unroll
-  for (int p = 0; p < kPair; ++p)
-    load_k_row<T, D>(a, kbase, s0, key_of(kPair + p), g, quad, kb[p]);
-  q_store<T, D, RTM, NT>(qv, q_lds);
+  for (int r = 0; r < kRing; ++r) load_k_row<T, D>(a, w.kbase, s0, key_of(r), g, quad, kr[r]);
+  q_store<T, D, RT, NT>(qv, q_lds);
   __syncthreads();
-  uint4 qreg[RegTiles<T, D, RTM>::n][NS];
+  uint4 qreg[RegTiles<T, D, RT>::n][NS];
 #pragma unroll
   for (int rt = 0; rt < RQ; ++rt)
 #pragma unroll
     for (int s = 0; s < NS; ++s) qreg[rt][s] = q_frag<T, D>(q_lds, rt, s, c, quad);
 
-  float ref[RTM], sum[RTM];
+  float ref[RT], sum[RT];
+  bool ready = false;   // every row's reference is set (wave-uniform)
 #pragma unroll
-  for (int rt = 0; rt < RTM; ++rt) {
+  for (int rt = 0; rt < RT; ++rt) {
     ref[rt] = -INFINITY;
     sum[rt] = 0.f;
   }
-  auto consume = [&](uint4 (&kf)[kPair][NS], int grp) {
+  auto consume = [&](const uint4 (&kf)[NS], int i) {
+    f32x4 acc[RT];
 #pragma unroll
-    for (int p = 0; p < kPair; ++p) {
-      const int base = c0 + 16 * (wave + NW * (kPair * grp + p));
-      f32x4 acc[RTM];
-#pragma unroll
-      for (int rt = 0; rt < RTM; ++rt)
-        if (rt < rt_n) acc[rt] = tile_logits<T, D, RTM, true>(kf[p], qreg, q_lds, rt, c, quad);
-      stats_update<RTM>(a, acc, ref, sum, rt_n, base, L, P, c, quad);
-    }
+    for (int rt = 0; rt < RT; ++rt)
+      acc[rt] = tile_logits<T, D, RT, true>(kf, qreg, q_lds, rt, c, quad);
+    stats_update<RT>(a, acc, ref, sum, ready, c0 + 16 * (wave + NW * i), L, P, c, quad);
   };
   // The chunk's partial: merge the four quads (same row c, different keys),
   // then the waves in order, and start the next chunk from empty pairs.
   auto flush = [&](int chunk) {
 #pragma unroll
-    for (int rt = 0; rt < RTM; ++rt) {
+    for (int rt = 0; rt < RT; ++rt) {
 #pragma unroll
       for (int o = 16; o <= 32; o <<= 1) {
         float ro = __shfl_xor(ref[rt], o);
@@ -137,34 +134,58 @@ __global__ __launch_bounds__(64 * kStatsWaves) void stats_kernel(const ScoreArgs
     }
     if (quad == 0) {
 #pragma unroll
-      for (int rt = 0; rt < RTM; ++rt) part[wave][rt * 16 + c] = make_float2(ref[rt], sum[rt]);
+      for (int rt = 0; rt < RT; ++rt) part[wave][rt * 16 + c] = make_float2(ref[rt], sum[rt]);
     }
     __syncthreads();
-    if (tid < rt_n * 16) {
+    if (tid < w.rt_n * 16) {
       float r0 = part[0][tid].x, s_0 = part[0][tid].y;
 #pragma unroll
-      for (int w = 1; w < NW; ++w) merge_stats(r0, s_0, part[w][tid].x, part[w][tid].y);
+      for (int v = 1; v < NW; ++v) merge_stats(r0, s_0, part[v][tid].x, part[v][tid].y);
       parts[(int64_t)chunk * a.row_slots + tid] = make_float2(r0, s_0);
     }
     __syncthreads();   // part is reused by the next chunk
+    ready = false;
 #pragma unroll
-    for (int rt = 0; rt < RTM; ++rt) {
+    for (int rt = 0; rt < RT; ++rt) {
       ref[rt] = -INFINITY;
       sum[rt] = 0.f;
     }
   };
-  int chunk = chunk0;
-  for (int grp = 0; grp < n_groups; grp += 2) {
-    consume(ka, grp);
+  int chunk = (int)blockIdx.y * a.cpw1;
+  for (int i = 0; i < n_tiles; i += kRing) {
 #pragma unroll
-    for (int p = 0; p < kPair; ++p)
-      load_k_row<T, D>(a, kbase, s0, key_of(kPair * (grp + 2) + p), g, quad, ka[p]);
-    consume(kb, grp + 1);
-#pragma unroll
-    for (int p = 0; p < kPair; ++p)
-      load_k_row<T, D>(a, kbase, s0, key_of(kPair * (grp + 3) + p), g, quad, kb[p]);
-    if ((grp + 2) % gpc == 0) flush(chunk++);   // loads of the next chunk are in flight
+    for (int r = 0; r < kRing; ++r) {
+      consume(kr[r], i + r);
+      load_k_row<T, D>(a, w.kbase, s0, key_of(i + r + kRing), g, quad, kr[r]);
+    }
+    if ((i + kRing) % tpc == 0) flush(chunk++);   // loads of the next chunk are in flight
   }
+}
+
+template <typename T, int D, int RTM, bool ML>
+__global__ __launch_bounds__(64 * kStatsWaves) void stats_kernel(const ScoreArgs a) {
+  Work w;
+  w.g = blockIdx.x;
+  w.layer = ML ? (int)blockIdx.z / a.batch : 0;
+  w.b = (int)blockIdx.z - w.layer * a.batch;
+  w.lv = layer_view<ML>(a, w.layer, w.g);
+  w.kbase = w.lv.k;
+  w.s0 = a.cu[w.b];
+  w.L = a.cu[w.b + 1] - w.s0;
+  const int chunk0 = (int)blockIdx.y * a.cpw1;
+  if (chunk0 == 0) {   // the column-sum kernel accumulates this histogram afterwards
+    int *h = a.hist + w.layer * a.hist_layer + ((int64_t)w.b * a.Hkv + w.g) * kHistBins;
+    for (int i = threadIdx.x; i < kHistBins; i += 64 * kStatsWaves) h[i] = 0;
+  }
+  w.c0 = chunk0 * a.chunk1;
+  if (w.c0 >= w.L) return;                   // uniform for the whole workgroup
+  w.n_chunks = min(a.cpw1, (w.L - w.c0 + a.chunk1 - 1) / a.chunk1);
+  w.P = w.L - a.W;
+  w.rt_n = w.lv.nsrh * a.th;
+
+  __shared__ uint4 q_lds[RTM * 16 * QLayout<T, D>::STRIDE];
+  __shared__ float2 part[kStatsWaves][16 * 12];
+  dispatch_rt<RTM>(w.rt_n, [&]<int RT>() { stats_body<T, D, RT>(a, w, q_lds, part); });
 }
 
 // ---------------------------------------------------------------------------
@@ -173,119 +194,128 @@ __global__ __launch_bounds__(64 * kStatsWaves) void stats_kernel(const ScoreArgs
 // MFMA operands: A = 16 window rows, B = 16 keys, so lane (quad, c) holds
 // rows 4*quad .. 4*quad+3 of the tile against key c.  The tiles of a chunk
 // plus one halo tile on each side, e = -1 .. chunk2/16, go to the waves
-// round-robin (chunk2 + 32 keys = 16 * kWaves * kPair * groups per chunk);
-// the pipeline runs on across chunks, each chunk ending with its pooling.
+// round-robin (chunk2 + 32 keys = 16 * kWaves * tiles per wave and chunk);
+// the ring runs on across chunks, each chunk ending with its pooling.
 // ---------------------------------------------------------------------------
-template <typename T, int D, int RTM, bool ML>
-__global__ __launch_bounds__(64 * kWaves) void colsum_kernel(const ScoreArgs a) {
-  constexpr int NS = Slices<T, D>::n, RQ = RegTiles<T, D, RTM>::v;
+template <typename T, int D, int RT, int CSW>
+__device__ __forceinline__ void colsum_body(const ScoreArgs &a, const Work &w, uint4 *q_lds,
+                                            float *bias_s, float (*cs)[CSW], float *stage,
+                                            int *hist_s) {
+  constexpr int NS = Slices<T, D>::n, RQ = RegTiles<T, D, RT>::v;
   constexpr int NT = 64 * kWaves;
-  constexpr int kMaxSrh = RTM;   // th >= 1
-  const int g = blockIdx.x;
-  const int layer = ML ? (int)blockIdx.z / a.batch : 0;
-  const int b = (int)blockIdx.z - layer * a.batch;
-  const LayerView lv = layer_view<ML>(a, layer, g);
-  const gptr<const char> kbase = lv.k;
-  const int s0 = a.cu[b];
-  const int L = a.cu[b + 1] - s0;
-  const int c0 = (int)blockIdx.y * a.cpw2 * a.chunk2;
-  if (c0 >= L) return;
-  const int c_end = min(L, c0 + a.cpw2 * a.chunk2);
-  const int P = L - a.W;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int c = lane & 15, quad = lane >> 4;
   const int tid = threadIdx.x;
-  const int nh = lv.nsrh;
-  const int rt_n = nh * a.th;
-  const gptr<float> out = lv.scores + (int64_t)g * a.T + s0;
-
-  // Window positions of this range are always kept: +inf.
-  for (int j = max(c0, P) + tid; j < c_end; j += NT) out[j] = INFINITY;
-  if (c0 >= P) return;                        // no prefix key in this range
-  // chunks of the range that hold prefix keys
-  const int n_chunks = min(a.cpw2, (P - c0 + a.chunk2 - 1) / a.chunk2);
-  const int gpc = (a.chunk2 + 32) / (16 * kWaves * kPair);   // 2-tile groups per wave and chunk
-  const int n_groups = gpc * n_chunks;
+  const int c0 = w.c0, L = w.L, P = w.P, s0 = w.s0, g = w.g;
+  const gptr<float> out = w.lv.scores + (int64_t)g * a.T + s0;
+  const int tpc = (a.chunk2 + 32) / (16 * kWaves);   // key tiles per wave and chunk
+  const int n_tiles = tpc * w.n_chunks;
   // chunk, tile index e in the chunk and key row of this lane for the i-th
   // tile of this wave (clamped into the chunk and its halo)
   auto key_of = [&](int i) {
-    const int grp = i / kPair;
-    const int ch = grp / gpc;
-    const int e = -1 + wave + kWaves * (i - ch * gpc * kPair);
+    const int ch = i / tpc;
+    const int e = -1 + wave + kWaves * (i - ch * tpc);
     const int cc0 = c0 + ch * a.chunk2;
     const int k_first = max(cc0 - 16, 0), k_last = min(cc0 + a.chunk2 + 16, L) - 1;
     return min(max(cc0 + 16 * e + c, k_first), k_last);
   };
 
-  __shared__ uint4 q_lds[RTM * 16 * QLayout<T, D>::STRIDE];
-  __shared__ float bias_s[RTM * 16];
-  __shared__ float cs[kMaxSrh][kMaxChunk2 + 32];
-  __shared__ int hist_s[kHistBins];
-  uint4 qv[QStage<T, D, RTM, NT>::n];
-  q_load<T, D, RTM, NT>(a, lv, b, rt_n, qv);
-  uint4 ka[kPair][NS], kb[kPair][NS];
+  uint4 qv[QStage<T, D, RT, NT>::n];
+  q_load<T, D, RT, NT>(a, w.lv, w.b, w.rt_n, qv);
+  uint4 kr[kRing][NS];
 #pragma unroll
-  for (int p = 0; p < kPair; ++p) load_k_row<T, D>(a, kbase, s0, key_of(p), g, quad, ka[p]);
-#pragma unroll
-  for (int p = 0; p < kPair; ++p)
-    load_k_row<T, D>(a, kbase, s0, key_of(kPair + p), g, quad, kb[p]);
-  q_store<T, D, RTM, NT>(qv, q_lds);
+  for (int r = 0; r < kRing; ++r) load_k_row<T, D>(a, w.kbase, s0, key_of(r), g, quad, kr[r]);
+  q_store<T, D, RT, NT>(qv, q_lds);
   for (int i = tid; i < kHistBins; i += NT) hist_s[i] = 0;
 
   // Row normalisers bias = ref + log2(sum), merged over every chunk of the
-  // statistics pass.
+  // statistics pass; rows past the group's own get +inf.
   merge_row_bias<NT>(a,
-                     a.stats + layer * a.stats_layer +
-                         ((int64_t)b * a.Hkv + g) * a.parts_stride * a.row_slots,
-                     a.row_slots, (L + a.chunk1 - 1) / a.chunk1, rt_n * 16, RTM * 16, bias_s);
+                     a.stats + w.layer * a.stats_layer +
+                         ((int64_t)w.b * a.Hkv + g) * a.parts_stride * a.row_slots,
+                     a.row_slots, (L + a.chunk1 - 1) / a.chunk1, w.rt_n * 16, RT * 16, bias_s);
   __syncthreads();
-  uint4 qreg[RegTiles<T, D, RTM>::n][NS];
+  uint4 qreg[RegTiles<T, D, RT>::n][NS];
 #pragma unroll
   for (int rt = 0; rt < RQ; ++rt)
 #pragma unroll
     for (int s = 0; s < NS; ++s) qreg[rt][s] = q_frag<T, D>(q_lds, rt, s, c, quad);
-  float bias[RTM][4];
+  float bias[RT][4];
 #pragma unroll
-  for (int rt = 0; rt < RTM; ++rt)
+  for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
     for (int r = 0; r < 4; ++r) bias[rt][r] = bias_s[rt * 16 + 4 * quad + r];
 
   // Column sums of a chunk plus one 16-key halo tile on each side:
   // cs[h][16 + x] holds the window sum of SRH h at key cc0 + x.
-  auto consume = [&](uint4 (&kf)[kPair][NS], int grp) {
-    const int ch = grp / gpc;
+  auto consume = [&](const uint4 (&kf)[NS], int i) {
+    const int ch = i / tpc;
     const int cc0 = c0 + ch * a.chunk2;
     const int p_end = min(cc0 + a.chunk2, P);
     const int ntiles = (p_end - cc0 + 15) >> 4;                       // tiles e = 0 .. ntiles-1
     const int e_lo = (cc0 > 0) ? -1 : 0;                              // left halo tile
     const int e_hi = (cc0 + 16 * ntiles < P) ? ntiles : ntiles - 1;   // right halo tile
-#pragma unroll
-    for (int p = 0; p < kPair; ++p) {
-      const int e = -1 + wave + kWaves * (kPair * (grp - ch * gpc) + p);
-      tile_window_sums<T, D, RTM, kMaxChunk2 + 32>(a, kf[p], qreg, q_lds, bias, rt_n, e,
-                                                   e >= e_lo && e <= e_hi, c, quad, cs);
-    }
+    const int e = -1 + wave + kWaves * (i - ch * tpc);
+    tile_window_sums<T, D, RT, CSW>(a, kf, qreg, q_lds, bias, e, e >= e_lo && e <= e_hi, c,
+                                    quad, cs);
   };
-  // Pooling of a finished chunk (S4); cs is rewritten by the next chunk only
-  // after every thread has pooled.
+  // Pooling of a finished chunk (S4); cs and stage are rewritten by the next
+  // chunk only after every thread has pooled and stored.
   auto pool = [&](int ch) {
     const int cc0 = c0 + ch * a.chunk2;
     __syncthreads();
-    pool_scores<NT, kMaxChunk2 + 32>(a, cs, nh, cc0, min(cc0 + a.chunk2, P), P, out, hist_s);
+    pool_chunk<NT, CSW>(a, cs, w.lv.nsrh, cc0, min(cc0 + a.chunk2, P), P, out, stage, hist_s);
     __syncthreads();
   };
-  for (int grp = 0; grp < n_groups; grp += 2) {
-    consume(ka, grp);
+  for (int i = 0; i < n_tiles; i += kRing) {
 #pragma unroll
-    for (int p = 0; p < kPair; ++p)
-      load_k_row<T, D>(a, kbase, s0, key_of(kPair * (grp + 2) + p), g, quad, ka[p]);
-    consume(kb, grp + 1);
-#pragma unroll
-    for (int p = 0; p < kPair; ++p)
-      load_k_row<T, D>(a, kbase, s0, key_of(kPair * (grp + 3) + p), g, quad, kb[p]);
-    if ((grp + 2) % gpc == 0) pool(grp / gpc);   // loads of the next chunk are in flight
+    for (int r = 0; r < kRing; ++r) {
+      consume(kr[r], i + r);
+      load_k_row<T, D>(a, w.kbase, s0, key_of(i + r + kRing), g, quad, kr[r]);
+    }
+    if ((i + kRing) % tpc == 0) pool(i / tpc);   // loads of the next chunk are in flight
   }
-  flush_hist<NT>(hist_s, a.hist + layer * a.hist_layer + ((int64_t)b * a.Hkv + g) * kHistBins);
+  flush_hist<NT>(hist_s,
+                 a.hist + w.layer * a.hist_layer + ((int64_t)w.b * a.Hkv + g) * kHistBins);
+}
+
+template <typename T, int D, int RTM, bool ML>
+__global__ __launch_bounds__(64 * kWaves) void colsum_kernel(const ScoreArgs a) {
+  constexpr int NT = 64 * kWaves;
+  constexpr int CSW = kMaxChunk2 + 32;
+  Work w;
+  w.g = blockIdx.x;
+  w.layer = ML ? (int)blockIdx.z / a.batch : 0;
+  w.b = (int)blockIdx.z - w.layer * a.batch;
+  w.lv = layer_view<ML>(a, w.layer, w.g);
+  w.kbase = w.lv.k;
+  w.s0 = a.cu[w.b];
+  w.L = a.cu[w.b + 1] - w.s0;
+  w.c0 = (int)blockIdx.y * a.cpw2 * a.chunk2;
+  if (w.c0 >= w.L) return;
+  w.P = w.L - a.W;
+  const int c_end = min(w.L, w.c0 + a.cpw2 * a.chunk2);
+  // Window positions of this range are always kept: +inf.
+  const gptr<float> out = w.lv.scores + (int64_t)w.g * a.T + w.s0;
+  for (int j = max(w.c0, w.P) + (int)threadIdx.x; j < c_end; j += NT) out[j] = INFINITY;
+  if (w.c0 >= w.P) return;                   // no prefix key in this range
+  // chunks of the range that hold prefix keys
+  w.n_chunks = min(a.cpw2, (w.P - w.c0 + a.chunk2 - 1) / a.chunk2);
+  w.rt_n = w.lv.nsrh * a.th;
+
+  // The staging buffer of the pooled scores is left out where it would not fit
+  // (fp32 queries with 12 row tiles); those scores are stored directly.
+  constexpr size_t kLds = sizeof(uint4) * RTM * 16 * QLayout<T, D>::STRIDE +
+                          sizeof(float) * (RTM * 16 + RTM * CSW + kHistBins);
+  constexpr int kStage = kLds + sizeof(float) * kMaxChunk2 <= 160 * 1024 ? kMaxChunk2 : 0;
+  __shared__ uint4 q_lds[RTM * 16 * QLayout<T, D>::STRIDE];
+  __shared__ float bias_s[RTM * 16];
+  __shared__ float cs[RTM][CSW];   // th >= 1: at most RTM SRHs
+  __shared__ float stage[kStage > 0 ? kStage : 1];   // one chunk's pooled scores
+  __shared__ int hist_s[kHistBins];
+  dispatch_rt<RTM>(w.rt_n, [&]<int RT>() {
+    colsum_body<T, D, RT, CSW>(a, w, q_lds, bias_s, cs, kStage > 0 ? stage : nullptr, hist_s);
+  });
 }
 
 // ---------------------------------------------------------------------------

@@ -216,7 +216,7 @@ def test_deterministic_bits(gpu):
 
 def test_scoring_path_choice_for_the_benchmark_shapes(gpu, scoring_path):
     for name, kw in [("llama1", {}), ("llama32", {}), ("ragged8", {}), ("tiny", {}),
-                     ("qwen128k", dict(seq_len=65536))]:
+                     ("qwen128k", dict(seq_len=32768))]:
         w = wl.get(name, **kw)
         lens = wl.seq_lengths(w)
         cu = wl.cu_seqlens(lens)
