@@ -31,6 +31,27 @@ if ROOT not in sys.path:
 
 METRIC = "prompt tokens compressed/sec per layer (1 GPU); % HBM roofline; MFMA util"
 HBM_PEAK_GBS = 8000.0
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # dense, MI355X
+
+# HBM bytes moved by one score phase (stats_kernel + colsum_kernel), measured
+# with rocprofv3: FETCH_SIZE x 2 (the factor a plain copy of known size gives
+# on this GPU) + WRITE_SIZE, in separate runs (profiles/).  A figure is valid
+# only for the kernel sources it was taken with: keyed by their hash.
+MEASURED_TRAFFIC = {
+    ("llama32", 32, "c68acfffd41e0b13"): (2 * (1053085.7 + 1188982.4) + 6248.0 + 33013.5) * 1024,
+}
+
+
+def kernel_source_hash() -> str:
+    import hashlib
+    import glob
+    root = os.path.join(ROOT, "paper_2606_24467_amd", "csrc")
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(root, "*.h")) + glob.glob(os.path.join(root, "*.hip"))):
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
 
 
 def log(*a):
@@ -152,6 +173,7 @@ def main():
     probs, outs = [], []
     score_bytes_total = 0
     alg_bytes_total = 0
+    score_flops_total = 0   # one pass of window-row x key dot products
     for lay in layers:
         p = C.Problem(lay["q_win"], lay["k"], lay["v"], lay["cu_seqlens"],
                       cu_seqlens_host=lay["cu_seqlens_host"], pool_kernel=w.pool_kernel,
@@ -164,6 +186,7 @@ def main():
                      torch.empty(shape, dtype=lay["v"].dtype, device=dev)))
         n_srh = int(lay["srh_mask"].sum())
         sb, gb = algorithmic_bytes(lens, w.n_kv_heads, w.head_dim, es, w.window, n_srh, B_l)
+        score_flops_total += 2 * w.window * n_srh * w.head_dim * sum(lens)
         score_bytes_total += sb
         alg_bytes_total += sb + gb
     q_l = [lay["q_win"] for lay in layers]
@@ -232,12 +255,15 @@ def main():
     value = tokens * n_layers / (ms_per_step / 1e3)
     achieved = score_bytes_total / (score_ms / 1e3) / 1e9
     e2e_gbs = alg_bytes_total / (ms_per_step / 1e3) / 1e9
+    traffic = MEASURED_TRAFFIC.get((w.name, n_layers, kernel_source_hash()))
+    dt = "bf16" if w.dtype == wl.BF16 else "f32"
+    mfma_tflops = score_flops_total / (score_ms / 1e3) / 1e12
 
     result = {
         "metric": METRIC, "value": value, "unit": "tokens/s/layer", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "bf16" if w.dtype == wl.BF16 else "f32", "data": "synthetic",
+        "dtype": dt, "data": "synthetic",
         "config": {"workload": f"{w.name}: {n_layers} layers, batch {w.batch}, "
                                f"{w.n_q_heads}q/{w.n_kv_heads}kv heads, D={w.head_dim}, "
                                f"L={'ragged ' + str(w.ragged) if w.ragged else w.seq_len}, "
@@ -248,8 +274,12 @@ def main():
                      "kernel": f"score phase: stats_kernel + colsum_kernel over {n_layers} "
                                f"layers (one compresskv_score_layers call)",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "avg_ms": score_ms, "bytes_per_launch": score_bytes_total},
+        "mfma": {"flops_per_launch": score_flops_total, "achieved": mfma_tflops,
+                 "peak": MFMA_PEAK_TFLOPS[dt], "unit": "TFLOP/s",
+                 "frac": mfma_tflops / MFMA_PEAK_TFLOPS[dt],
+                 "note": "algorithmic Q.K^T FLOPs of the score phase (one pass)"},
         "end_to_end": {"algorithmic_bytes_per_step": alg_bytes_total, "achieved_gbs": e2e_gbs,
                        "frac": e2e_gbs / HBM_PEAK_GBS},
     }
