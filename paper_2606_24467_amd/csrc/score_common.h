@@ -19,7 +19,8 @@ struct QLayout {
   static constexpr int STRIDE = U4 + 1;        // padded row stride in LDS (bank spread)
 };
 
-constexpr int kWaves = 8;       // waves per column-sum workgroup
+constexpr int kWaves = 4;       // waves per column-sum workgroup (two per CU: one streams
+                                // keys while the other pools its chunk)
 constexpr int kRing = 4;        // key tiles per wave in the load ring: kRing - 1 in flight
                                 // while one is consumed
 

@@ -189,7 +189,7 @@ __global__ __launch_bounds__(64 * kStatsWaves) void stats_kernel(const ScoreArgs
 }
 
 // ---------------------------------------------------------------------------
-// S2+S3+S4.  Grid (Hkv, ceil(max_chunks2 / cpw2), batch [x layers]), 512
+// S2+S3+S4.  Grid (Hkv, ceil(max_chunks2 / cpw2), batch [x layers]), 256
 // threads; a workgroup covers cpw2 consecutive chunks of chunk2 keys.
 // MFMA operands: A = 16 window rows, B = 16 keys, so lane (quad, c) holds
 // rows 4*quad .. 4*quad+3 of the tile against key c.  The tiles of a chunk
