@@ -153,7 +153,7 @@ struct GatherArgs {
 
 // One layer of the table as the host hands it over (SRH mask as bits over the
 // query heads); put_layers_kernel expands the mask into per-group lists.
-constexpr int kPutLayers = 8;
+constexpr int kPutLayers = 32;   // ~3.1 KB of kernel arguments: one launch for up to 32 layers
 struct PutEntry {
   const void *q, *k, *v;
   float *scores;
