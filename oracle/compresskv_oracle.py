@@ -9,7 +9,9 @@ What it computes (CompressKV, section 3.3 "Token selection driven by Semantic
 Retrieval Heads", with the SnapKV local-window setting of section 4,
 "Implementation Details"):
 
-  for every sequence b and every KV group g of one layer
+  for every sequence b and every KV group g of one layer (per-group mode; the
+  layer-shared mode averages the pooled vectors of all the layer's SRHs and
+  keeps one index set for every group)
     1. attention of the last W prompt queries of each Semantic Retrieval Head
        (SRH) h of the group against all keys of the prompt, causal inside the
        window, softmax over the whole row;
@@ -50,6 +52,8 @@ POOL_MAX = 0
 POOL_AVG = 1
 POOL_THEN_MEAN = 0
 MEAN_THEN_POOL = 1
+PER_GROUP = 0       # one index set per KV group, chosen by that group's SRHs
+LAYER_SHARED = 1    # one index set for every head of the layer (section 3.3)
 
 
 # --------------------------------------------------------------------------
@@ -150,6 +154,32 @@ def group_scores(q_heads: list[np.ndarray], k_seq: np.ndarray, scale: float,
 
 
 # --------------------------------------------------------------------------
+# Steps 1-4 for a whole layer with one shared index set (section 3.3: the
+# layer's top SRHs, each attending to its own group's keys, are compressed by
+# the window sum and pooling, and the compressed vectors are averaged; every
+# head of the layer then keeps the same tokens).  Pool each SRH, then average
+# (the paper's order).
+# --------------------------------------------------------------------------
+def layer_scores(q_and_keys: list[tuple[np.ndarray, np.ndarray]], scale: float,
+                 pool_kernel: int, pool_type: int = POOL_MAX) -> np.ndarray:
+    """Score of every prefix token of one sequence for the whole layer.
+
+    q_and_keys: one (q [W, D], k [L, D]) pair per SRH of the layer, k being
+    the keys of the SRH's own KV group.
+    """
+    W = q_and_keys[0][0].shape[0]
+    L = q_and_keys[0][1].shape[0]
+    P = L - W
+    if P == 0:
+        return np.zeros(0)
+    pooled = []
+    for q, k_seq in q_and_keys:
+        a = row_softmax(window_logits(q, k_seq, scale))
+        pooled.append(pool1d(window_column_sums(a, P), pool_kernel, pool_type))
+    return np.mean(np.stack(pooled), axis=0)
+
+
+# --------------------------------------------------------------------------
 # Step 5: budgeted top-N that always keeps the window (section 3.3: the N
 # best-scoring tokens keep their KV pairs, the rest are evicted; the window
 # is kept as in SnapKV, section 4).
@@ -188,8 +218,9 @@ def compress_layer(q_win: np.ndarray, k: np.ndarray, v: np.ndarray,
                    pool_kernel: int, pool_type: int = POOL_MAX,
                    reduce_order: int = POOL_THEN_MEAN, scale: float | None = None,
                    k_values: np.ndarray | None = None,
-                   q_values: np.ndarray | None = None) -> LayerResult:
-    """CompressKV eviction of one layer, per KV group.
+                   q_values: np.ndarray | None = None,
+                   index_mode: int = PER_GROUP) -> LayerResult:
+    """CompressKV eviction of one layer.
 
     q_win: [batch, W, Hq, D] window queries (any float dtype, or raw bits when
            q_values gives the float64 values).
@@ -198,6 +229,10 @@ def compress_layer(q_win: np.ndarray, k: np.ndarray, v: np.ndarray,
            (needed when k holds raw bf16 bits).
     cu_seqlens: [batch+1] offsets of the sequences in the packed T axis.
     srh_mask: [Hq] nonzero for Semantic Retrieval Heads.
+    index_mode: PER_GROUP (each KV group selects with its own SRHs; every
+        group needs one) or LAYER_SHARED (one selection from all the layer's
+        SRHs, kept by every group; pool-then-mean only; scores[g] then holds
+        the layer score for every g).
     """
     qv = np.asarray(q_values if q_values is not None else q_win, dtype=np.float64)
     kv = np.asarray(k_values if k_values is not None else k, dtype=np.float64)
@@ -210,6 +245,29 @@ def compress_layer(q_win: np.ndarray, k: np.ndarray, v: np.ndarray,
     k_out = np.zeros((batch, Hkv, budget, D), dtype=k.dtype)
     v_out = np.zeros((batch, Hkv, budget, D), dtype=v.dtype)
     scores = np.zeros((Hkv, T), dtype=np.float64)
+    if index_mode == LAYER_SHARED:
+        if reduce_order != POOL_THEN_MEAN:
+            raise ValueError("the layer-shared index set pools each SRH, then averages")
+        srh = [h for h in range(Hq) if srh_mask[h]]
+        if not srh:
+            raise ValueError("the layer has no Semantic Retrieval Head")
+        for b in range(batch):
+            s0, s1 = int(cu_seqlens[b]), int(cu_seqlens[b + 1])
+            L = s1 - s0
+            P = L - W
+            sc = layer_scores([(qv[b, :, h, :], kv[s0:s1, h // G, :]) for h in srh], scale,
+                              pool_kernel, pool_type)
+            sel = select_tokens(sc, L, W, budget)
+            n = sel.shape[0]
+            for g in range(Hkv):
+                scores[g, s0:s0 + P] = sc
+                scores[g, s0 + P:s1] = np.inf
+                idx[b, g, :n] = sel
+                k_out[b, g, :n] = k[s0 + sel, g, :]
+                v_out[b, g, :n] = v[s0 + sel, g, :]
+        return LayerResult(idx=idx, k_out=k_out, v_out=v_out, scores=scores)
+    if index_mode != PER_GROUP:
+        raise ValueError("unknown index mode")
     for b in range(batch):
         s0, s1 = int(cu_seqlens[b]), int(cu_seqlens[b + 1])
         L = s1 - s0

@@ -6,6 +6,7 @@ import pytest
 
 import oracle as O
 import oracle.compresskv_oracle as M
+from tests import test_oracle_layer_shared as lpins
 from tests import test_oracle_pins as pins
 from tests import test_workloads as wtests
 
@@ -85,8 +86,18 @@ def _group_scores_wrong_order(q_heads, k_seq, scale, pool_kernel, pool_type=0, r
     return _orig["group_scores"](q_heads, k_seq, scale, pool_kernel, pool_type, 1 - reduce_order)
 
 
+def _layer_scores_first_group_keys(q_and_keys, scale, pool_kernel, pool_type=0):
+    k0 = q_and_keys[0][1]                                # every SRH reads group 0's keys
+    return _orig["layer_scores"]([(q, k0) for q, _ in q_and_keys], scale, pool_kernel, pool_type)
+
+
+def _layer_scores_sum(q_and_keys, scale, pool_kernel, pool_type=0):
+    return _orig["layer_scores"](q_and_keys, scale, pool_kernel, pool_type) * len(q_and_keys)
+
+
 _orig = {name: getattr(M, name) for name in
-         ("window_logits", "window_column_sums", "pool1d", "select_tokens", "group_scores")}
+         ("window_logits", "window_column_sums", "pool1d", "select_tokens", "group_scores",
+          "layer_scores")}
 
 MUTANTS = {
     "window keys left out of the softmax": ("window_logits", _logits_no_window_in_denominator),
@@ -101,6 +112,8 @@ MUTANTS = {
     "keeps the lowest scores": ("select_tokens", _select_smallest),
     "sum over SRHs instead of mean": ("group_scores", _group_scores_sum_heads),
     "pool and head mean swapped": ("group_scores", _group_scores_wrong_order),
+    "layer SRHs read one group's keys": ("layer_scores", _layer_scores_first_group_keys),
+    "sum over the layer's SRHs": ("layer_scores", _layer_scores_sum),
 }
 
 PINS = [
@@ -115,6 +128,9 @@ PINS = [
     pins.test_select_constant_scores_keeps_lowest_positions,
     pins.test_all_heads_mask_is_snapkv_gqa,
     lambda: wtests.test_needles_retained_by_oracle_on_tiny(0),
+    lambda: lpins.test_layer_shared_matches_batched_torch(0, O.POOL_MAX,
+                                                          [1, 0, 0, 0, 1, 1, 1, 0]),
+    lpins.test_layer_score_weights_heads_not_groups,
 ]
 
 
