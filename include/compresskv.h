@@ -66,6 +66,12 @@ extern "C" {
 #define CKV_POOL_THEN_MEAN 0 /* pool each SRH, then average (section 3.3) */
 #define CKV_MEAN_THEN_POOL 1 /* average the SRH window sums, then pool once */
 
+/* which heads share an index set */
+#define CKV_INDEX_PER_GROUP 0 /* every KV group selects with its own SRHs (each group needs one) */
+#define CKV_INDEX_LAYER 1     /* section 3.3: one selection per sequence from all the layer's SRHs
+                                 (each against its own group's keys), kept by every group;
+                                 groups without an SRH are allowed; CKV_POOL_THEN_MEAN only */
+
 /* Sizes and options of one layer.  head_dim must be 64 or 128. */
 typedef struct ckv_problem {
   int32_t batch;        /* number of packed sequences, >= 1 */
@@ -82,6 +88,8 @@ typedef struct ckv_problem {
   const int32_t *cu_seqlens_host; /* host copy of the same offsets */
   int64_t k_stride_tok, k_stride_head; /* elements; >= D, 16-byte aligned rows */
   int64_t v_stride_tok, v_stride_head;
+  int32_t index_mode;   /* CKV_INDEX_PER_GROUP (0) or CKV_INDEX_LAYER */
+  int32_t reserved;     /* must be 0 */
 } ckv_problem;
 
 /*
@@ -96,8 +104,11 @@ size_t compresskv_workspace_bytes(const ckv_problem *p, const uint8_t *srh_mask_
  * S1-S4: pooled, SRH-averaged score of every prefix token, per KV group.
  *   scores[g, t] for t in sequence b: the score of position t - cu[b] if that
  *   position is a prefix position (< L_b - W), +inf on the W window positions.
- * srh_mask_host: uint8 [n_q_heads]; every KV group needs at least one SRH and
- *   at most 12 row tiles (ceil(W/16) * n_srh <= 12).
+ *   With CKV_INDEX_LAYER every row g holds the layer score (the mean over all
+ *   the layer's SRHs of their pooled window sums).
+ * srh_mask_host: uint8 [n_q_heads]; every KV group needs at least one SRH
+ *   (CKV_INDEX_LAYER: the layer needs one) and at most 12 row tiles
+ *   (ceil(W/16) * n_srh <= 12).
  * Every sequence needs L_b >= W.  ws: >= compresskv_workspace_bytes(), any
  * contents, 256-byte aligned.
  */
@@ -107,7 +118,8 @@ int compresskv_score(const ckv_problem *p, const void *q_win, const void *k,
 
 /*
  * S5: retained positions per (sequence, KV group), ascending, from scores laid
- * out as compresskv_score writes them.  If L_b <= budget all L_b positions
+ * out as compresskv_score writes them (with CKV_INDEX_LAYER: one selection per
+ * sequence from row 0, written into every group's row of idx).  If L_b <= budget all L_b positions
  * are kept; otherwise the (budget - W) highest prefix scores (ties: lowest
  * position) and the W window positions.  Entries past the kept count are -1.
  * Requires budget >= W.  Scores must be non-negative or +inf (NaN: undefined).

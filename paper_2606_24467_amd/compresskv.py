@@ -20,6 +20,7 @@ OK, INVALID_ARGUMENT, UNSUPPORTED, WORKSPACE_TOO_SMALL, HIP_ERROR = 0, 1, 2, 3, 
 F32, BF16 = 0, 1
 POOL_MAX, POOL_AVG = 0, 1
 POOL_THEN_MEAN, MEAN_THEN_POOL = 0, 1
+INDEX_PER_GROUP, INDEX_LAYER = 0, 1
 
 _HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
                        "include", "compresskv.h")
@@ -43,6 +44,8 @@ class CkvProblem(ctypes.Structure):
         ("k_stride_head", ctypes.c_int64),
         ("v_stride_tok", ctypes.c_int64),
         ("v_stride_head", ctypes.c_int64),
+        ("index_mode", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
     ]
 
 
@@ -137,7 +140,7 @@ class Problem:
     def __init__(self, q_win: torch.Tensor, k: torch.Tensor, v: torch.Tensor,
                  cu_seqlens: torch.Tensor, *, cu_seqlens_host=None, pool_kernel: int = 7,
                  pool_type: int = POOL_MAX, reduce_order: int = POOL_THEN_MEAN,
-                 scale: float | None = None):
+                 scale: float | None = None, index_mode: int = INDEX_PER_GROUP):
         if q_win.dim() != 4 or k.dim() != 3 or v.dim() != 3:
             raise ValueError("q_win must be [batch, W, Hq, D], k and v [T, Hkv, D]")
         if q_win.dtype not in _DTYPES or k.dtype != q_win.dtype or v.dtype != q_win.dtype:
@@ -164,7 +167,8 @@ class Problem:
             reduce_order=reduce_order, scale=float(scale) if scale else 0.0,
             cu_seqlens=cu_seqlens.data_ptr(), cu_seqlens_host=self._cu_host.ctypes.data,
             k_stride_tok=k.stride(0), k_stride_head=k.stride(1),
-            v_stride_tok=v.stride(0), v_stride_head=v.stride(1))
+            v_stride_tok=v.stride(0), v_stride_head=v.stride(1), index_mode=index_mode,
+            reserved=0)
 
     @property
     def lengths(self) -> np.ndarray:

@@ -118,6 +118,11 @@ int check_problem(const ckv_problem *p) {
     return fail(CKV_INVALID_ARGUMENT, "reduce_order must be CKV_POOL_THEN_MEAN or CKV_MEAN_THEN_POOL");
   if (!(std::isfinite(p->scale)))
     return fail(CKV_INVALID_ARGUMENT, "scale must be finite");
+  if (p->index_mode != CKV_INDEX_PER_GROUP && p->index_mode != CKV_INDEX_LAYER)
+    return fail(CKV_INVALID_ARGUMENT, "index_mode must be CKV_INDEX_PER_GROUP or CKV_INDEX_LAYER");
+  if (p->reserved != 0) return fail(CKV_INVALID_ARGUMENT, "reserved must be 0");
+  if (p->index_mode == CKV_INDEX_LAYER && p->reduce_order != CKV_POOL_THEN_MEAN)
+    return fail(CKV_UNSUPPORTED, "CKV_INDEX_LAYER needs reduce_order CKV_POOL_THEN_MEAN");
   if (!p->cu_seqlens || !p->cu_seqlens_host)
     return fail(CKV_INVALID_ARGUMENT, "cu_seqlens and cu_seqlens_host are both required");
   if (!aligned(p->cu_seqlens, 4)) return fail(CKV_UNSUPPORTED, "cu_seqlens must be 4-byte aligned");
@@ -139,7 +144,8 @@ int check_problem(const ckv_problem *p) {
 }
 
 // Per-group SRH lists of one layer from its host mask (`layer` only names it
-// in messages).
+// in messages).  Every group needs an SRH, except with the layer-shared index
+// set, which needs one in the layer.
 int layer_srh(const ckv_problem *p, const uint8_t *mask, int layer, LayerSrh &ls) {
   if (!mask) return fail(CKV_INVALID_ARGUMENT, "srh_mask_host is NULL");
   const int G = p->n_q_heads / p->n_kv_heads;
@@ -154,12 +160,14 @@ int layer_srh(const ckv_problem *p, const uint8_t *mask, int layer, LayerSrh &ls
         ++n;
       }
     }
-    if (n == 0)
+    if (n == 0 && p->index_mode != CKV_INDEX_LAYER)
       return fail(CKV_INVALID_ARGUMENT, "layer %d: KV group %d has no Semantic Retrieval Head",
                   layer, g);
     ls.nmax = std::max(ls.nmax, n);
     ls.off[g + 1] = (uint16_t)ls.head.size();
   }
+  if (ls.head.empty())
+    return fail(CKV_INVALID_ARGUMENT, "layer %d has no Semantic Retrieval Head", layer);
   return CKV_OK;
 }
 
@@ -195,6 +203,7 @@ void choose_path(const ckv_problem *p, Plan &pl) {
   pl.fused = false;
   const char *path = std::getenv("CKV_PATH");
   if (!path || std::string(path) != "single") return;
+  if (p->index_mode == CKV_INDEX_LAYER) return;   // its groups may have no SRH
   if (p->batch > ckv::kFusedMaxBatch) return;
   for (int ut : {4, 2}) {
     const int resident = ckv::fused_resident_workgroups(p->dtype == CKV_BF16, p->head_dim,
@@ -371,7 +380,27 @@ ckv::SelectArgs select_args(const ckv_problem *p, const Plan &pl, const int *his
   s.Hkv = p->n_kv_heads;
   s.W = p->window;
   s.batch = p->batch;
+  const bool shared = p->index_mode == CKV_INDEX_LAYER;
+  s.n_sel = shared ? 1 : p->n_kv_heads;
+  s.out_groups = shared ? p->n_kv_heads : 1;
+  if (shared) s.hist = nullptr;   // the histograms are per group: count the layer score
   return s;
+}
+
+// Layer-shared index set: the layer score into every group's row.
+hipError_t launch_combine_if_shared(const ckv_problem *p, const Plan &pl, const LayerSrh *srh,
+                                    float *scores, const ckv::LayerDesc *table, int n_layers,
+                                    hipStream_t stream) {
+  if (p->index_mode != CKV_INDEX_LAYER) return hipSuccess;
+  ckv::CombineArgs c{};
+  if (srh) c.l0 = layer_desc(srh, nullptr, nullptr, nullptr, scores, nullptr, nullptr, nullptr, 0);
+  c.layers = table;
+  c.cu = p->cu_seqlens;
+  c.T = (int32_t)pl.T;
+  c.Hkv = p->n_kv_heads;
+  c.W = p->window;
+  c.batch = p->batch;
+  return ckv::launch_combine(c, n_layers, pl.lmax, stream);
 }
 
 ckv::GatherArgs gather_args(const ckv_problem *p) {
@@ -532,6 +561,9 @@ int run_layers(const ckv_problem *p, int n_layers, const LayerPtrs &lp, const ui
                                                 p->batch, n_layers, s),
                        "score")))
     return st;
+  if ((st = hip_status(launch_combine_if_shared(p, pl, nullptr, nullptr, table, n_layers, s),
+                       "combine")))
+    return st;
   if (!full) return ok();
   ckv::SelectArgs sa = select_args(p, pl, a.hist);
   sa.layers = table;
@@ -596,6 +628,10 @@ int compresskv_score(const ckv_problem *p, const void *q_win, const void *k,
   if ((st = hip_status(launch_scoring(p, pl, q_win, k, scores, ws, (hipStream_t)stream),
                        "score")))
     return st;
+  if ((st = hip_status(
+           launch_combine_if_shared(p, pl, &pl.srh, scores, nullptr, 0, (hipStream_t)stream),
+           "combine")))
+    return st;
   return ok();
 }
 
@@ -655,6 +691,9 @@ int compresskv_compress_layer(const ckv_problem *p, const void *q_win, const voi
                       : reinterpret_cast<float *>(static_cast<char *>(ws) + pl.scores_off);
   hipStream_t s = (hipStream_t)stream;
   if ((st = hip_status(launch_scoring(p, pl, q_win, k, scores, ws, s), "score"))) return st;
+  if ((st = hip_status(launch_combine_if_shared(p, pl, &pl.srh, scores, nullptr, 0, s),
+                       "combine")))
+    return st;
   const int *hist = reinterpret_cast<const int *>(static_cast<char *>(ws) + pl.hist_off);
   ckv::SelectArgs sa = select_args(p, pl, hist);
   sa.l0 = layer_desc(nullptr, nullptr, nullptr, nullptr, scores, idx, nullptr, nullptr, budget);

@@ -100,6 +100,18 @@ __device__ __forceinline__ LayerView layer_view(const A &a, int layer, int g) {
   return v;
 }
 
+// SRHs of group g of the layer.
+template <bool ML, typename A>
+__device__ __forceinline__ int srh_count(const A &a, int layer, int g) {
+  if constexpr (ML) {
+    gptr<const LayerDesc> d = to_global(a.layers) + layer;
+    return d->srh_off[g + 1] - d->srh_off[g];
+  } else {
+    (void)layer;
+    return a.l0.srh_off[g + 1] - a.l0.srh_off[g];
+  }
+}
+
 // Arguments of the scoring kernels.
 struct ScoreArgs {
   LayerDesc l0;            // single-layer calls
@@ -139,6 +151,16 @@ struct SelectArgs {
   const LayerDesc *layers;
   const int *hist;         // per layer [batch][Hkv][kHistBins], or NULL (then counted here)
   int64_t hist_layer;
+  const int32_t *cu;
+  int32_t T, Hkv, W, batch;
+  int32_t n_sel;           // selections per (layer, sequence): Hkv, or 1 (layer-shared set)
+  int32_t out_groups;      // idx rows each selection writes: 1, or Hkv (layer-shared set)
+};
+
+// Layer-shared index set: the layer score from the per-group scores.
+struct CombineArgs {
+  LayerDesc l0;            // uses scores, srh_off
+  const LayerDesc *layers;
   const int32_t *cu;
   int32_t T, Hkv, W, batch;
 };

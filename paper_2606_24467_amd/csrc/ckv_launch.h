@@ -14,6 +14,8 @@ hipError_t launch_score_layers(const ScoreArgs &a, int dtype_bf16, int head_dim,
 // Selection and gather; n_layers > 0 reads the operands from the table
 // (a.layers), n_layers == 0 from a.l0.
 hipError_t launch_select(const SelectArgs &a, int n_layers, hipStream_t stream);
+// Layer-shared index set: layer score into every group's row of the scores.
+hipError_t launch_combine(const CombineArgs &a, int n_layers, int lmax, hipStream_t stream);
 // Writes table entries [first, first + count) from a.e (count <= kPutLayers).
 hipError_t launch_put_layers(const PutArgs &a, hipStream_t stream);
 

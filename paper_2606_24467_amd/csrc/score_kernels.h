@@ -178,7 +178,9 @@ __global__ __launch_bounds__(64 * kStatsWaves) void stats_kernel(const ScoreArgs
     for (int i = threadIdx.x; i < kHistBins; i += 64 * kStatsWaves) h[i] = 0;
   }
   w.c0 = chunk0 * a.chunk1;
-  if (w.c0 >= w.L) return;                   // uniform for the whole workgroup
+  // uniform for the whole workgroup (a group without an SRH is not scored:
+  // the layer-shared index set ignores it)
+  if (w.c0 >= w.L || w.lv.nsrh == 0) return;
   w.n_chunks = min(a.cpw1, (w.L - w.c0 + a.chunk1 - 1) / a.chunk1);
   w.P = w.L - a.W;
   w.rt_n = w.lv.nsrh * a.th;
@@ -292,7 +294,7 @@ __global__ __launch_bounds__(64 * kWaves) void colsum_kernel(const ScoreArgs a) 
   w.s0 = a.cu[w.b];
   w.L = a.cu[w.b + 1] - w.s0;
   w.c0 = (int)blockIdx.y * a.cpw2 * a.chunk2;
-  if (w.c0 >= w.L) return;
+  if (w.c0 >= w.L || w.lv.nsrh == 0) return;
   w.P = w.L - a.W;
   const int c_end = min(w.L, w.c0 + a.cpw2 * a.chunk2);
   // Window positions of this range are always kept: +inf.

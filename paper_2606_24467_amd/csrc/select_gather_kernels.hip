@@ -100,7 +100,7 @@ __device__ __forceinline__ void load_round(gptr<const uint32_t> sc, int P, int r
 // Grid (Hkv, batch [x layers]), 1024 threads.
 template <bool ML>
 __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a) {
-  const int g = blockIdx.x;
+  const int g = blockIdx.x;         // selection index: the KV group, or 0 (layer-shared set)
   const int layer = ML ? (int)blockIdx.y / a.batch : 0;
   const int b = (int)blockIdx.y - layer * a.batch;
   const LayerView lv = layer_view<ML>(a, layer, 0);
@@ -109,13 +109,17 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a)
   const int s0 = a.cu[b];
   const int L = a.cu[b + 1] - s0;
   const gptr<int32_t> out = lv.idx + ((int64_t)b * a.Hkv + g) * budget;
+  // position `pos` of the kept list, in every idx row this selection serves
+  auto put = [&](int pos, int32_t val) {
+    for (int r = 0; r < a.out_groups; ++r) out[(int64_t)r * budget + pos] = val;
+  };
   if (L <= budget) {
-    for (int j = tid; j < budget; j += kSelThreads) out[j] = (j < L) ? j : -1;
+    for (int j = tid; j < budget; j += kSelThreads) put(j, (j < L) ? j : -1);
     return;
   }
   const int P = L - a.W;
   const int k = budget - a.W;       // prefix tokens to keep, 0 <= k < P
-  for (int w = tid; w < a.W; w += kSelThreads) out[k + w] = P + w;
+  for (int w = tid; w < a.W; w += kSelThreads) put(k + w, P + w);
   if (k == 0) return;
   const gptr<const uint32_t> sc =
       reinterpret_cast<gptr<const uint32_t>>(lv.scores + (int64_t)g * a.T + s0);
@@ -234,7 +238,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a)
         keep = true;
         --eq_left;
       }
-      if (keep && pos < k) out[pos++] = j0 + e;   // bound holds for finite scores; guards NaN
+      if (keep && pos < k) put(pos++, j0 + e);   // bound holds for finite scores; guards NaN
     }
     eq_base += eq_total;
     pos_base += sel_total;
@@ -314,11 +318,49 @@ hipError_t launch_put_layers(const PutArgs &a, hipStream_t stream) {
 
 hipError_t launch_select(const SelectArgs &a, int n_layers, hipStream_t stream) {
   if (n_layers > 0)
-    hipLaunchKernelGGL(select_kernel<true>, dim3(a.Hkv, a.batch * n_layers), dim3(kSelThreads),
+    hipLaunchKernelGGL(select_kernel<true>, dim3(a.n_sel, a.batch * n_layers), dim3(kSelThreads),
                        0, stream, a);
   else
-    hipLaunchKernelGGL(select_kernel<false>, dim3(a.Hkv, a.batch), dim3(kSelThreads), 0, stream,
+    hipLaunchKernelGGL(select_kernel<false>, dim3(a.n_sel, a.batch), dim3(kSelThreads), 0, stream,
                        a);
+  return hipGetLastError();
+}
+
+// Layer-shared index set (section 3.3): the layer score of a prefix position
+// is the mean over all the layer's SRHs of their pooled window sums, i.e. the
+// per-group scores weighted by each group's SRH count; it replaces every
+// group's row (window positions stay +inf).  Grid (ceil(max L / 256), batch
+// [x layers]), 256 threads, one position per thread.
+template <bool ML>
+__global__ __launch_bounds__(256) void combine_kernel(const CombineArgs a) {
+  const int layer = ML ? (int)blockIdx.y / a.batch : 0;
+  const int b = (int)blockIdx.y - layer * a.batch;
+  const LayerView lv = layer_view<ML>(a, layer, 0);
+  const int s0 = a.cu[b];
+  const int L = a.cu[b + 1] - s0;
+  const int t = (int)blockIdx.x * 256 + (int)threadIdx.x;
+  if (t >= L) return;
+  const gptr<float> sc = lv.scores + s0 + t;
+  float v = INFINITY;
+  if (t < L - a.W) {
+    float acc = 0.f;
+    int n_total = 0;
+    for (int g = 0; g < a.Hkv; ++g) {
+      const int n = srh_count<ML>(a, layer, g);
+      if (n) acc += (float)n * sc[(int64_t)g * a.T];
+      n_total += n;
+    }
+    v = acc / (float)n_total;
+  }
+  for (int g = 0; g < a.Hkv; ++g) sc[(int64_t)g * a.T] = v;
+}
+
+hipError_t launch_combine(const CombineArgs &a, int n_layers, int lmax, hipStream_t stream) {
+  const dim3 grid((lmax + 255) / 256, a.batch * (n_layers > 0 ? n_layers : 1));
+  if (n_layers > 0)
+    hipLaunchKernelGGL(combine_kernel<true>, grid, dim3(256), 0, stream, a);
+  else
+    hipLaunchKernelGGL(combine_kernel<false>, grid, dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 

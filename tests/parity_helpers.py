@@ -35,7 +35,8 @@ def device_tensors(x: wl.LayerInputs, dev):
 
 
 def run_oracle(x: wl.LayerInputs, budget=None, pool_kernel=None, pool_type=None,
-               reduce_order=O.POOL_THEN_MEAN, scale=None) -> O.LayerResult:
+               reduce_order=O.POOL_THEN_MEAN, scale=None,
+               index_mode=O.PER_GROUP) -> O.LayerResult:
     w = x.workload
     kb = x.bits("k") if x.dtype == wl.BF16 else x.k.view(np.uint32)
     vb = x.bits("v") if x.dtype == wl.BF16 else x.v.view(np.uint32)
@@ -43,7 +44,7 @@ def run_oracle(x: wl.LayerInputs, budget=None, pool_kernel=None, pool_type=None,
                             x.budget if budget is None else budget,
                             w.pool_kernel if pool_kernel is None else pool_kernel,
                             w.pool_type if pool_type is None else pool_type,
-                            reduce_order, scale=scale, k_values=x.k)
+                            reduce_order, scale=scale, k_values=x.k, index_mode=index_mode)
 
 
 def raw_bits(t: torch.Tensor) -> np.ndarray:

@@ -105,6 +105,10 @@ INVALID = [
     ("stride", dict(k_stride_tok=100), C.UNSUPPORTED),
     ("stride zero", dict(v_stride_head=0), C.INVALID_ARGUMENT),
     ("too many kv heads", dict(n_kv_heads=256, n_q_heads=256), C.UNSUPPORTED),
+    ("index mode", dict(index_mode=2), C.INVALID_ARGUMENT),
+    ("reserved", dict(reserved=1), C.INVALID_ARGUMENT),
+    ("layer set, mean then pool", dict(index_mode=C.INDEX_LAYER, reduce_order=C.MEAN_THEN_POOL),
+     C.UNSUPPORTED),
 ]
 
 
@@ -140,6 +144,25 @@ def test_mask_rules(L):
     c = Case(W=64, Hq=32, Hkv=4)
     c.mask[:] = 1                      # 8 SRHs x 4 row tiles = 32 > 12
     assert c.score(L) == C.UNSUPPORTED
+
+
+def test_mask_rules_of_the_layer_shared_set(L):
+    c = _mutate(Case(), index_mode=C.INDEX_LAYER)
+    c.mask[:] = 0
+    c.mask[0] = 1                      # group 1 has no SRH: allowed for a layer-wide set
+    assert c.ws_bytes(L) > 0
+    assert L.compresskv_last_error().decode() == ""
+    c.mask[:] = 0                      # but the layer needs one
+    assert c.score(L) == C.INVALID_ARGUMENT
+    assert "no Semantic Retrieval Head" in L.compresskv_last_error().decode()
+    assert c.ws_bytes(L) == 0
+    m = _mutate(LayersCase(n_layers=3), index_mode=C.INDEX_LAYER)
+    m.masks[1, :] = 0
+    m.masks[1, 0] = 1
+    assert m.ws_bytes(L) > 0
+    m.masks[2, :] = 0
+    assert m.compress_layers(L) == C.INVALID_ARGUMENT
+    assert "layer 2" in L.compresskv_last_error().decode()
 
 
 def test_budget_pointer_and_workspace_rules(L):
