@@ -55,12 +55,14 @@ struct Plan {
   uint32_t head_end_mask = 0;
   // single-layer workspace: scores | stats | counters | histograms
   // multi-layer workspace:  table | scores | stats | histograms (all per layer)
-  size_t table_off = 0, scores_off = 0, stats_off = 0, counters_off = 0, hist_off = 0, total = 0;
+  size_t table_off = 0, scores_off = 0, stats_off = 0, counters_off = 0, bias_off = 0,
+         hist_off = 0, total = 0;
   int64_t stats_layer = 0, hist_layer = 0;   // elements per layer
   bool fused = false;      // single-pass scoring kernel
-  int unit_tiles = 4;      // its key tiles per wave per unit
   int n_units_max = 0;     // its units per (sequence, group), largest
-  int n_counters = 0;      // ints zeroed before it (ticket, fallbacks, arrivals, histograms)
+  int fused_grid = 0;      // its persistent workgroups
+  int n_counters = 0;      // ints zeroed before it (ticket, fallbacks, arrivals,
+                           // published normalisers, histograms)
   int max_parts = 0;       // partial-statistics slots per group in the workspace
   LayerSrh srh;            // single-layer calls
 };
@@ -191,8 +193,8 @@ int check_mask(const ckv_problem *p, const uint8_t *mask, Plan &pl) {
   return set_row_tiles(p, pl.srh.nmax, pl);
 }
 
-// Keys per fused unit: 16 keys x 4 waves x unit_tiles.
-int fused_units(int L, int unit_tiles) { return (L + 64 * unit_tiles - 1) / (64 * unit_tiles); }
+// Units of the single-pass kernel in a sequence of L keys.
+int fused_units(int L) { return (L + ckv::fused_unit_keys() - 1) / ckv::fused_unit_keys(); }
 
 // The two-kernel path is the default.  CKV_PATH=single selects the
 // single-pass kernel where it applies: every group's units must fit in half of
@@ -204,20 +206,16 @@ void choose_path(const ckv_problem *p, Plan &pl) {
   const char *path = std::getenv("CKV_PATH");
   if (!path || std::string(path) != "single") return;
   if (p->index_mode == CKV_INDEX_LAYER) return;   // its groups may have no SRH
-  if (p->batch > ckv::kFusedMaxBatch) return;
-  for (int ut : {4, 2}) {
-    const int resident = ckv::fused_resident_workgroups(p->dtype == CKV_BF16, p->head_dim,
-                                                        pl.rt_max, ut);
-    if (resident <= 0) continue;
-    int nmax = 0;
-    for (int b = 0; b < p->batch; ++b)
-      nmax = std::max(nmax, fused_units(p->cu_seqlens_host[b + 1] - p->cu_seqlens_host[b], ut));
-    if (2 * nmax <= resident) {
-      pl.fused = true;
-      pl.unit_tiles = ut;
-      pl.n_units_max = nmax;
-      return;
-    }
+  if (p->batch > ckv::kFusedMaxBatch || p->dtype != CKV_BF16) return;
+  const int resident = ckv::fused_resident_workgroups(1, p->head_dim, pl.rt_max);
+  if (resident <= 0) return;
+  int nmax = 0;
+  for (int b = 0; b < p->batch; ++b)
+    nmax = std::max(nmax, fused_units(p->cu_seqlens_host[b + 1] - p->cu_seqlens_host[b]));
+  if (2 * nmax <= resident) {
+    pl.fused = true;
+    pl.n_units_max = nmax;
+    pl.fused_grid = resident;
   }
 }
 
@@ -238,32 +236,49 @@ void set_chunks(const ckv_problem *p, Plan &pl) {
   pl.max_chunks2 = std::max(1, (pl.lmax + c2 - 1) / c2);
 }
 
+// The block the single-pass kernel zeroes before it runs, from `start`:
+// [0] ticket, [1] fallbacks, [64 ..) arrivals per (layer, group), then the
+// published (normaliser, marker) pairs per (layer, group, row slot), then the
+// first-digit histograms per (layer, group) (also used by the two-pass path).
+void set_counters(const ckv_problem *p, Plan &pl, size_t start, int n_layers) {
+  const size_t lg = (size_t)p->batch * p->n_kv_heads * n_layers;
+  pl.counters_off = start;
+  pl.bias_off = start + round_up((64 + lg) * sizeof(int), 256);
+  pl.hist_off = pl.bias_off + round_up(lg * pl.rt_max * 16 * sizeof(float2), 256);
+  pl.n_counters = (int)((pl.hist_off - pl.counters_off) / sizeof(int) + lg * ckv::kHistBins);
+  pl.total = pl.hist_off + round_up(lg * ckv::kHistBins * sizeof(int), 256);
+}
+
+// Partial-statistics slots per group: enough for either path's chunking.
+int partial_slots(const Plan &pl) {
+  int parts = pl.max_chunks1;
+  parts = std::max(parts, fused_units(pl.lmax));
+  return parts;
+}
+
+// Single-layer workspace: a one-entry layer table (for the single-pass
+// kernel), scores, partial row statistics, then the counters block.
 void make_plan(const ckv_problem *p, Plan &pl, bool decide_path) {
   set_chunks(p, pl);
   pl.n_layers = 1;
   if (decide_path) choose_path(p, pl);
-  // partial row statistics: enough slots for either path's chunking, plus one
-  // per group for the published normalisers of the single-pass kernel
-  int parts = pl.max_chunks1;
-  for (int ut : {2, 4}) parts = std::max(parts, fused_units(pl.lmax, ut) + 1);
+  pl.max_parts = partial_slots(pl);
   const size_t groups = (size_t)p->batch * p->n_kv_heads;
-  pl.scores_off = 0;
-  pl.stats_off = round_up((size_t)p->n_kv_heads * pl.T * sizeof(float), 256);
-  pl.counters_off = pl.stats_off +
-                    round_up(groups * parts * (size_t)pl.rt_max * 16 * sizeof(float2), 256);
-  // counters block: [0] ticket, [1] fallbacks, [64 ..) arrivals, ready flags,
-  // then the histograms
-  pl.hist_off = pl.counters_off + round_up((64 + 2 * groups) * sizeof(int), 256);
-  pl.n_counters = (int)((pl.hist_off - pl.counters_off) / sizeof(int) + groups * ckv::kHistBins);
-  pl.total = pl.hist_off + round_up(groups * ckv::kHistBins * sizeof(int), 256);
-  pl.max_parts = parts;
+  pl.table_off = 0;
+  pl.scores_off = round_up(sizeof(ckv::LayerDesc), 256);
+  pl.stats_off =
+      pl.scores_off + round_up((size_t)p->n_kv_heads * pl.T * sizeof(float), 256);
+  set_counters(p, pl,
+               pl.stats_off +
+                   round_up(groups * pl.max_parts * (size_t)pl.rt_max * 16 * sizeof(float2), 256),
+               1);
   pl.stats_layer = 0;
   pl.hist_layer = 0;
 }
 
-// Multi-layer workspace: the layer table, then per layer the scores, the
-// partial row statistics and the first-digit histograms.
-void make_plan_layers(const ckv_problem *p, int n_layers, Plan &pl) {
+// Multi-layer workspace: the layer table, then per layer the scores and the
+// partial row statistics, then the counters block (per layer inside).
+void make_plan_layers(const ckv_problem *p, int n_layers, Plan &pl, bool decide_path) {
   set_chunks(p, pl);
   pl.n_layers = n_layers;
   // Longer workgroups once there are enough of them: a few rounds of the
@@ -277,7 +292,8 @@ void make_plan_layers(const ckv_problem *p, int n_layers, Plan &pl) {
   if (e1 > 0) pl.cpw1 = std::min(e1, 64);
   if (e2 > 0) pl.cpw2 = std::min(e2, 64);
   pl.fused = false;
-  pl.max_parts = pl.max_chunks1;
+  if (decide_path) choose_path(p, pl);
+  pl.max_parts = partial_slots(pl);
   const size_t groups = (size_t)p->batch * p->n_kv_heads;
   pl.stats_layer = (int64_t)(groups * pl.max_parts * (size_t)pl.rt_max * 16);
   pl.hist_layer = (int64_t)(groups * ckv::kHistBins);
@@ -285,8 +301,9 @@ void make_plan_layers(const ckv_problem *p, int n_layers, Plan &pl) {
   pl.scores_off = round_up((size_t)n_layers * sizeof(ckv::LayerDesc), 256);
   pl.stats_off = pl.scores_off +
                  round_up((size_t)n_layers * p->n_kv_heads * pl.T * sizeof(float), 256);
-  pl.hist_off = pl.stats_off + round_up((size_t)n_layers * pl.stats_layer * sizeof(float2), 256);
-  pl.total = pl.hist_off + round_up((size_t)n_layers * pl.hist_layer * sizeof(int), 256);
+  set_counters(p, pl,
+               pl.stats_off + round_up((size_t)n_layers * pl.stats_layer * sizeof(float2), 256),
+               n_layers);
 }
 
 // Fields of the scoring arguments shared by every layer.
@@ -418,33 +435,6 @@ ckv::GatherArgs gather_args(const ckv_problem *p) {
   return g;
 }
 
-// S1-S4 of a single-layer call on the path the plan chose.
-hipError_t launch_scoring(const ckv_problem *p, const Plan &pl, const void *q, const void *k,
-                          float *scores, void *ws, hipStream_t stream) {
-  ckv::ScoreArgs a = score_args(p, pl, ws);
-  a.l0 = layer_desc(&pl.srh, q, k, nullptr, scores, nullptr, nullptr, nullptr, 0);
-  if (!pl.fused)
-    return ckv::launch_score(a, p->dtype == CKV_BF16, p->head_dim, pl.rt_max, p->batch, stream);
-  ckv::FusedArgs f{};
-  f.s = a;
-  int *ctr = reinterpret_cast<int *>(static_cast<char *>(ws) + pl.counters_off);
-  f.ticket = ctr;
-  f.fallbacks = ctr + 1;
-  f.arrive = ctr + 64;
-  f.ready = ctr + 64 + p->batch * p->n_kv_heads;
-  f.bias_slot = pl.max_parts - 1;
-  int acc = 0;
-  for (int b = 0; b <= p->batch; ++b) {
-    f.seq_units[b] = acc;
-    if (b < p->batch)
-      acc += p->n_kv_heads *
-             fused_units(p->cu_seqlens_host[b + 1] - p->cu_seqlens_host[b], pl.unit_tiles);
-  }
-  f.n_units_total = acc;
-  return ckv::launch_fused_score(f, p->dtype == CKV_BF16, p->head_dim, pl.rt_max, pl.unit_tiles,
-                                 pl.n_counters, stream);
-}
-
 // Host-side arrays of a multi-layer call (entries may be NULL where the call
 // does not use them).
 struct LayerPtrs {
@@ -535,6 +525,57 @@ hipError_t put_layers(const ckv_problem *p, const Plan &pl, int n_layers, const 
   return hipSuccess;
 }
 
+// The single-pass kernel over n_layers layers of the table a.layers.
+hipError_t launch_fused(const ckv_problem *p, const Plan &pl, const ckv::ScoreArgs &a, void *ws,
+                        int n_layers, hipStream_t stream) {
+  ckv::FusedArgs f{};
+  f.s = a;
+  int *ctr = reinterpret_cast<int *>(static_cast<char *>(ws) + pl.counters_off);
+  f.ticket = ctr;
+  f.fallbacks = ctr + 1;
+  f.arrive = ctr + 64;
+  f.bias = reinterpret_cast<float2 *>(static_cast<char *>(ws) + pl.bias_off);
+  int acc = 0;
+  for (int b = 0; b <= p->batch; ++b) {
+    f.seq_units[b] = acc;
+    if (b < p->batch)
+      acc += p->n_kv_heads * fused_units(p->cu_seqlens_host[b + 1] - p->cu_seqlens_host[b]);
+  }
+  f.units_per_layer = acc;
+  f.n_units_total = acc * n_layers;
+  const int grid = std::min(pl.fused_grid, f.n_units_total);
+  return ckv::launch_fused_score(f, p->dtype == CKV_BF16, p->head_dim, pl.rt_max, pl.n_counters,
+                                 grid, stream);
+}
+
+// S1-S4 of a single-layer call on the path the plan chose.
+hipError_t launch_scoring(const ckv_problem *p, const Plan &pl, const void *q, const void *k,
+                          float *scores, void *ws, hipStream_t stream) {
+  ckv::ScoreArgs a = score_args(p, pl, ws);
+  a.l0 = layer_desc(&pl.srh, q, k, nullptr, scores, nullptr, nullptr, nullptr, 0);
+  if (!pl.fused)
+    return ckv::launch_score(a, p->dtype == CKV_BF16, p->head_dim, pl.rt_max, p->batch, stream);
+  // the single-pass kernel reads its operands from a layer table
+  LayerPtrs lp;
+  lp.q = &q;
+  lp.k = &k;
+  std::vector<uint32_t> bits(ckv::kMaxQHeads / 32, 0u);
+  for (uint8_t h : pl.srh.head) bits[h / 32] |= 1u << (h % 32);
+  hipError_t e = put_layers(p, pl, 1, lp, bits, scores, ws, stream);
+  if (e != hipSuccess) return e;
+  a.layers = reinterpret_cast<const ckv::LayerDesc *>(static_cast<char *>(ws) + pl.table_off);
+  return launch_fused(p, pl, a, ws, 1, stream);
+}
+
+// S1-S4 of a multi-layer call on the path the plan chose.
+hipError_t launch_scoring_layers(const ckv_problem *p, const Plan &pl, const ckv::ScoreArgs &a,
+                                 void *ws, int n_layers, hipStream_t stream) {
+  if (!pl.fused)
+    return ckv::launch_score_layers(a, p->dtype == CKV_BF16, p->head_dim, pl.rt_max, p->batch,
+                                    n_layers, stream);
+  return launch_fused(p, pl, a, ws, n_layers, stream);
+}
+
 // S1-S4 (and, with budgets, S5-S6) of a multi-layer call.
 int run_layers(const ckv_problem *p, int n_layers, const LayerPtrs &lp, const uint8_t *masks,
                float *scores_or_null, void *ws, size_t ws_bytes, void *stream, bool full) {
@@ -545,8 +586,9 @@ int run_layers(const ckv_problem *p, int n_layers, const LayerPtrs &lp, const ui
   if ((st = check_layers(p, n_layers, masks, lp, pl, &bits))) return st;
   if (!full && (st = check_ptr(scores_or_null, "scores", 4))) return st;
   if (scores_or_null && (st = check_ptr(scores_or_null, "scores", 4))) return st;
-  make_plan_layers(p, n_layers, pl);
+  make_plan_layers(p, n_layers, pl, false);
   if ((st = check_ws(pl, ws, ws_bytes))) return st;
+  make_plan_layers(p, n_layers, pl, true);
   float *scores = scores_or_null
                       ? scores_or_null
                       : reinterpret_cast<float *>(static_cast<char *>(ws) + pl.scores_off);
@@ -557,10 +599,7 @@ int run_layers(const ckv_problem *p, int n_layers, const LayerPtrs &lp, const ui
       reinterpret_cast<const ckv::LayerDesc *>(static_cast<char *>(ws) + pl.table_off);
   ckv::ScoreArgs a = score_args(p, pl, ws);
   a.layers = table;
-  if ((st = hip_status(ckv::launch_score_layers(a, p->dtype == CKV_BF16, p->head_dim, pl.rt_max,
-                                                p->batch, n_layers, s),
-                       "score")))
-    return st;
+  if ((st = hip_status(launch_scoring_layers(p, pl, a, ws, n_layers, s), "score"))) return st;
   if ((st = hip_status(launch_combine_if_shared(p, pl, nullptr, nullptr, table, n_layers, s),
                        "combine")))
     return st;
@@ -709,7 +748,7 @@ size_t compresskv_layers_workspace_bytes(const ckv_problem *p, int32_t n_layers,
   Plan pl;
   if (check_problem(p) || check_layers(p, n_layers, srh_masks_host, LayerPtrs{}, pl, nullptr))
     return 0;
-  make_plan_layers(p, n_layers, pl);
+  make_plan_layers(p, n_layers, pl, false);
   ok();
   return pl.total;
 }

@@ -54,6 +54,15 @@ __device__ __forceinline__ gptr<T> to_global(T *p) {
   return (gptr<T>)p;
 }
 
+// Read-only during a kernel (the layer table, the sequence offsets): uniform
+// loads through the constant address space become scalar loads.
+template <typename T>
+using cptr = const __attribute__((address_space(4))) T *;
+template <typename T>
+__device__ __forceinline__ cptr<T> to_const(const T *p) {
+  return (cptr<T>)p;
+}
+
 // What a workgroup uses of its layer, as global pointers; off / nsrh describe
 // the SRHs of group g (srh_head[off .. off + nsrh)).
 struct LayerView {
@@ -70,7 +79,7 @@ template <bool ML, typename A>
 __device__ __forceinline__ LayerView layer_view(const A &a, int layer, int g) {
   LayerView v;
   if constexpr (ML) {
-    gptr<const LayerDesc> d = to_global(a.layers) + layer;
+    cptr<LayerDesc> d = to_const(a.layers) + layer;
     v.q = to_global(static_cast<const char *>(d->q));
     v.k = to_global(static_cast<const char *>(d->k));
     v.v = to_global(static_cast<const char *>(d->v));
@@ -78,7 +87,7 @@ __device__ __forceinline__ LayerView layer_view(const A &a, int layer, int g) {
     v.idx = to_global(d->idx);
     v.k_out = to_global(static_cast<char *>(d->k_out));
     v.v_out = to_global(static_cast<char *>(d->v_out));
-    v.srh_head = &d->srh_head[0];
+    v.srh_head = &(to_global(a.layers) + layer)->srh_head[0];
     v.budget = d->budget;
     v.off = d->srh_off[g];
     v.nsrh = d->srh_off[g + 1] - v.off;
@@ -136,14 +145,14 @@ struct ScoreArgs {
 
 // Arguments of the single-pass scoring kernel (single-layer calls).
 struct FusedArgs {
-  ScoreArgs s;             // s.stats holds the published partials: [group][unit][row]
+  ScoreArgs s;             // s.stats holds the published partials: [layer][group][unit][row]
   int *ticket;             // one counter
   int *fallbacks;          // waits that hit their bound (diagnostic)
-  int *arrive;             // [batch * Hkv] units of each group that have published
-  int *ready;              // [batch * Hkv] the group's normalisers are published
-  int bias_slot;           // partial slot (per group) that holds the published normalisers
-  int n_units_total;
-  int seq_units[65];       // first ticket of sequence b (group-major numbering), b <= batch
+  int *arrive;             // [layers][batch * Hkv] units of each group that have published
+  float2 *bias;            // [layers][batch * Hkv][row_slots] (normaliser, marker) pairs
+  int n_units_total;       // units of all layers
+  int units_per_layer;     // seq_units[batch]
+  int seq_units[65];       // first ticket of sequence b within a layer (group-major), b <= batch
 };
 
 struct SelectArgs {

@@ -24,10 +24,11 @@ constexpr int kWaves = 4;       // waves per column-sum workgroup (two per CU: o
 constexpr int kRing = 4;        // key tiles per wave in the load ring: kRing - 1 in flight
                                 // while one is consumed
 
-// Row tiles kept in registers: all of them when they fit in 64 VGPRs, else none.
-template <typename T, int D, int RTM>
+// Row tiles kept in registers: all of them when they fit in 64 VGPRs (and QR
+// allows it), else none.
+template <typename T, int D, int RTM, bool QR = true>
 struct RegTiles {
-  static constexpr int v = RTM * Slices<T, D>::n <= 16 ? RTM : 0;
+  static constexpr int v = QR && RTM * Slices<T, D>::n <= 16 ? RTM : 0;
   static constexpr int n = v > 0 ? v : 1;   // array extent
 };
 
@@ -96,12 +97,12 @@ __device__ __forceinline__ void load_k_row(const ScoreArgs &a, gptr<const char> 
 
 // logits of row tile rt against one key tile; KEYS_AS_A selects the operand
 // order (true: lane holds 4 keys of one row; false: 4 rows of one key).
-template <typename T, int D, int RTM, bool KEYS_AS_A>
+template <typename T, int D, int RTM, bool KEYS_AS_A, bool QR = true>
 __device__ __forceinline__ f32x4 tile_logits(const uint4 (&kf)[Slices<T, D>::n],
-                                             const uint4 (&qreg)[RegTiles<T, D, RTM>::n]
+                                             const uint4 (&qreg)[RegTiles<T, D, RTM, QR>::n]
                                                                 [Slices<T, D>::n],
                                              const uint4 *q_lds, int rt, int c, int quad) {
-  constexpr int NS = Slices<T, D>::n, RQ = RegTiles<T, D, RTM>::v;
+  constexpr int NS = Slices<T, D>::n, RQ = RegTiles<T, D, RTM, QR>::v;
   f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int s = 0; s < NS; ++s) {
@@ -116,12 +117,54 @@ __device__ __forceinline__ f32x4 tile_logits(const uint4 (&kf)[Slices<T, D>::n],
   return acc;
 }
 
+// Logits of every row tile against one key tile, slice-major: the RT
+// accumulation chains are independent, so the matrix pipeline interleaves
+// them instead of waiting on one chain at a time.  Each tile accumulates its
+// slices in the same order as tile_logits.
+template <typename T, int D, int RT, bool KEYS_AS_A, bool QR = true>
+__device__ __forceinline__ void tile_logits_all(const uint4 (&kf)[Slices<T, D>::n],
+                                                const uint4 (&qreg)[RegTiles<T, D, RT, QR>::n]
+                                                                   [Slices<T, D>::n],
+                                                const uint4 *q_lds, int c, int quad,
+                                                f32x4 (&acc)[RT]) {
+  constexpr int NS = Slices<T, D>::n, RQ = RegTiles<T, D, RT, QR>::v;
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      uint4 qv;
+      if (rt < RQ) {
+        qv = qreg[rt < RQ ? rt : 0][s];
+      } else {
+        qv = q_frag<T, D>(q_lds, rt, s, c, quad);
+      }
+      acc[rt] = KEYS_AS_A ? mfma_slice<T>(kf[s], qv, acc[rt]) : mfma_slice<T>(qv, kf[s], acc[rt]);
+    }
+  }
+}
+
 // Row-tile counts the scoring loops are compiled for: a group with rt_n row
 // tiles runs the smallest of them that is >= rt_n; the extra tiles hold zero
 // queries (their rows are never read back), so every loop over row tiles has
 // a compile-time bound and no branch.
 __host__ __device__ constexpr int rt_class(int rt_n) {
   return rt_n <= 4 ? rt_n : rt_n <= 6 ? 6 : rt_n <= 8 ? 8 : 12;
+}
+
+// Calls body.template operator()<RT>() with RT = rt_class(rt_n) (<= RTM).
+template <int RTM, typename F>
+__device__ __forceinline__ void dispatch_rt(int rt_n, F &&body) {
+  switch (rt_class(rt_n)) {
+    case 1: if constexpr (RTM >= 1) body.template operator()<1>(); break;
+    case 2: if constexpr (RTM >= 2) body.template operator()<2>(); break;
+    case 3: if constexpr (RTM >= 3) body.template operator()<3>(); break;
+    case 4: if constexpr (RTM >= 4) body.template operator()<4>(); break;
+    case 6: if constexpr (RTM >= 6) body.template operator()<6>(); break;
+    case 8: if constexpr (RTM >= 8) body.template operator()<8>(); break;
+    default: if constexpr (RTM >= 12) body.template operator()<12>(); break;
+  }
 }
 
 // Sum of v over the four quads (lanes c, c + 16, c + 32, c + 48) in every lane,
@@ -155,9 +198,10 @@ __device__ __forceinline__ void stats_update(const ScoreArgs &a, const f32x4 (&a
     bool over = false;
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
-      float t = 0.f;
+      // (e0 + e1) + e2 + e3: the terms are never -0, so this is 0 + e0 + ...
+      float t = fast_exp2(__builtin_fmaf(acc[rt][0], a.c1, -ref[rt]));
 #pragma unroll
-      for (int r = 0; r < 4; ++r) t += fast_exp2(__builtin_fmaf(acc[rt][r], a.c1, -ref[rt]));
+      for (int r = 1; r < 4; ++r) t += fast_exp2(__builtin_fmaf(acc[rt][r], a.c1, -ref[rt]));
       s_new[rt] = sum[rt] + t;
       over |= !(s_new[rt] <= 0x1p64f);   // also true for inf and nan
     }
@@ -226,7 +270,7 @@ __device__ __forceinline__ float2 load_partial_coherent(const float2 *p) {
 // (fixed order per thread, then a shuffle tree over tpr threads per row).
 // Padding rows (window index >= W) and rows >= rows get +inf.  COHERENT reads
 // the partials at agent scope (they were written by this kernel).
-template <int NT, bool COHERENT = false>
+template <int NT, bool COHERENT = false, int kBatch = 8>
 __device__ __forceinline__ void merge_row_bias(const ScoreArgs &a, const float2 *parts,
                                                int64_t stride, int n_parts, int rows,
                                                int rows_cap, float *bias_s) {
@@ -236,8 +280,7 @@ __device__ __forceinline__ void merge_row_bias(const ScoreArgs &a, const float2 
   const int row = tid / tpr, sub = tid % tpr;
   float m = -INFINITY, sm = 0.f;
   if (row < rows) {
-    // batches of 8 loads in flight, merged in index order
-    constexpr int kBatch = 8;
+    // batches of kBatch loads in flight, merged in index order
     for (int k0 = sub; k0 < n_parts; k0 += kBatch * tpr) {
       float2 v[kBatch];
 #pragma unroll
@@ -267,22 +310,24 @@ __device__ __forceinline__ void merge_row_bias(const ScoreArgs &a, const float2 
 // key c): in-lane over the 4 rows and the SRH's row tiles, then across the
 // quads.  cs[h][16 + 16*e + c] receives SRH h's sum for key c of tile e.  Row
 // tiles past the group's own (zero queries) have bias +inf and add nothing.
-template <typename T, int D, int RT, int CSW>
+template <typename T, int D, int RT, int CSW, bool QR = true>
 __device__ __forceinline__ void tile_window_sums(const ScoreArgs &a,
                                                  const uint4 (&kf)[Slices<T, D>::n],
-                                                 const uint4 (&qreg)[RegTiles<T, D, RT>::n]
+                                                 const uint4 (&qreg)[RegTiles<T, D, RT, QR>::n]
                                                                     [Slices<T, D>::n],
                                                  const uint4 *q_lds, const float (&bias)[RT][4],
                                                  int e, bool keep, int c, int quad,
                                                  float (*cs)[CSW]) {
-  // per row tile: the lane's 4 rows (no branch between the row tiles)
+  // per row tile: the lane's 4 rows (no branch between the row tiles); the
+  // terms are never -0, so starting from the first term equals starting from 0
+  f32x4 acc[RT];
+  tile_logits_all<T, D, RT, false, QR>(kf, qreg, q_lds, c, quad, acc);
   float vt[RT];
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
-    const f32x4 acc = tile_logits<T, D, RT, false>(kf, qreg, q_lds, rt, c, quad);
-    vt[rt] = 0.f;
+    vt[rt] = fast_exp2(__builtin_fmaf(acc[rt][0], a.c1, -bias[rt][0]));
 #pragma unroll
-    for (int r = 0; r < 4; ++r) vt[rt] += fast_exp2(__builtin_fmaf(acc[r], a.c1, -bias[rt][r]));
+    for (int r = 1; r < 4; ++r) vt[rt] += fast_exp2(__builtin_fmaf(acc[rt][r], a.c1, -bias[rt][r]));
   }
   // per SRH: its row tiles, then the quads
   int hh = 0;

@@ -43,20 +43,6 @@ struct Work {
   int layer, b, g, s0, L, P, c0, n_chunks, rt_n;
 };
 
-// Calls body.template operator()<RT>() with RT = rt_class(rt_n) (<= RTM).
-template <int RTM, typename F>
-__device__ __forceinline__ void dispatch_rt(int rt_n, F &&body) {
-  switch (rt_class(rt_n)) {
-    case 1: if constexpr (RTM >= 1) body.template operator()<1>(); break;
-    case 2: if constexpr (RTM >= 2) body.template operator()<2>(); break;
-    case 3: if constexpr (RTM >= 3) body.template operator()<3>(); break;
-    case 4: if constexpr (RTM >= 4) body.template operator()<4>(); break;
-    case 6: if constexpr (RTM >= 6) body.template operator()<6>(); break;
-    case 8: if constexpr (RTM >= 8) body.template operator()<8>(); break;
-    default: if constexpr (RTM >= 12) body.template operator()<12>(); break;
-  }
-}
-
 // ---------------------------------------------------------------------------
 // S1+S2 partial statistics.  Grid (Hkv, ceil(max_chunks1 / cpw1), batch
 // [x layers]), 64 * kStatsWaves threads; a workgroup covers cpw1 consecutive
@@ -115,9 +101,7 @@ __device__ __forceinline__ void stats_body(const ScoreArgs &a, const Work &w, ui
   }
   auto consume = [&](const uint4 (&kf)[NS], int i) {
     f32x4 acc[RT];
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt)
-      acc[rt] = tile_logits<T, D, RT, true>(kf, qreg, q_lds, rt, c, quad);
+    tile_logits_all<T, D, RT, true>(kf, qreg, q_lds, c, quad, acc);
     stats_update<RT>(a, acc, ref, sum, ready, c0 + 16 * (wave + NW * i), L, P, c, quad);
   };
   // The chunk's partial: merge the four quads (same row c, different keys),

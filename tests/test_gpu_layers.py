@@ -14,6 +14,18 @@ from tests import parity_helpers as H
 pytestmark = pytest.mark.gpu
 
 
+@pytest.fixture(autouse=True, params=["two", "single"])
+def scoring_path(request, monkeypatch):
+    """Every case runs on the two-pass path (the default) and on the
+    single-pass kernel (where it applies); the per-layer calls it is compared
+    with take the same path."""
+    if request.param == "single":
+        monkeypatch.setenv("CKV_PATH", "single")
+    else:
+        monkeypatch.delenv("CKV_PATH", raising=False)
+    return request.param
+
+
 def _say(*a):
     print(*a, file=sys.stderr, flush=True)
 
@@ -59,8 +71,7 @@ def _per_layer(p, q, k, v, masks, budgets):
     return out
 
 
-def test_compress_layers_matches_oracle_ragged(gpu, monkeypatch):
-    monkeypatch.delenv("CKV_PATH", raising=False)
+def test_compress_layers_matches_oracle_ragged(gpu):
     w = wl.get("ragged8", batch=3, n_layers=5, ragged=(700, 2600), srh_per_group=(1, 3),
                n_needle=4)
     budgets = [64, 300, 2600, 32, 1111]     # 2600 >= every length (all kept); 32 = W
@@ -84,8 +95,7 @@ def test_compress_layers_matches_oracle_ragged(gpu, monkeypatch):
         _say(f"  layer {l} ok, boundary swaps {swaps}")
 
 
-def test_compress_layers_qwen_shape_reduced(gpu, monkeypatch):
-    monkeypatch.delenv("CKV_PATH", raising=False)
+def test_compress_layers_qwen_shape_reduced(gpu):
     w = wl.get("qwen128k", seq_len=12000 + 5, n_layers=3, n_needle=8)
     budgets = [200, 64, 1777]
     xs = [wl.make_layer(w, l, seed=22, budget=B) for l, B in enumerate(budgets)]
@@ -102,11 +112,10 @@ def test_compress_layers_qwen_shape_reduced(gpu, monkeypatch):
         _check_needles(x, budgets[l], idxs[l].cpu().numpy())
 
 
-def test_full_32_layer_stack(gpu, monkeypatch):
+def test_full_32_layer_stack(gpu):
     """The 32-layer Llama-3-8B-shaped stack at L = 32768 as the benchmark runs
     it: one multi-layer call, bit-identical to per-layer calls on every layer,
     and two sampled layers checked against the oracle in full."""
-    monkeypatch.delenv("CKV_PATH", raising=False)
     w = wl.get("llama32")
     layers = [wl.make_layer_device(w, l, 0, gpu) for l in range(w.n_layers)]
     _say(f"case llama32 full stack, budgets {[d['budget'] for d in layers]}")
