@@ -7,17 +7,17 @@ product package.
 
 What it computes:
 
-  * the Semantic Retrieval Head score of every attention head (section 3.1,
+  * the Semantic Retrieval Head score of every attention head (section 3.2,
     equation 1): over the decoding steps of calibration samples, the
     attention mass a head puts on the answer span, counted at the steps whose
     generated token belongs to the answer;
-  * the SRH set of every layer: its top-k heads by that score (section 3.2);
-  * the eviction error of a layer (section 3.3, equations 2-4): over decoding
+  * the SRH set of every layer: its top-k heads by that score (section 3.3);
+  * the eviction error of a layer (section 3.4, equations 2-4): over decoding
     steps, the Frobenius norm of the difference between the attention block's
     output (after the output projection) with the compressed and with the full
     KV cache, relative to the full-cache output;
   * the layer budgets: a minimum m per layer, the rest of the total in
-    proportion to the normalised errors, each layer capped at M (section 3.3
+    proportion to the normalised errors, each layer capped at M (section 3.4
     and section 4, "Implementation Details").
 
 Readings of points the paper leaves open (restated where used, and listed in

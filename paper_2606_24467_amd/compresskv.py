@@ -1,6 +1,7 @@
 """Python binding of libcompresskv (ctypes; argument marshalling only).
 
-The functions mirror the C ABI in include/compresskv.h and take torch tensors
+The functions mirror the C ABI in include/compresskv.h and
+include/compresskv_offline.h and take torch tensors
 for device memory; every computation runs in the HIP library.  There is no
 fallback: if the library is missing or fails to load, every call raises.
 """
@@ -22,8 +23,8 @@ POOL_MAX, POOL_AVG = 0, 1
 POOL_THEN_MEAN, MEAN_THEN_POOL = 0, 1
 INDEX_PER_GROUP, INDEX_LAYER = 0, 1
 
-_HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
-                       "include", "compresskv.h")
+_INCLUDE = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
+_HEADERS = [os.path.join(_INCLUDE, h) for h in ("compresskv.h", "compresskv_offline.h")]
 
 
 class CkvProblem(ctypes.Structure):
@@ -49,12 +50,22 @@ class CkvProblem(ctypes.Structure):
     ]
 
 
+class CkvSrhProblem(ctypes.Structure):
+    _fields_ = [
+        ("n_samples", ctypes.c_int32),
+        ("n_steps", ctypes.c_int32),
+        ("n_heads", ctypes.c_int32),
+        ("ctx_len", ctypes.c_int32),
+        ("spans_host", ctypes.c_void_p),
+    ]
+
+
 _LIB = None
 
 
 def exported_names() -> list[str]:
-    """Function names the public header declares."""
-    text = open(_HEADER).read()
+    """Function names the public headers declare."""
+    text = "".join(open(h).read() for h in _HEADERS)
     return sorted(set(re.findall(r"\b(compresskv_[a-z_]+)\s*\(", text)))
 
 
@@ -92,6 +103,11 @@ def lib() -> ctypes.CDLL:
     L.compresskv_status_string.restype = ctypes.c_char_p
     L.compresskv_last_error.argtypes = []
     L.compresskv_last_error.restype = ctypes.c_char_p
+    SP = ctypes.POINTER(CkvSrhProblem)
+    L.compresskv_srh_scores.argtypes = [SP, vp, vp, vp, vp, vp, vp]
+    L.compresskv_srh_scores.restype = ctypes.c_int
+    L.compresskv_select_srh.argtypes = [i32, i32, vp, i32, vp, vp]
+    L.compresskv_select_srh.restype = ctypes.c_int
     _LIB = L
     return L
 
@@ -377,3 +393,52 @@ def compress_layers(p: Problem, q_wins, ks, vs, srh_masks, budgets, *, want_scor
 
 def default_scale(head_dim: int) -> float:
     return 1.0 / math.sqrt(head_dim)
+
+
+# ---------------------------------------------------------------------------
+# Offline analyses (include/compresskv_offline.h)
+# ---------------------------------------------------------------------------
+def srh_problem(attn: torch.Tensor, spans_host) -> tuple:
+    """ckv_srh_problem for attention weights [S, N, H, L]; returns it with the
+    host span array it points to (keep both alive for the call)."""
+    S, N, H, Lc = attn.shape
+    spans_np = np.ascontiguousarray(np.asarray(spans_host, dtype=np.int32).reshape(S, 2))
+    p = CkvSrhProblem(n_samples=S, n_steps=N, n_heads=H, ctx_len=Lc,
+                      spans_host=spans_np.ctypes.data)
+    return p, spans_np
+
+
+def compresskv_srh_scores(p: CkvSrhProblem, attn, gen_tokens, ctx_tokens, spans, scores,
+                          stream=None) -> None:
+    _check("compresskv_srh_scores",
+           lib().compresskv_srh_scores(ctypes.byref(p), _ptr(attn), _ptr(gen_tokens),
+                                       _ptr(ctx_tokens), _ptr(spans), _ptr(scores),
+                                       _stream(stream)))
+
+
+def compresskv_select_srh(n_layers: int, heads_per_layer: int, scores, top_k: int, srh_mask,
+                          stream=None) -> None:
+    _check("compresskv_select_srh",
+           lib().compresskv_select_srh(n_layers, heads_per_layer, _ptr(scores), top_k,
+                                       _ptr(srh_mask), _stream(stream)))
+
+
+def srh_scores(attn: torch.Tensor, gen_tokens: torch.Tensor, ctx_tokens: torch.Tensor,
+               spans_host, stream=None) -> torch.Tensor:
+    """Equation 1 for every head: fp32 [H]."""
+    if attn.dtype != torch.float32 or not attn.is_contiguous():
+        raise ValueError("attn must be a contiguous fp32 tensor [S, N, H, L]")
+    p, spans_np = srh_problem(attn, spans_host)
+    spans = torch.from_numpy(spans_np).to(attn.device)
+    scores = torch.empty(attn.shape[2], dtype=torch.float32, device=attn.device)
+    compresskv_srh_scores(p, attn, gen_tokens.to(torch.int32).contiguous(),
+                          ctx_tokens.to(torch.int32).contiguous(), spans, scores, stream)
+    return scores
+
+
+def select_srh(scores: torch.Tensor, n_layers: int, top_k: int, stream=None) -> torch.Tensor:
+    """Each layer's top_k heads: uint8 mask [n_layers, heads per layer]."""
+    hp = scores.numel() // n_layers
+    mask = torch.empty((n_layers, hp), dtype=torch.uint8, device=scores.device)
+    compresskv_select_srh(n_layers, hp, scores.contiguous(), top_k, mask, stream)
+    return mask

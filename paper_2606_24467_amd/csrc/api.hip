@@ -10,28 +10,15 @@
 #include <vector>
 
 #include "../../include/compresskv.h"
+#include "api_common.h"
 #include "ckv_launch.h"
 
 namespace {
 
-thread_local std::string g_last_error;
-
-int fail(int status, const char *fmt, ...) {
-  char buf[512];
-  va_list ap;
-  va_start(ap, fmt);
-  vsnprintf(buf, sizeof buf, fmt, ap);
-  va_end(ap);
-  g_last_error = buf;
-  return status;
-}
-
-int ok() {
-  g_last_error.clear();
-  return CKV_OK;
-}
-
-bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+using ckv_api::aligned;
+using ckv_api::fail;
+using ckv_api::g_last_error;
+using ckv_api::ok;
 
 int elem_size(const ckv_problem *p) { return p->dtype == CKV_BF16 ? 2 : 4; }
 
