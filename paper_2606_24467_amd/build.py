@@ -16,7 +16,7 @@ CSRC = os.path.join(HERE, "csrc")
 LIBDIR = os.path.join(HERE, "lib")
 LIBNAME = "libcompresskv.so"
 SOURCES = ["api.hip", "score_kernels.hip", "score_layers.hip", "fused_score.hip",
-           "select_gather_kernels.hip", "offline.hip"]
+           "select_gather_kernels.hip", "offline.hip", "decode_error.hip"]
 ARCH = "gfx950"
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++20", "-fPIC",

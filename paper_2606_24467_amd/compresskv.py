@@ -60,6 +60,15 @@ class CkvSrhProblem(ctypes.Structure):
     ]
 
 
+class CkvErrorProblem(ctypes.Structure):
+    _fields_ = [
+        ("n_steps", ctypes.c_int32),
+        ("d_model", ctypes.c_int32),
+        ("budget", ctypes.c_int32),
+        ("eps", ctypes.c_float),
+    ]
+
+
 _LIB = None
 
 
@@ -108,6 +117,13 @@ def lib() -> ctypes.CDLL:
     L.compresskv_srh_scores.restype = ctypes.c_int
     L.compresskv_select_srh.argtypes = [i32, i32, vp, i32, vp, vp]
     L.compresskv_select_srh.restype = ctypes.c_int
+    EP = ctypes.POINTER(CkvErrorProblem)
+    L.compresskv_layer_error_workspace_bytes.argtypes = [P, EP]
+    L.compresskv_layer_error_workspace_bytes.restype = sz
+    L.compresskv_layer_error.argtypes = [P, EP, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.compresskv_layer_error.restype = ctypes.c_int
+    L.compresskv_allocate_budgets.argtypes = [i32, vp, ctypes.c_int64, i32, i32, vp]
+    L.compresskv_allocate_budgets.restype = ctypes.c_int
     _LIB = L
     return L
 
@@ -442,3 +458,43 @@ def select_srh(scores: torch.Tensor, n_layers: int, top_k: int, stream=None) -> 
     mask = torch.empty((n_layers, hp), dtype=torch.uint8, device=scores.device)
     compresskv_select_srh(n_layers, hp, scores.contiguous(), top_k, mask, stream)
     return mask
+
+
+def compresskv_layer_error_workspace_bytes(p: Problem, e: CkvErrorProblem) -> int:
+    n = lib().compresskv_layer_error_workspace_bytes(ctypes.byref(p.c), ctypes.byref(e))
+    if n == 0:
+        raise CompressKVError("compresskv_layer_error_workspace_bytes", INVALID_ARGUMENT)
+    return n
+
+
+def compresskv_layer_error(p: Problem, e: CkvErrorProblem, q_dec, k, v, k_out, v_out, w_o, err,
+                           ws, stream=None) -> None:
+    _check("compresskv_layer_error",
+           lib().compresskv_layer_error(ctypes.byref(p.c), ctypes.byref(e), _ptr(q_dec), _ptr(k),
+                                        _ptr(v), _ptr(k_out), _ptr(v_out), _ptr(w_o), _ptr(err),
+                                        _ptr(ws), ws.numel() * ws.element_size(),
+                                        _stream(stream)))
+
+
+def layer_error(p: Problem, q_dec: torch.Tensor, k, v, k_out: torch.Tensor, v_out, w_o,
+                eps: float = 1e-6, stream=None) -> torch.Tensor:
+    """Equations 2-4 for one layer: fp32 [1] on the device.  k_out / v_out are
+    the compact caches [batch, Hkv, budget, D] of the eviction path."""
+    e = CkvErrorProblem(n_steps=q_dec.shape[1], d_model=w_o.shape[0], budget=k_out.shape[2],
+                        eps=eps)
+    ws = torch.empty(compresskv_layer_error_workspace_bytes(p, e), dtype=torch.uint8,
+                     device=q_dec.device)
+    err = torch.empty(1, dtype=torch.float32, device=q_dec.device)
+    compresskv_layer_error(p, e, q_dec.contiguous(), k, v, k_out.contiguous(), v_out.contiguous(),
+                           w_o.contiguous(), err, ws, stream)
+    return err
+
+
+def allocate_budgets(errors, total: int, min_budget: int, max_budget: int) -> np.ndarray:
+    """Layer budgets (host): int32 [n_layers]."""
+    e = np.ascontiguousarray(np.asarray(errors, dtype=np.float32))
+    out = np.zeros(e.shape[0], dtype=np.int32)
+    _check("compresskv_allocate_budgets",
+           lib().compresskv_allocate_budgets(e.shape[0], e.ctypes.data, int(total), min_budget,
+                                             max_budget, out.ctypes.data))
+    return out

@@ -1,7 +1,12 @@
 // Offline analyses of CompressKV (include/compresskv_offline.h): the SRH
-// score of every head (section 3.2, equation 1) and each layer's SRH set
-// (section 3.3).
+// score of every head (section 3.2, equation 1), each layer's SRH set
+// (section 3.3) and the layer budgets from the layers' eviction errors
+// (section 3.4; the errors themselves are computed in decode_error.hip).
 #include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <vector>
 
 #include "../../include/compresskv_offline.h"
 #include "api_common.h"
@@ -112,6 +117,67 @@ int compresskv_select_srh(int32_t n_layers, int32_t heads_per_layer, const float
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess)
     return fail(CKV_HIP_ERROR, "select srh launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int compresskv_allocate_budgets(int32_t n_layers, const float *errors_host, int64_t total,
+                                int32_t min_budget, int32_t max_budget, int32_t *budgets_host) {
+  if (n_layers < 1) return fail(CKV_INVALID_ARGUMENT, "n_layers must be >= 1 (got %d)", n_layers);
+  if (!errors_host || !budgets_host)
+    return fail(CKV_INVALID_ARGUMENT, "errors_host and budgets_host are required");
+  if (min_budget < 1 || max_budget < min_budget)
+    return fail(CKV_INVALID_ARGUMENT, "need 1 <= min_budget <= max_budget");
+  const int n = n_layers;
+  if (total < (int64_t)n * min_budget || total > (int64_t)n * max_budget)
+    return fail(CKV_INVALID_ARGUMENT, "total must lie in [n_layers * min, n_layers * max]");
+  double esum = 0.0;
+  for (int i = 0; i < n; ++i) {
+    const float e = errors_host[i];
+    if (!std::isfinite(e) || e < 0.f)
+      return fail(CKV_INVALID_ARGUMENT, "layer %d: error must be finite and >= 0", i);
+    esum += e;
+  }
+  // normalised errors (a layer set of all-zero errors shares evenly)
+  std::vector<double> w(n), share(n, 0.0);
+  for (int i = 0; i < n; ++i) w[i] = esum > 0.0 ? (double)errors_host[i] / esum : 0.0;
+  std::vector<char> capped(n, 0);
+  for (;;) {
+    int n_free = 0;
+    double wsum = 0.0;
+    for (int i = 0; i < n; ++i)
+      if (!capped[i]) {
+        ++n_free;
+        wsum += w[i];
+      }
+    const double rest =
+        (double)(total - (int64_t)(n - n_free) * max_budget - (int64_t)n_free * min_budget);
+    bool over = false;
+    for (int i = 0; i < n; ++i) {
+      if (capped[i]) continue;
+      share[i] = wsum > 0.0 ? rest * w[i] / wsum : rest / n_free;
+      over |= (min_budget + share[i] > max_budget);
+    }
+    if (!over) break;
+    for (int i = 0; i < n; ++i)
+      if (!capped[i] && min_budget + share[i] > max_budget) capped[i] = 1;
+  }
+  int64_t used = 0;
+  std::vector<int> order;
+  for (int i = 0; i < n; ++i) {
+    if (capped[i]) {
+      budgets_host[i] = max_budget;
+    } else {
+      budgets_host[i] = min_budget + (int32_t)std::floor(share[i]);
+      order.push_back(i);
+    }
+    used += budgets_host[i];
+  }
+  // the units left by rounding down: largest fractional parts first
+  std::stable_sort(order.begin(), order.end(), [&](int x, int y) {
+    return share[x] - std::floor(share[x]) > share[y] - std::floor(share[y]);
+  });
+  for (int64_t left = total - used, j = 0; left > 0 && j < (int64_t)order.size(); --left, ++j)
+    budgets_host[order[j]] += 1;
   return ok();
 }
 

@@ -59,3 +59,111 @@ def test_select_srh_validation(L):
     assert f(32, 32, None, 4, FAKE, None) == C.INVALID_ARGUMENT
     assert f(32, 32, FAKE, 4, None, None) == C.INVALID_ARGUMENT
     assert f(32, 32, FAKE + 2, 4, FAKE, None) == C.UNSUPPORTED
+
+
+# ------------------------------------------------------------------ budgets
+# compresskv_allocate_budgets is host code: it runs here, without a GPU.
+import os
+from oracle import offline_oracle as OO
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def test_allocate_budgets_hand_worked(L):
+    rows = {}
+    for line in open(os.path.join(GOLDEN, "budget_worked.txt")):
+        line = line.strip()
+        if line and not line.startswith("#"):
+            k, *v = line.split()
+            rows[k] = v
+    got = C.allocate_budgets([float(x) for x in rows["errors"]], int(rows["total"][0]),
+                             int(rows["min"][0]), int(rows["max"][0]))
+    assert got.tolist() == [int(x) for x in rows["budgets"]]
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_allocate_budgets_matches_oracle(L, seed):
+    """The paper's setting (m = 32, M = 3 x the per-layer average) on random
+    error profiles, identical to the oracle's integer budgets."""
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(2, 81))
+    per = int(rng.integers(64, 2049))
+    e = rng.gamma(0.4, size=n).astype(np.float32)
+    if seed == 0:
+        e[:] = 1.0          # equal errors
+    if seed == 1:
+        e[3:] = 0.0         # most layers error-free
+    got = C.allocate_budgets(e, n * per, 32, 3 * per)
+    want = OO.allocate_budgets(OO.normalize_errors(e.astype(np.float64)), n * per, 32, 3 * per)
+    assert got.tolist() == want.tolist()
+
+
+def test_allocate_budgets_validation(L):
+    f = L.compresskv_allocate_budgets
+    e = np.ones(4, dtype=np.float32)
+    out = np.zeros(4, dtype=np.int32)
+    assert f(0, e.ctypes.data, 100, 1, 50, out.ctypes.data) == C.INVALID_ARGUMENT
+    assert f(4, None, 100, 1, 50, out.ctypes.data) == C.INVALID_ARGUMENT
+    assert f(4, e.ctypes.data, 100, 1, 50, None) == C.INVALID_ARGUMENT
+    assert f(4, e.ctypes.data, 100, 0, 50, out.ctypes.data) == C.INVALID_ARGUMENT
+    assert f(4, e.ctypes.data, 100, 60, 50, out.ctypes.data) == C.INVALID_ARGUMENT
+    assert f(4, e.ctypes.data, 3, 1, 50, out.ctypes.data) == C.INVALID_ARGUMENT     # < n * min
+    assert f(4, e.ctypes.data, 201, 1, 50, out.ctypes.data) == C.INVALID_ARGUMENT   # > n * max
+    bad = e.copy()
+    bad[2] = -1
+    assert f(4, bad.ctypes.data, 100, 1, 50, out.ctypes.data) == C.INVALID_ARGUMENT
+    bad[2] = np.nan
+    assert f(4, bad.ctypes.data, 100, 1, 50, out.ctypes.data) == C.INVALID_ARGUMENT
+    assert f(4, e.ctypes.data, 100, 1, 50, out.ctypes.data) == C.OK
+    assert out.tolist() == [25, 25, 25, 25]
+
+
+# -------------------------------------------------------------- layer error
+def _err_case(**kw):
+    c = _Case(**kw)
+    e = C.CkvErrorProblem(n_steps=kw.get("T", 4), d_model=64, budget=32, eps=1e-6)
+    return c, e
+
+
+class _Case:
+    def __init__(self, lens=(100, 200), Hq=8, Hkv=2, D=128, T=4, dtype=C.BF16):
+        self.cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+        self.p = C.CkvProblem(batch=len(lens), n_q_heads=Hq, n_kv_heads=Hkv, head_dim=D,
+                              window=1, dtype=dtype, pool_type=C.POOL_MAX, pool_kernel=1,
+                              reduce_order=C.POOL_THEN_MEAN, scale=0.0, cu_seqlens=FAKE,
+                              cu_seqlens_host=self.cu.ctypes.data, k_stride_tok=Hkv * D,
+                              k_stride_head=D, v_stride_tok=Hkv * D, v_stride_head=D)
+
+
+def _layer_error(L, c, e, ws_bytes=1 << 40, ws=FAKE, err=FAKE, **ptrs):
+    args = {n: ptrs.get(n, FAKE) for n in ("q", "k", "v", "ko", "vo", "w")}
+    return L.compresskv_layer_error(ctypes.byref(c.p), ctypes.byref(e), args["q"], args["k"],
+                                    args["v"], args["ko"], args["vo"], args["w"], err, ws,
+                                    ws_bytes, None)
+
+
+def test_layer_error_validation(L):
+    c, e = _err_case()
+    need = L.compresskv_layer_error_workspace_bytes(ctypes.byref(c.p), ctypes.byref(e))
+    assert need > 0 and need % 256 == 0
+    assert _layer_error(L, c, e, ws_bytes=need - 1) == C.WORKSPACE_TOO_SMALL
+    assert _layer_error(L, c, e, ws=FAKE + 16) == C.UNSUPPORTED
+    for n in ("q", "k", "v", "ko", "vo", "w"):
+        assert _layer_error(L, c, e, **{n: 0}) == C.INVALID_ARGUMENT, n
+        assert _layer_error(L, c, e, **{n: FAKE + 8}) == C.UNSUPPORTED, n
+    assert _layer_error(L, c, e, err=0) == C.INVALID_ARGUMENT
+    for field, val, st in [("n_steps", 0, C.INVALID_ARGUMENT), ("d_model", 0, C.INVALID_ARGUMENT),
+                           ("budget", 0, C.INVALID_ARGUMENT), ("eps", -1.0, C.INVALID_ARGUMENT),
+                           ("n_steps", 17, C.UNSUPPORTED)]:     # 17 steps x 4 heads > 64 rows
+        c2, e2 = _err_case()
+        setattr(e2, field, val)
+        assert _layer_error(L, c2, e2) == st, field
+    c3, e3 = _err_case(lens=tuple([50] * 9), T=4)                 # 9 x 4 vectors > 32
+    assert _layer_error(L, c3, e3) == C.UNSUPPORTED
+    c4, e4 = _err_case(Hq=2, Hkv=2, D=64)                          # Hq * D = 128: not a multiple of 256
+    assert _layer_error(L, c4, e4) == C.UNSUPPORTED
+    c5, e5 = _err_case(D=96)
+    assert _layer_error(L, c5, e5) == C.UNSUPPORTED
+    c6, e6 = _err_case()
+    c6.cu[1] = 0                                                   # empty sequence
+    assert _layer_error(L, c6, e6) == C.INVALID_ARGUMENT

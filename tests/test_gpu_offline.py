@@ -104,3 +104,95 @@ def test_calibration_to_layer_masks(gpu):
         kth = np.sort(w)[::-1][3]
         diff = np.flatnonzero(m_gpu[l] != m_ora[l])
         assert np.all(np.abs(w[diff] - kth) <= SRH_RTOL * kth), (l, diff)
+
+
+# ------------------------------------------------------------ equations 2 - 4
+ERR_RTOL = 2e-3   # fp32 attention and projection (exp2, fixed-order sums) against fp64
+
+
+def _error_case(seed, lens, Hq, Hkv, D, T, B, d_model, dtype):
+    """Full caches, decoding queries, W_O and a synthetic compact cache (a
+    random sorted subset of min(L, B) positions per sequence and group, its
+    K/V rows copied on the host), with the values the kernels read."""
+    rng = np.random.default_rng(seed)
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    tt = torch.bfloat16 if dtype == C.BF16 else torch.float32
+    def rnd(*shape, s=1.0):
+        return torch.from_numpy((rng.standard_normal(shape) * s).astype(np.float32)).to(tt)
+    k = rnd(int(cu[-1]), Hkv, D)
+    v = rnd(int(cu[-1]), Hkv, D)
+    q = rnd(len(lens), T, Hq, D, s=2.0)
+    w_o = rnd(d_model, Hq * D, s=1.0 / np.sqrt(Hq * D))
+    batch = len(lens)
+    idx = np.full((batch, Hkv, B), -1, dtype=np.int64)
+    k_out = torch.zeros((batch, Hkv, B, D), dtype=tt)
+    v_out = torch.zeros((batch, Hkv, B, D), dtype=tt)
+    for b, L in enumerate(lens):
+        n = min(L, B)
+        for g in range(Hkv):
+            keep = np.sort(rng.choice(L, size=n, replace=False))
+            idx[b, g, :n] = keep
+            k_out[b, g, :n] = k[cu[b] + keep, g]
+            v_out[b, g, :n] = v[cu[b] + keep, g]
+    return dict(cu=cu, k=k, v=v, q=q, w_o=w_o, idx=idx, k_out=k_out, v_out=v_out)
+
+
+def _gpu_error(c, gpu, eps=1e-6):
+    k, v, q = c["k"].to(gpu), c["v"].to(gpu), c["q"].to(gpu)
+    cu = torch.from_numpy(c["cu"]).to(gpu)
+    qw = torch.zeros((q.shape[0], 1, q.shape[2], q.shape[3]), dtype=q.dtype, device=gpu)
+    p = C.Problem(qw, k, v, cu, cu_seqlens_host=c["cu"], pool_kernel=1)
+    return C.layer_error(p, q, k, v, c["k_out"].to(gpu), c["v_out"].to(gpu), c["w_o"].to(gpu),
+                         eps=eps).item()
+
+
+def _oracle_error(c, eps=1e-6):
+    f = lambda t: t.float().numpy().astype(np.float64)
+    return OO.layer_error(f(c["q"]), f(c["k"]), f(c["v"]), c["cu"], c["idx"], f(c["w_o"]), eps=eps)
+
+
+@pytest.mark.parametrize("name,kw", [
+    ("bf16 D128 ragged", dict(lens=(3000, 1700), Hq=32, Hkv=8, D=128, T=8, B=256, d_model=512,
+                              dtype=C.BF16)),
+    ("bf16 64 rows", dict(lens=(2500,), Hq=32, Hkv=8, D=128, T=16, B=300, d_model=256,
+                          dtype=C.BF16)),
+    ("fp32 D64", dict(lens=(700, 1300, 90), Hq=8, Hkv=2, D=64, T=5, B=100, d_model=200,
+                      dtype=C.F32)),
+    ("bf16 one step", dict(lens=(1025,), Hq=8, Hkv=8, D=128, T=1, B=17, d_model=64,
+                           dtype=C.BF16)),
+])
+def test_layer_error_matches_oracle(gpu, name, kw):
+    _say(f"case layer error {name}")
+    c = _error_case(11, **kw)
+    got = _gpu_error(c, gpu)
+    want = _oracle_error(c)
+    assert want > 0
+    np.testing.assert_allclose(got, want, rtol=ERR_RTOL)
+
+
+def test_layer_error_is_zero_when_every_position_is_kept(gpu):
+    """B >= L: the compact cache holds every row in order, so both attentions
+    see the same keys in the same chunks and the error is exactly 0."""
+    c = _error_case(12, lens=(900, 400), Hq=16, Hkv=4, D=128, T=4, B=1024, d_model=128,
+                    dtype=C.BF16)
+    for b, L in enumerate((900, 400)):
+        for g in range(4):
+            assert np.array_equal(c["idx"][b, g, :L], np.arange(L))
+    assert _gpu_error(c, gpu) == 0.0
+
+
+def test_errors_to_layer_budgets(gpu):
+    """Four layers: GPU errors, then the library's allocation, against the
+    oracle's errors and allocation (the paper's m = 32, M = 3 x average)."""
+    errs_gpu, errs_ora = [], []
+    for l, B in enumerate((40, 120, 300, 80)):
+        c = _error_case(20 + l, lens=(2000,), Hq=32, Hkv=8, D=128, T=8, B=B, d_model=256,
+                        dtype=C.BF16)
+        errs_gpu.append(_gpu_error(c, gpu))
+        errs_ora.append(_oracle_error(c))
+    np.testing.assert_allclose(errs_gpu, errs_ora, rtol=ERR_RTOL)
+    per = 128
+    got = C.allocate_budgets(np.array(errs_gpu, dtype=np.float32), 4 * per, 32, 3 * per)
+    want = OO.allocate_budgets(OO.normalize_errors(np.array(errs_ora)), 4 * per, 32, 3 * per)
+    assert got.sum() == 4 * per
+    assert np.all(np.abs(got - want) <= 1)   # equal up to the rounding of nearly equal shares
