@@ -287,3 +287,41 @@ def compress_layer(q_win: np.ndarray, k: np.ndarray, v: np.ndarray,
             k_out[b, g, :n] = k[s0 + sel, g, :]
             v_out[b, g, :n] = v[s0 + sel, g, :]
     return LayerResult(idx=idx, k_out=k_out, v_out=v_out, scores=scores)
+
+
+def compress_layer_heads(q_win: np.ndarray, k: np.ndarray, v: np.ndarray,
+                         cu_seqlens: np.ndarray, srh_mask: np.ndarray,
+                         group_budgets: np.ndarray, pool_kernel: int,
+                         pool_type: int = POOL_MAX, reduce_order: int = POOL_THEN_MEAN,
+                         scale: float | None = None,
+                         k_values: np.ndarray | None = None) -> LayerResult:
+    """Per-group budgets (head-level budget allocation, combined with CompressKV
+    in section 4 "Orthogonal to Prior Efficiency Methods"): group g keeps
+    group_budgets[g] tokens, chosen exactly as in compress_layer.
+
+    The outputs are ragged per group: with off[g] = sum of the budgets of the
+    groups before g, idx[b, off[g] + j] is group g's j-th kept position and
+    k_out[b, off[g] + j] its row (-1 / zeros past the kept count).
+    scores are those of compress_layer (they do not depend on the budget).
+    """
+    group_budgets = np.asarray(group_budgets, dtype=np.int64)
+    Hkv = k.shape[1]
+    batch, D = q_win.shape[0], k.shape[2]
+    off = np.concatenate([[0], np.cumsum(group_budgets)])
+    total = int(off[-1])
+    idx = np.full((batch, total), -1, dtype=np.int64)
+    k_out = np.zeros((batch, total, D), dtype=k.dtype)
+    v_out = np.zeros((batch, total, D), dtype=v.dtype)
+    scores = None
+    for g in range(Hkv):
+        res = compress_layer(q_win, k, v, cu_seqlens, srh_mask, int(group_budgets[g]),
+                             pool_kernel, pool_type, reduce_order, scale=scale,
+                             k_values=k_values)
+        if scores is None:
+            scores = res.scores
+        o = int(off[g])
+        idx[:, o:o + int(group_budgets[g])] = res.idx[:, g]
+        k_out[:, o:o + int(group_budgets[g])] = res.k_out[:, g]
+        v_out[:, o:o + int(group_budgets[g])] = res.v_out[:, g]
+    return LayerResult(idx=idx, k_out=k_out, v_out=v_out, scores=scores)
+
