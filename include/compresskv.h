@@ -188,6 +188,31 @@ int compresskv_compress_layers(const ckv_problem *p, int32_t n_layers,
                                float *scores_or_null, void *ws, size_t ws_bytes, void *stream);
 
 /*
+ * Head-level budgets (per-group budgets, as in the combination of CompressKV
+ * with head-level allocation, section 4 "Orthogonal to Prior Efficiency
+ * Methods"): KV group g keeps group_budgets_host[g] (>= W) positions, chosen
+ * exactly as by compresskv_select with that budget.  The outputs are ragged
+ * per group: with off[g] = the sum of the budgets of groups 0 .. g-1 and
+ * total = the sum of all of them,
+ *   idx    int32 [batch][total]:   entry j of (b, g) at b * total + off[g] + j
+ *   k_out, v_out [batch][total][D]: row b * total + off[g] + j, dtype of k / v
+ * with -1 / zero rows past a group's kept count.  Needs CKV_INDEX_PER_GROUP
+ * (CKV_UNSUPPORTED otherwise) and batch * total < 2^31.  The workspace of
+ * compresskv_compress_layer_heads is compresskv_workspace_bytes(p, mask,
+ * max_g group_budgets_host[g]).
+ */
+int compresskv_select_heads(const ckv_problem *p, const float *scores,
+                            const int32_t *group_budgets_host, int32_t *idx, void *stream);
+int compresskv_gather_heads(const ckv_problem *p, const void *k, const void *v,
+                            const int32_t *idx, const int32_t *group_budgets_host, void *k_out,
+                            void *v_out, void *stream);
+int compresskv_compress_layer_heads(const ckv_problem *p, const void *q_win, const void *k,
+                                    const void *v, const uint8_t *srh_mask_host,
+                                    const int32_t *group_budgets_host, int32_t *idx, void *k_out,
+                                    void *v_out, float *scores_or_null, void *ws, size_t ws_bytes,
+                                    void *stream);
+
+/*
  * Which scoring implementation compresskv_score / _compress_layer will use for
  * this problem: 2 = two passes over K (the default), 1 = single pass (each key
  * read once from HBM), used when the environment variable CKV_PATH=single is

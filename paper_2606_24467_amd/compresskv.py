@@ -117,6 +117,13 @@ def lib() -> ctypes.CDLL:
     L.compresskv_srh_scores.restype = ctypes.c_int
     L.compresskv_select_srh.argtypes = [i32, i32, vp, i32, vp, vp]
     L.compresskv_select_srh.restype = ctypes.c_int
+    L.compresskv_select_heads.argtypes = [P, vp, vp, vp, vp]
+    L.compresskv_gather_heads.argtypes = [P, vp, vp, vp, vp, vp, vp, vp]
+    L.compresskv_compress_layer_heads.argtypes = [P, vp, vp, vp, u8p, vp, vp, vp, vp, vp, vp, sz,
+                                                  vp]
+    for f in ("compresskv_select_heads", "compresskv_gather_heads",
+              "compresskv_compress_layer_heads"):
+        getattr(L, f).restype = ctypes.c_int
     EP = ctypes.POINTER(CkvErrorProblem)
     L.compresskv_layer_error_workspace_bytes.argtypes = [P, EP]
     L.compresskv_layer_error_workspace_bytes.restype = sz
@@ -498,3 +505,49 @@ def allocate_budgets(errors, total: int, min_budget: int, max_budget: int) -> np
            lib().compresskv_allocate_budgets(e.shape[0], e.ctypes.data, int(total), min_budget,
                                              max_budget, out.ctypes.data))
     return out
+
+
+# ---------------------------------------------------------------------------
+# Head-level (per-group) budgets
+# ---------------------------------------------------------------------------
+def _budgets(group_budgets) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(group_budgets, dtype=np.int32))
+
+
+def compresskv_select_heads(p: Problem, scores, group_budgets, idx, stream=None) -> None:
+    gb = _budgets(group_budgets)
+    _check("compresskv_select_heads",
+           lib().compresskv_select_heads(ctypes.byref(p.c), _ptr(scores), gb.ctypes.data,
+                                         _ptr(idx), _stream(stream)))
+
+
+def compresskv_gather_heads(p: Problem, k, v, idx, group_budgets, k_out, v_out,
+                            stream=None) -> None:
+    gb = _budgets(group_budgets)
+    _check("compresskv_gather_heads",
+           lib().compresskv_gather_heads(ctypes.byref(p.c), _ptr(k), _ptr(v), _ptr(idx),
+                                         gb.ctypes.data, _ptr(k_out), _ptr(v_out),
+                                         _stream(stream)))
+
+
+def compress_layer_heads(p: Problem, q_win, k, v, srh_mask, group_budgets, *, want_scores=False,
+                         ws=None, stream=None):
+    """S1-S6 with per-group budgets: (idx [batch, total], k_out, v_out
+    [batch, total, D], scores or None), total = sum of the budgets."""
+    gb = _budgets(group_budgets)
+    total = int(gb.sum())
+    dev = k.device
+    idx = torch.empty((p.batch, total), dtype=torch.int32, device=dev)
+    k_out = torch.empty((p.batch, total, k.shape[2]), dtype=k.dtype, device=dev)
+    v_out = torch.empty((p.batch, total, v.shape[2]), dtype=v.dtype, device=dev)
+    scores = (torch.empty((k.shape[1], p.total_tokens), dtype=torch.float32, device=dev)
+              if want_scores else None)
+    mask = _mask(srh_mask)
+    if ws is None:
+        ws = workspace(p, mask, int(gb.max()), dev)
+    _check("compresskv_compress_layer_heads",
+           lib().compresskv_compress_layer_heads(
+               ctypes.byref(p.c), _ptr(q_win), _ptr(k), _ptr(v), mask.ctypes.data, gb.ctypes.data,
+               _ptr(idx), _ptr(k_out), _ptr(v_out), _ptr(scores), _ptr(ws),
+               ws.numel() * ws.element_size(), _stream(stream)))
+    return idx, k_out, v_out, scores

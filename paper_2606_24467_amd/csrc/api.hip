@@ -602,6 +602,32 @@ int run_layers(const ckv_problem *p, int n_layers, const LayerPtrs &lp, const ui
   return ok();
 }
 
+// Per-group budgets from the host array (head-level allocation).
+int check_group_budgets(const ckv_problem *p, const int32_t *gb_host, ckv::GroupBudgets &gb,
+                        int *max_budget) {
+  if (!gb_host) return fail(CKV_INVALID_ARGUMENT, "group_budgets_host is NULL");
+  if (p->index_mode == CKV_INDEX_LAYER)
+    return fail(CKV_UNSUPPORTED, "per-group budgets need per-group selections "
+                                 "(CKV_INDEX_PER_GROUP)");
+  int64_t total = 0;
+  *max_budget = 0;
+  gb = ckv::GroupBudgets{};
+  for (int g = 0; g < p->n_kv_heads; ++g) {
+    if (gb_host[g] < p->window)
+      return fail(CKV_INVALID_ARGUMENT, "group %d: budget (%d) must be >= window (%d)", g,
+                  gb_host[g], p->window);
+    gb.budget[g] = gb_host[g];
+    gb.off[g] = (int32_t)total;
+    total += gb_host[g];
+    *max_budget = std::max(*max_budget, gb_host[g]);
+  }
+  if (total * p->batch > INT32_MAX)
+    return fail(CKV_UNSUPPORTED, "batch * sum of the group budgets must fit in int32");
+  gb.on = 1;
+  gb.total = (int32_t)total;
+  return CKV_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -770,6 +796,80 @@ int compresskv_compress_layers(const ckv_problem *p, int32_t n_layers,
   lp.v_out = v_out_ptrs_host;
   lp.budgets = budgets_host;
   return run_layers(p, n_layers, lp, srh_masks_host, scores_or_null, ws, ws_bytes, stream, true);
+}
+
+int compresskv_select_heads(const ckv_problem *p, const float *scores,
+                            const int32_t *group_budgets_host, int32_t *idx, void *stream) {
+  int st, max_budget;
+  ckv::GroupBudgets gb;
+  if ((st = check_problem(p))) return st;
+  if ((st = check_group_budgets(p, group_budgets_host, gb, &max_budget))) return st;
+  if ((st = check_ptr(scores, "scores", 4)) || (st = check_ptr(idx, "idx", 4))) return st;
+  Plan pl;
+  pl.T = p->cu_seqlens_host[p->batch];
+  ckv::SelectArgs sa = select_args(p, pl, nullptr);
+  sa.gb = gb;
+  sa.l0 = layer_desc(nullptr, nullptr, nullptr, nullptr, const_cast<float *>(scores), idx,
+                     nullptr, nullptr, max_budget);
+  if ((st = hip_status(ckv::launch_select(sa, 0, (hipStream_t)stream), "select"))) return st;
+  return ok();
+}
+
+int compresskv_gather_heads(const ckv_problem *p, const void *k, const void *v,
+                            const int32_t *idx, const int32_t *group_budgets_host, void *k_out,
+                            void *v_out, void *stream) {
+  int st, max_budget;
+  ckv::GroupBudgets gb;
+  if ((st = check_problem(p))) return st;
+  if ((st = check_group_budgets(p, group_budgets_host, gb, &max_budget))) return st;
+  if ((st = check_ptr(k, "k", 16)) || (st = check_ptr(v, "v", 16)) ||
+      (st = check_ptr(idx, "idx", 4)) || (st = check_ptr(k_out, "k_out", 16)) ||
+      (st = check_ptr(v_out, "v_out", 16)))
+    return st;
+  ckv::GatherArgs ga = gather_args(p);
+  ga.gb = gb;
+  ga.l0 = layer_desc(nullptr, nullptr, k, v, nullptr, const_cast<int32_t *>(idx), k_out, v_out,
+                     max_budget);
+  if ((st = hip_status(ckv::launch_gather(ga, 0, max_budget, (hipStream_t)stream), "gather")))
+    return st;
+  return ok();
+}
+
+int compresskv_compress_layer_heads(const ckv_problem *p, const void *q_win, const void *k,
+                                    const void *v, const uint8_t *srh_mask_host,
+                                    const int32_t *group_budgets_host, int32_t *idx, void *k_out,
+                                    void *v_out, float *scores_or_null, void *ws, size_t ws_bytes,
+                                    void *stream) {
+  Plan pl;
+  int st, max_budget;
+  ckv::GroupBudgets gb;
+  if ((st = check_problem(p))) return st;
+  if ((st = check_mask(p, srh_mask_host, pl))) return st;
+  if ((st = check_group_budgets(p, group_budgets_host, gb, &max_budget))) return st;
+  if ((st = check_ptr(q_win, "q_win", 16)) || (st = check_ptr(k, "k", 16)) ||
+      (st = check_ptr(v, "v", 16)) || (st = check_ptr(idx, "idx", 4)) ||
+      (st = check_ptr(k_out, "k_out", 16)) || (st = check_ptr(v_out, "v_out", 16)))
+    return st;
+  if (scores_or_null && (st = check_ptr(scores_or_null, "scores", 4))) return st;
+  make_plan(p, pl, false);
+  if ((st = check_ws(pl, ws, ws_bytes))) return st;
+  make_plan(p, pl, true);
+  float *scores = scores_or_null
+                      ? scores_or_null
+                      : reinterpret_cast<float *>(static_cast<char *>(ws) + pl.scores_off);
+  hipStream_t s = (hipStream_t)stream;
+  if ((st = hip_status(launch_scoring(p, pl, q_win, k, scores, ws, s), "score"))) return st;
+  const int *hist = reinterpret_cast<const int *>(static_cast<char *>(ws) + pl.hist_off);
+  ckv::SelectArgs sa = select_args(p, pl, hist);
+  sa.gb = gb;
+  sa.l0 = layer_desc(nullptr, nullptr, nullptr, nullptr, scores, idx, nullptr, nullptr,
+                     max_budget);
+  if ((st = hip_status(ckv::launch_select(sa, 0, s), "select"))) return st;
+  ckv::GatherArgs ga = gather_args(p);
+  ga.gb = gb;
+  ga.l0 = layer_desc(nullptr, nullptr, k, v, nullptr, idx, k_out, v_out, max_budget);
+  if ((st = hip_status(ckv::launch_gather(ga, 0, max_budget, s), "gather"))) return st;
+  return ok();
 }
 
 }  // extern "C"

@@ -155,6 +155,22 @@ struct FusedArgs {
   int seq_units[65];       // first ticket of sequence b within a layer (group-major), b <= batch
 };
 
+// Per-group budgets (head-level allocation): group g keeps budget[g] rows,
+// stored ragged: entry j of (sequence b, group g) is row b * total + off[g] + j.
+struct GroupBudgets {
+  int32_t on;
+  int32_t total;                    // sum of the budgets
+  int32_t budget[kMaxKvHeads];
+  int32_t off[kMaxKvHeads];         // exclusive prefix sums
+};
+
+// Where (sequence b, group g)'s kept list starts in idx (rows of the
+// compact cache), and its budget.
+__device__ __forceinline__ int64_t kept_base(const GroupBudgets &gb, int b, int g, int Hkv,
+                                             int budget) {
+  return gb.on ? (int64_t)b * gb.total + gb.off[g] : ((int64_t)b * Hkv + g) * budget;
+}
+
 struct SelectArgs {
   LayerDesc l0;            // uses scores, idx, budget
   const LayerDesc *layers;
@@ -164,6 +180,7 @@ struct SelectArgs {
   int32_t T, Hkv, W, batch;
   int32_t n_sel;           // selections per (layer, sequence): Hkv, or 1 (layer-shared set)
   int32_t out_groups;      // idx rows each selection writes: 1, or Hkv (layer-shared set)
+  GroupBudgets gb;         // per-group budgets (single-layer calls), if gb.on
 };
 
 // Layer-shared index set: the layer score from the per-group scores.
@@ -180,6 +197,7 @@ struct GatherArgs {
   const int32_t *cu;
   int64_t k_stride_tok, k_stride_head, v_stride_tok, v_stride_head;  // bytes
   int32_t Hkv, batch, row_bytes;
+  GroupBudgets gb;         // per-group budgets (single-layer calls), if gb.on
 };
 
 // One layer of the table as the host hands it over (SRH mask as bits over the

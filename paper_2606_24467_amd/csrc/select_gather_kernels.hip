@@ -104,11 +104,11 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a)
   const int layer = ML ? (int)blockIdx.y / a.batch : 0;
   const int b = (int)blockIdx.y - layer * a.batch;
   const LayerView lv = layer_view<ML>(a, layer, 0);
-  const int budget = lv.budget;
+  const int budget = a.gb.on ? a.gb.budget[g] : lv.budget;
   const int tid = threadIdx.x;
   const int s0 = a.cu[b];
   const int L = a.cu[b + 1] - s0;
-  const gptr<int32_t> out = lv.idx + ((int64_t)b * a.Hkv + g) * budget;
+  const gptr<int32_t> out = lv.idx + kept_base(a.gb, b, g, a.Hkv, budget);
   // position `pos` of the kept list, in every idx row this selection serves
   auto put = [&](int pos, int32_t val) {
     for (int r = 0; r < a.out_groups; ++r) out[(int64_t)r * budget + pos] = val;
@@ -253,7 +253,7 @@ __global__ __launch_bounds__(256) void gather_kernel(const GatherArgs a) {
   const int layer = ML ? (int)blockIdx.z / a.batch : 0;
   const int b = (int)blockIdx.z - layer * a.batch;
   const LayerView lv = layer_view<ML>(a, layer, 0);
-  const int budget = lv.budget;
+  const int budget = a.gb.on ? a.gb.budget[g] : lv.budget;
   const gptr<const char> kb = lv.k;
   const gptr<const char> vb = lv.v;
   const int lanes_per_row = a.row_bytes >> 4;
@@ -262,7 +262,7 @@ __global__ __launch_bounds__(256) void gather_kernel(const GatherArgs a) {
   const int r_in = threadIdx.x / lanes_per_row;
   const int s0 = a.cu[b];
   const int L = a.cu[b + 1] - s0;
-  const int64_t obase = ((int64_t)b * a.Hkv + g) * budget;
+  const int64_t obase = kept_base(a.gb, b, g, a.Hkv, budget);
   {
     const int r = blockIdx.x * rows_per_pass + r_in;
     if (r >= budget) return;

@@ -260,3 +260,26 @@ def test_multi_layer_row_tile_limit_uses_the_largest_layer(L):
     c.masks[1, :] = 1                               # layer 1: 8 SRHs x 4 row tiles > 12
     assert c.compress_layers(L) == C.UNSUPPORTED
     assert c.ws_bytes(L) == 0
+
+
+def test_group_budget_rules(L):
+    c = Case()                                   # Hkv = 2, W = 16
+    gb = np.array([64, 32], dtype=np.int32)
+    f_sel = lambda b, p=c.p: L.compresskv_select_heads(ctypes.byref(p), FAKE, b, FAKE, None)
+    f_gat = lambda b, p=c.p: L.compresskv_gather_heads(ctypes.byref(p), FAKE, FAKE, FAKE, b,
+                                                       FAKE, FAKE, None)
+    f_all = lambda b, p=c.p, ws=1 << 40: L.compresskv_compress_layer_heads(
+        ctypes.byref(p), FAKE, FAKE, FAKE, c.mask.ctypes.data, b, FAKE, FAKE, FAKE, None, FAKE,
+        ws, None)
+    for f in (f_sel, f_gat, f_all):
+        assert f(None) == C.INVALID_ARGUMENT
+        low = np.array([64, 15], dtype=np.int32)          # group 1 below W
+        assert f(low.ctypes.data) == C.INVALID_ARGUMENT
+        assert "group 1" in L.compresskv_last_error().decode()
+    layer = _mutate(Case(), index_mode=C.INDEX_LAYER)
+    assert L.compresskv_select_heads(ctypes.byref(layer.p), FAKE, gb.ctypes.data, FAKE,
+                                     None) == C.UNSUPPORTED
+    need = c.ws_bytes(L, budget=64)
+    assert f_all(gb.ctypes.data, ws=need - 1) == C.WORKSPACE_TOO_SMALL
+    assert L.compresskv_gather_heads(ctypes.byref(c.p), FAKE, FAKE, FAKE + 2, gb.ctypes.data,
+                                     FAKE, FAKE, None) == C.UNSUPPORTED
