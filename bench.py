@@ -116,6 +116,79 @@ def cpu_baseline(layers, w, seconds):
                       f"layers' worth), {t_total:.1f} s of oracle time, scaled to one layer"}
 
 
+def _time_ms(torch, fn, reps=5):
+    """Mean HIP-event time of fn() on the current stream (after one warm-up)."""
+    fn()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(reps)]
+    for e0, e1 in ev:
+        e0.record()
+        fn()
+        e1.record()
+    torch.cuda.synchronize()
+    return float(sum(e0.elapsed_time(e1) for e0, e1 in ev) / reps)
+
+
+def bench_offline(dev, C, wl, torch, np):
+    """The offline analyses at the sizes of the Llama-3-8B setting, synthetic
+    inputs: one JSON line per measurement with its algorithmic bytes."""
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+    # SRH score (equation 1): 4 samples x 32 decoding steps, 32 layers x 32 heads,
+    # 8192-token contexts, 32-token answer spans, every other step an answer token
+    S, N, H, Lc, span = 4, 32, 1024, 8192, 32
+    attn = torch.rand((S, N, H, Lc), generator=g, device=dev, dtype=torch.float32)
+    ctx = torch.randint(0, 30000, (S, Lc), generator=g, device=dev, dtype=torch.int32)
+    spans = np.array([[100 + 1000 * s, span] for s in range(S)], dtype=np.int32)
+    gen = torch.full((S, N), 40000, device=dev, dtype=torch.int32)
+    for s in range(S):
+        gen[s, ::2] = ctx[s, spans[s, 0]]
+    ms = _time_ms(torch, lambda: C.srh_scores(attn, gen, ctx, spans))
+    hit_bytes = S * (N // 2) * H * span * 4
+    print(json.dumps({"metric": "SRH score (equation 1)", "workload":
+                      f"{S} samples x {N} steps, {H} heads, context {Lc}, span {span}",
+                      "ms": ms, "algorithmic_bytes": hit_bytes,
+                      "achieved_GBs": hit_bytes / ms / 1e6, "bound": "latency"}), flush=True)
+    del attn
+    # layer eviction error (equations 2-4) at one Llama-3-8B layer: L = 32768,
+    # 32 query / 8 KV heads, D = 128, bf16, 8 decoding steps, budget 256,
+    # W_O 4096 x 4096
+    L, Hq, Hkv, D, T, B, dm = 32768, 32, 8, 128, 8, 256, 4096
+    bf = torch.bfloat16
+    k = torch.randn((L, Hkv, D), generator=g, device=dev).to(bf)
+    v = torch.randn((L, Hkv, D), generator=g, device=dev).to(bf)
+    k_out = k[:B].permute(1, 0, 2).contiguous()[None]
+    v_out = v[:B].permute(1, 0, 2).contiguous()[None]
+    q_dec = torch.randn((1, T, Hq, D), generator=g, device=dev).to(bf)
+    w_o = (torch.randn((dm, Hq * D), generator=g, device=dev) / 64).to(bf)
+    cu_host = np.array([0, L], dtype=np.int32)
+    cu = torch.from_numpy(cu_host).to(dev)
+    p = C.Problem(torch.zeros((1, 1, Hq, D), dtype=bf, device=dev), k, v, cu,
+                  cu_seqlens_host=cu_host, pool_kernel=1)
+    ms = _time_ms(torch, lambda: C.layer_error(p, q_dec, k, v, k_out, v_out, w_o))
+    nbytes = 2 * L * Hkv * D * 2 + 2 * Hkv * B * D * 2 + dm * Hq * D * 2 + T * Hq * D * 2
+    print(json.dumps({"metric": "layer eviction error (equations 2-4)", "workload":
+                      f"L={L}, {Hq}q/{Hkv}kv heads, D={D}, bf16, {T} steps, budget {B}, "
+                      f"W_O {dm}x{Hq * D}", "ms": ms, "algorithmic_bytes": nbytes,
+                      "achieved_GBs": nbytes / ms / 1e6, "peak_GBs": 8000.0,
+                      "frac": nbytes / ms / 1e6 / 8000.0, "bound": "hbm"}), flush=True)
+    # per-group budgets against one fixed budget at the same total, one
+    # Llama-3-8B layer at 32768 tokens
+    w = wl.get("llama1")
+    lay = wl.make_layer_device(w, 0, 0, dev)
+    p1 = C.Problem(lay["q_win"], lay["k"], lay["v"], lay["cu_seqlens"],
+                   cu_seqlens_host=lay["cu_seqlens_host"], pool_kernel=w.pool_kernel,
+                   pool_type=w.pool_type)
+    budgets = [64, 128, 256, 512, 1024, 1536, 2048, 2624]           # sum 8192 = 8 x 1024
+    ws = C.workspace(p1, lay["srh_mask"], max(budgets), dev)
+    ms_h = _time_ms(torch, lambda: C.compress_layer_heads(p1, lay["q_win"], lay["k"], lay["v"],
+                                                          lay["srh_mask"], budgets, ws=ws))
+    ms_f = _time_ms(torch, lambda: C.compress_layer(p1, lay["q_win"], lay["k"], lay["v"],
+                                                    lay["srh_mask"], 1024, ws=ws))
+    print(json.dumps({"metric": "per-group budgets (compress_layer_heads)", "workload":
+                      "llama1: L=32768, 32q/8kv, D=128, bf16; budgets 64..2624 per group, "
+                      "sum 8192", "ms": ms_h, "fixed_budget_1024_ms": ms_f}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -132,6 +205,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--streams", type=int, default=2,
                     help="per-layer mode: alternate the layers over this many streams")
+    ap.add_argument("--offline", action="store_true",
+                    help="only time the offline analyses (SRH scores, layer eviction error) "
+                         "and the per-group-budget path, one JSON line each")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain elementwise copy of MIB MiB (3 times): the "
                          "reference point that scales the HBM byte counters")
@@ -159,6 +235,9 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration_bytes_read": n, "copy_calibration_bytes_written": n,
                           "launches": 3, "kernel": "torch neg (elementwise, fp32)"}), flush=True)
+        return
+    if args.offline:
+        bench_offline(dev, C, wl, torch, np)
         return
     w = wl.get(args.workload)
     n_layers = args.layers or w.n_layers

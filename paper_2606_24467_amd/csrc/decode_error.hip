@@ -8,8 +8,9 @@
 //                       group) against one 512-key chunk, QK^T on MFMA, online
 //                       softmax in LDS, P.V on the VALU; partial (max, sum, O)
 //   dec_combine_kernel  merges the chunks of every row into A (fp32)
-//   dec_proj_kernel     y = W_O x for x = A_full and A_full - A_comp, 64 rows of
-//                       W_O per workgroup; per-workgroup sums of y^2
+//   dec_proj_kernel     y = W_O x for x = A_full and A_full - A_comp on fp32
+//                       MFMA (16 rows of W_O per workgroup, one wave per 16
+//                       vectors); per-workgroup sums of y^2
 //   dec_error_kernel    the per-step norms, their ratios and the layer sum
 //
 // Every reduction runs in a fixed order, so the result is deterministic.
@@ -24,9 +25,9 @@
 
 namespace ckv {
 
-constexpr int kDecChunk = 512;   // keys per attention workgroup
-constexpr int kDecSub = 128;     // keys per softmax step inside it (8 tiles)
-constexpr int kProjRows = 64;    // W_O rows per projection workgroup
+constexpr int kDecChunk = 256;   // keys per attention workgroup
+constexpr int kDecSub = 64;      // keys per softmax step inside it (one tile per wave)
+constexpr int kProjRows = 16;    // W_O rows per projection workgroup
 constexpr int kMaxDecRows = 64;  // decoding steps x query heads per group
 constexpr int kMaxVectors = 32;  // sequences x decoding steps
 
@@ -127,9 +128,9 @@ __global__ __launch_bounds__(256) void dec_attn_kernel(const DecArgs a) {
     for (int d = 0; d < 4; ++d) acc[i][d] = 0.f;
 
   for (int k0 = c0; k0 < c_end; k0 += kDecSub) {
-    // S: logits of the step's 8 key tiles (2 per wave), scaled to log2 units
+    // S: logits of the step's key tiles (kDecSub / 64 per wave), in log2 units
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < kDecSub / 64; ++i) {
       const int e = wave + 4 * i;
       const int key = min(k0 + 16 * e + c, cc.n_keys - 1);
       uint4 kf[NS];
@@ -157,13 +158,14 @@ __global__ __launch_bounds__(256) void dec_attn_kernel(const DecArgs a) {
       }
     }
     __syncthreads();
-    // online softmax: four threads per row, 32 keys each
+    // online softmax: four threads per row, kDecSub / 4 keys each
     {
+      constexpr int KPT = kDecSub / 4;
       const int r = tid >> 2, part = tid & 3;
       if (r < RP) {
-        float* zr = zs + r * ZS + 32 * part;
+        float* zr = zs + r * ZS + KPT * part;
         float mx = -INFINITY;
-        for (int j = 0; j < 32; ++j) mx = fmaxf(mx, zr[j]);
+        for (int j = 0; j < KPT; ++j) mx = fmaxf(mx, zr[j]);
         mx = fmaxf(mx, __shfl_xor(mx, 1));
         mx = fmaxf(mx, __shfl_xor(mx, 2));
         const float m_old = m_s[r];
@@ -171,7 +173,7 @@ __global__ __launch_bounds__(256) void dec_attn_kernel(const DecArgs a) {
         // a row with no visible key yet keeps zero weight
         const float alpha = (m_new == -INFINITY) ? 1.f : fast_exp2(m_old - m_new);
         float sm = 0.f;
-        for (int j = 0; j < 32; ++j) {
+        for (int j = 0; j < KPT; ++j) {
           const float p = (m_new == -INFINITY) ? 0.f : fast_exp2(zr[j] - m_new);
           zr[j] = p;
           sm += p;
@@ -223,111 +225,157 @@ __global__ __launch_bounds__(256) void dec_attn_kernel(const DecArgs a) {
   }
 }
 
-// Grid (Hkv, batch * 2), 256 threads: A of every row of the group from its
-// chunks, in chunk order.
+// Grid (R, Hkv, batch * 2), D threads: A of row r of the group from its
+// chunks.  The chunk maxima and weights are formed in parallel (LDS), the
+// weighted sums run over the chunks in order (thread d: column d).
 template <int D>
-__global__ __launch_bounds__(256) void dec_combine_kernel(const DecArgs a) {
-  const int g = blockIdx.x, b = (int)blockIdx.y >> 1, cache = (int)blockIdx.y & 1;
+__global__ __launch_bounds__(D) void dec_combine_kernel(const DecArgs a) {
+  constexpr int kMaxCh = 1024;   // chunks per pass of the weight table
+  __shared__ float w_s[kMaxCh];
+  __shared__ float red[D];
+  const int r = blockIdx.x, g = blockIdx.y, b = (int)blockIdx.z >> 1, cache = (int)blockIdx.z & 1;
+  const int d = threadIdx.x;
   const int L = a.cu[b + 1] - a.cu[b];
   const int n_keys = cache == 0 ? L : min(L, a.B);
   const int nch = (n_keys + kDecChunk - 1) / kDecChunk;
   const int64_t slot0 = (((int64_t)cache * a.batch + b) * a.Hkv + g) * a.n_chunks;
-  for (int i = threadIdx.x; i < a.R * D; i += 256) {
-    const int r = i / D, d = i - r * D;
-    float M = -INFINITY;
-    for (int ch = 0; ch < nch; ++ch) M = fmaxf(M, a.part_ml[(slot0 + ch) * kMaxDecRows + r].x);
-    float lsum = 0.f, o = 0.f;
-    for (int ch = 0; ch < nch; ++ch) {
-      const float2 ml = a.part_ml[(slot0 + ch) * kMaxDecRows + r];
-      const float w = fast_exp2(ml.x - M);
-      lsum += ml.y * w;
-      o += a.part_o[((slot0 + ch) * kMaxDecRows + r) * D + d] * w;
-    }
-    const int t = r / a.G, h = g * a.G + (r - t * a.G);
-    a.a[((((int64_t)cache * a.batch + b) * a.T + t) * a.Hq + h) * D + d] = o / lsum;
+  // the row's maximum over its chunks: per thread over chunks d, d + D, ...,
+  // then a tree in LDS (max is exact in any order)
+  float M = -INFINITY;
+  for (int ch = d; ch < nch; ch += D) M = fmaxf(M, a.part_ml[(slot0 + ch) * kMaxDecRows + r].x);
+  red[d] = M;
+  __syncthreads();
+  for (int h = D / 2; h > 0; h >>= 1) {
+    if (d < h) red[d] = fmaxf(red[d], red[d + h]);
+    __syncthreads();
   }
+  M = red[0];
+  float lsum = 0.f, o = 0.f;
+  for (int c0 = 0; c0 < nch; c0 += kMaxCh) {
+    const int n = min(kMaxCh, nch - c0);
+    __syncthreads();
+    for (int ch = d; ch < n; ch += D)
+      w_s[ch] = fast_exp2(a.part_ml[(slot0 + c0 + ch) * kMaxDecRows + r].x - M);
+    __syncthreads();
+    const float *po = a.part_o + ((slot0 + c0) * kMaxDecRows + r) * D + d;
+#pragma unroll 8
+    for (int ch = 0; ch < n; ++ch) o += po[(int64_t)ch * kMaxDecRows * D] * w_s[ch];
+    // every thread forms the same sum of the chunk sums, in chunk order
+    for (int ch = 0; ch < n; ++ch)
+      lsum += a.part_ml[(slot0 + c0 + ch) * kMaxDecRows + r].y * w_s[ch];
+  }
+  const int t = r / a.G, h = g * a.G + (r - t * a.G);
+  a.a[((((int64_t)cache * a.batch + b) * a.T + t) * a.Hq + h) * D + d] = o / lsum;
 }
 
 struct ProjArgs {
   const char *w_o;          // [d_model][HD], dtype T
   const float *a;           // [2][NV][HD]: A_full, A_comp
-  float *part_ss;           // [n_wg][2][NV]: sums of y_full^2, y_diff^2 over the workgroup's rows
+  float *part_ss;           // [n_wg][2][kMaxVectors]: sums of y_full^2, y_diff^2 over the
+                            // workgroup's rows of W_O
   int d_model, HD, NV;
 };
 
-// Grid (ceil(d_model / 64)), 256 threads: thread (quarter, row) accumulates
-// row o's dot products with every vector over a quarter of HD; the quarters
-// are added in order, then the squares over the workgroup's rows.
-template <typename T>
+// Grid (ceil(d_model / 16)), 256 threads.  The vectors are the rows of
+// X = [A_full (NV rows); A_full - A_comp (NV rows); zeros], in XT tiles of 16;
+// wave w computes Y = X W_O^T over the w-th quarter of the columns for every
+// X tile and the workgroup's 16 rows of W_O with v_mfma_f32_16x16x4_f32
+// (MFMA operands as in the scoring kernels: lane (quad, c) holds floats
+// 16 s + 4 quad .. +3 of row c of each tile).  The quarters are added in
+// order, then y^2 is summed over the 16 rows of W_O (lanes c, fixed butterfly).
+template <typename T, int XT>
 __global__ __launch_bounds__(256) void dec_proj_kernel(const ProjArgs p) {
-  constexpr int KC = 256;   // columns staged per step
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int o = (int)blockIdx.x * kProjRows + lane;
-  __shared__ float xs[2][kMaxVectors][KC];
-  __shared__ float ys[4][kProjRows][2 * kMaxVectors + 1];
-  float sf[kMaxVectors], sd[kMaxVectors];
+  const int c = lane & 15, quad = lane >> 4;
+  const int o = (int)blockIdx.x * kProjRows + c;            // this lane's row of W_O
+  const bool o_ok = o < p.d_model;
+  const T *wr = reinterpret_cast<const T *>(p.w_o) + (int64_t)(o_ok ? o : 0) * p.HD;
+  const float *xf[XT], *xc[XT];
+  int kind[XT];
 #pragma unroll
-  for (int n = 0; n < kMaxVectors; ++n) sf[n] = sd[n] = 0.f;
-  const int quarter = KC / 4;
-  for (int k0 = 0; k0 < p.HD; k0 += KC) {
-    __syncthreads();
-    for (int i = tid; i < p.NV * KC; i += 256) {
-      const int n = i / KC, k = i - n * KC;
-      const float f = p.a[(int64_t)n * p.HD + k0 + k];
-      const float cmp = p.a[((int64_t)p.NV + n) * p.HD + k0 + k];
-      xs[0][n][k] = f;
-      xs[1][n][k] = f - cmp;
+  for (int x = 0; x < XT; ++x) {
+    const int n = 16 * x + c;                                 // this lane's row of X tile x
+    kind[x] = n < p.NV ? 0 : (n < 2 * p.NV ? 1 : 2);          // full, difference, padding
+    const int v = kind[x] == 0 ? n : (kind[x] == 1 ? n - p.NV : 0);
+    xf[x] = p.a + (int64_t)v * p.HD;
+    xc[x] = p.a + (int64_t)(p.NV + v) * p.HD;
+  }
+  f32x4 acc[XT];
+#pragma unroll
+  for (int x = 0; x < XT; ++x) acc[x] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int q4 = p.HD / 4;                                    // columns per wave
+  for (int k0 = wave * q4 + 4 * quad; k0 < (wave + 1) * q4; k0 += 16) {
+    float4 wv;
+    if constexpr (sizeof(T) == 2) {
+      const uint2 raw = *reinterpret_cast<const uint2 *>(wr + k0);
+      wv = make_float4(__uint_as_float(raw.x << 16), __uint_as_float(raw.x & 0xFFFF0000u),
+                       __uint_as_float(raw.y << 16), __uint_as_float(raw.y & 0xFFFF0000u));
+    } else {
+      wv = *reinterpret_cast<const float4 *>(wr + k0);
     }
-    __syncthreads();
-    if (o < p.d_model) {
-      const T *wr = reinterpret_cast<const T *>(p.w_o) + (int64_t)o * p.HD + k0 + wave * quarter;
-      for (int k = 0; k < quarter; ++k) {
-        const float w = (float)wr[k];
-        const int kk = wave * quarter + k;
+    if (!o_ok) wv = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-        for (int n = 0; n < kMaxVectors; ++n) {
-          if (n < p.NV) {
-            sf[n] = __builtin_fmaf(w, xs[0][n][kk], sf[n]);
-            sd[n] = __builtin_fmaf(w, xs[1][n][kk], sd[n]);
-          }
-        }
+    for (int x = 0; x < XT; ++x) {
+      float4 xv = *reinterpret_cast<const float4 *>(xf[x] + k0);
+      if (kind[x] == 1) {
+        const float4 y = *reinterpret_cast<const float4 *>(xc[x] + k0);
+        xv = make_float4(xv.x - y.x, xv.y - y.y, xv.z - y.z, xv.w - y.w);
+      } else if (kind[x] == 2) {
+        xv = make_float4(0.f, 0.f, 0.f, 0.f);
       }
+      acc[x] = mfma_slice<float>(__builtin_bit_cast(uint4, xv), __builtin_bit_cast(uint4, wv),
+                                 acc[x]);
     }
   }
+  __shared__ f32x4 part[4][XT][64];
 #pragma unroll
-  for (int n = 0; n < kMaxVectors; ++n) {
-    ys[wave][lane][n] = sf[n];
-    ys[wave][lane][kMaxVectors + n] = sd[n];
-  }
+  for (int x = 0; x < XT; ++x) part[wave][x][lane] = acc[x];
   __syncthreads();
-  // thread j < 2 NV: squares of the workgroup's rows in row order
-  if (tid < 2 * p.NV) {
-    const int col = tid < p.NV ? tid : kMaxVectors + (tid - p.NV);
-    float ss = 0.f;
-    for (int r = 0; r < kProjRows; ++r) {
-      if ((int)blockIdx.x * kProjRows + r >= p.d_model) break;
-      const float y = ((ys[0][r][col] + ys[1][r][col]) + ys[2][r][col]) + ys[3][r][col];
-      ss = __builtin_fmaf(y, y, ss);
+  // wave x < XT finishes X tile x: quarters in order, then the squares
+  if (wave < XT) {
+    const f32x4 y = ((part[0][wave][lane] + part[1][wave][lane]) + part[2][wave][lane]) +
+                    part[3][wave][lane];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float sq = y[r] * y[r];
+#pragma unroll
+      for (int m = 1; m < 16; m <<= 1) sq += __shfl_xor(sq, m);
+      const int row = 16 * wave + 4 * quad + r;
+      if (c == 0 && row < 2 * p.NV)
+        p.part_ss[((int64_t)blockIdx.x * 2 + (row < p.NV ? 0 : 1)) * kMaxVectors +
+                  (row < p.NV ? row : row - p.NV)] = sq;
     }
-    p.part_ss[((int64_t)blockIdx.x * 2 + (tid < p.NV ? 0 : 1)) * kMaxVectors +
-              (tid < p.NV ? tid : tid - p.NV)] = ss;
   }
 }
 
-// One thread: per vector the norms over all workgroups (in order), the ratio,
-// and the sum over vectors.
-__global__ void dec_error_kernel(const float *part_ss, int n_wg, int NV, float eps, float *err) {
-  if (threadIdx.x != 0 || blockIdx.x != 0) return;
-  float e = 0.f;
-  for (int n = 0; n < NV; ++n) {
+// One workgroup of kMaxVectors waves' worth of lanes: wave n sums vector n's
+// squares over the projection workgroups (lane l: workgroups l, l + 64, ...
+// in order, then a fixed butterfly), forms the ratio, and thread 0 adds the
+// ratios in vector order.
+__global__ __launch_bounds__(64 * kMaxVectors / 2) void dec_error_kernel(const float *part_ss,
+                                                                        int n_wg, int NV,
+                                                                        float eps, float *err) {
+  __shared__ float ratio[kMaxVectors];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  for (int n = wave; n < NV; n += blockDim.x / 64) {
     float sf = 0.f, sd = 0.f;
-    for (int w = 0; w < n_wg; ++w) {
+    for (int w = lane; w < n_wg; w += 64) {
       sf += part_ss[((int64_t)w * 2 + 0) * kMaxVectors + n];
       sd += part_ss[((int64_t)w * 2 + 1) * kMaxVectors + n];
     }
-    e += sqrtf(sd) / (sqrtf(sf) + eps);
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) {
+      sf += __shfl_xor(sf, m);
+      sd += __shfl_xor(sd, m);
+    }
+    if (lane == 0) ratio[n] = sqrtf(sd) / (sqrtf(sf) + eps);
   }
-  err[0] = e;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float e = 0.f;
+    for (int n = 0; n < NV; ++n) e += ratio[n];
+    err[0] = e;
+  }
 }
 
 template <typename T, int D>
@@ -340,10 +388,15 @@ static void launch_dec_t(const DecArgs &a, const ProjArgs &pa, int rt, int n_wg,
     case 3: hipLaunchKernelGGL((dec_attn_kernel<T, D, 3>), g1, dim3(256), 0, s, a); break;
     default: hipLaunchKernelGGL((dec_attn_kernel<T, D, 4>), g1, dim3(256), 0, s, a); break;
   }
-  hipLaunchKernelGGL((dec_combine_kernel<D>), dim3(a.Hkv, a.batch * 2), dim3(256), 0, s, a);
-  hipLaunchKernelGGL((dec_proj_kernel<T>), dim3(n_wg), dim3(256), 0, s, pa);
-  hipLaunchKernelGGL(dec_error_kernel, dim3(1), dim3(64), 0, s, pa.part_ss, n_wg, pa.NV, eps,
-                     err);
+  hipLaunchKernelGGL((dec_combine_kernel<D>), dim3(a.R, a.Hkv, a.batch * 2), dim3(D), 0, s, a);
+  switch ((2 * pa.NV + 15) / 16) {
+    case 1: hipLaunchKernelGGL((dec_proj_kernel<T, 1>), dim3(n_wg), dim3(256), 0, s, pa); break;
+    case 2: hipLaunchKernelGGL((dec_proj_kernel<T, 2>), dim3(n_wg), dim3(256), 0, s, pa); break;
+    case 3: hipLaunchKernelGGL((dec_proj_kernel<T, 3>), dim3(n_wg), dim3(256), 0, s, pa); break;
+    default: hipLaunchKernelGGL((dec_proj_kernel<T, 4>), dim3(n_wg), dim3(256), 0, s, pa); break;
+  }
+  hipLaunchKernelGGL(dec_error_kernel, dim3(1), dim3(64 * kMaxVectors / 2), 0, s, pa.part_ss, n_wg,
+                     pa.NV, eps, err);
 }
 
 }  // namespace ckv
