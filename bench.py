@@ -38,18 +38,23 @@ MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # dense, MI355X
 # on this GPU) + WRITE_SIZE, in separate runs (profiles/).  A figure is valid
 # only for the kernel sources it was taken with: keyed by their hash.
 MEASURED_TRAFFIC = {
-    ("llama32", 32, "c68acfffd41e0b13"): (2 * (1053085.7 + 1188982.4) + 6248.0 + 33013.5) * 1024,
+    ("llama32", 32, "9aef9fb61f8247bb"): (2 * (1052747.3 + 1124644.3) + 6248.0 + 33013.5) * 1024,
 }
+
+
+# The sources that decide what the score phase reads and writes: its kernels,
+# their device building blocks and the host plan (chunking, workspace).
+SCORE_PHASE_SOURCES = ("ckv_device.h", "score_common.h", "score_kernels.h", "score_layers.hip",
+                       "api.hip")
 
 
 def kernel_source_hash() -> str:
     import hashlib
-    import glob
     root = os.path.join(ROOT, "paper_2606_24467_amd", "csrc")
     h = hashlib.sha256()
-    for f in sorted(glob.glob(os.path.join(root, "*.h")) + glob.glob(os.path.join(root, "*.hip"))):
-        h.update(os.path.basename(f).encode())
-        with open(f, "rb") as fh:
+    for f in SCORE_PHASE_SOURCES:
+        h.update(f.encode())
+        with open(os.path.join(root, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
