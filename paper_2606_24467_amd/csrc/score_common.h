@@ -310,18 +310,14 @@ __device__ __forceinline__ void merge_row_bias(const ScoreArgs &a, const float2 
 // key c): in-lane over the 4 rows and the SRH's row tiles, then across the
 // quads.  cs[h][16 + 16*e + c] receives SRH h's sum for key c of tile e.  Row
 // tiles past the group's own (zero queries) have bias +inf and add nothing.
-template <typename T, int D, int RT, int CSW, bool QR = true>
-__device__ __forceinline__ void tile_window_sums(const ScoreArgs &a,
-                                                 const uint4 (&kf)[Slices<T, D>::n],
-                                                 const uint4 (&qreg)[RegTiles<T, D, RT, QR>::n]
-                                                                    [Slices<T, D>::n],
-                                                 const uint4 *q_lds, const float (&bias)[RT][4],
-                                                 int e, bool keep, int c, int quad,
-                                                 float (*cs)[CSW]) {
+// The VALU half of tile_window_sums: window sums of a tile from its logits.
+template <int RT, int CSW>
+__device__ __forceinline__ void window_sums_from_logits(const ScoreArgs &a, const f32x4 (&acc)[RT],
+                                                        const float (&bias)[RT][4], int e,
+                                                        bool keep, int c, int quad,
+                                                        float (*cs)[CSW]) {
   // per row tile: the lane's 4 rows (no branch between the row tiles); the
   // terms are never -0, so starting from the first term equals starting from 0
-  f32x4 acc[RT];
-  tile_logits_all<T, D, RT, false, QR>(kf, qreg, q_lds, c, quad, acc);
   float vt[RT];
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
@@ -342,6 +338,19 @@ __device__ __forceinline__ void tile_window_sums(const ScoreArgs &a,
       ++hh;
     }
   }
+}
+
+template <typename T, int D, int RT, int CSW, bool QR = true>
+__device__ __forceinline__ void tile_window_sums(const ScoreArgs &a,
+                                                 const uint4 (&kf)[Slices<T, D>::n],
+                                                 const uint4 (&qreg)[RegTiles<T, D, RT, QR>::n]
+                                                                    [Slices<T, D>::n],
+                                                 const uint4 *q_lds, const float (&bias)[RT][4],
+                                                 int e, bool keep, int c, int quad,
+                                                 float (*cs)[CSW]) {
+  f32x4 acc[RT];
+  tile_logits_all<T, D, RT, false, QR>(kf, qreg, q_lds, c, quad, acc);
+  window_sums_from_logits<RT, CSW>(a, acc, bias, e, keep, c, quad, cs);
 }
 
 // Pooling along the token axis (positions clipped to the prefix [0, P)), then

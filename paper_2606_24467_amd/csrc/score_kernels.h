@@ -183,6 +183,12 @@ __global__ __launch_bounds__(64 * kStatsWaves) void stats_kernel(const ScoreArgs
 // round-robin (chunk2 + 32 keys = 16 * kWaves * tiles per wave and chunk);
 // the ring runs on across chunks, each chunk ending with its pooling.
 // ---------------------------------------------------------------------------
+// Key tiles per wave in the column sums' load ring (tiles per wave and chunk,
+// 16, is a multiple of it).  With the logits issued one tile ahead, two slots
+// keep two tiles in flight per wave and the kernel within 256 VGPRs (two
+// waves per SIMD); four slots measured slower (268 VGPRs, one wave).
+constexpr int kRingCs = 2;
+
 template <typename T, int D, int RT, int CSW>
 __device__ __forceinline__ void colsum_body(const ScoreArgs &a, const Work &w, uint4 *q_lds,
                                             float *bias_s, float (*cs)[CSW], float *stage,
@@ -208,9 +214,9 @@ __device__ __forceinline__ void colsum_body(const ScoreArgs &a, const Work &w, u
 
   uint4 qv[QStage<T, D, RT, NT>::n];
   q_load<T, D, RT, NT>(a, w.lv, w.b, w.rt_n, qv);
-  uint4 kr[kRing][NS];
+  uint4 kr[kRingCs][NS];
 #pragma unroll
-  for (int r = 0; r < kRing; ++r) load_k_row<T, D>(a, w.kbase, s0, key_of(r), g, quad, kr[r]);
+  for (int r = 0; r < kRingCs; ++r) load_k_row<T, D>(a, w.kbase, s0, key_of(r), g, quad, kr[r]);
   q_store<T, D, RT, NT>(qv, q_lds);
   for (int i = tid; i < kHistBins; i += NT) hist_s[i] = 0;
 
@@ -233,8 +239,10 @@ __device__ __forceinline__ void colsum_body(const ScoreArgs &a, const Work &w, u
     for (int r = 0; r < 4; ++r) bias[rt][r] = bias_s[rt * 16 + 4 * quad + r];
 
   // Column sums of a chunk plus one 16-key halo tile on each side:
-  // cs[h][16 + x] holds the window sum of SRH h at key cc0 + x.
-  auto consume = [&](const uint4 (&kf)[NS], int i) {
+  // cs[h][16 + x] holds the window sum of SRH h at key cc0 + x.  The logits
+  // of the wave's next tile are issued before the current tile's exp2 and
+  // sums, so the matrix pipeline works while the VALU does.
+  auto finish_tile = [&](const f32x4 (&lg)[RT], int i) {
     const int ch = i / tpc;
     const int cc0 = c0 + ch * a.chunk2;
     const int p_end = min(cc0 + a.chunk2, P);
@@ -242,8 +250,7 @@ __device__ __forceinline__ void colsum_body(const ScoreArgs &a, const Work &w, u
     const int e_lo = (cc0 > 0) ? -1 : 0;                              // left halo tile
     const int e_hi = (cc0 + 16 * ntiles < P) ? ntiles : ntiles - 1;   // right halo tile
     const int e = -1 + wave + kWaves * (i - ch * tpc);
-    tile_window_sums<T, D, RT, CSW>(a, kf, qreg, q_lds, bias, e, e >= e_lo && e <= e_hi, c,
-                                    quad, cs);
+    window_sums_from_logits<RT, CSW>(a, lg, bias, e, e >= e_lo && e <= e_hi, c, quad, cs);
   };
   // Pooling of a finished chunk (S4); cs and stage are rewritten by the next
   // chunk only after every thread has pooled and stored.
@@ -253,13 +260,22 @@ __device__ __forceinline__ void colsum_body(const ScoreArgs &a, const Work &w, u
     pool_chunk<NT, CSW>(a, cs, w.lv.nsrh, cc0, min(cc0 + a.chunk2, P), P, out, stage, hist_s);
     __syncthreads();
   };
-  for (int i = 0; i < n_tiles; i += kRing) {
+  // slot r of the ring holds the tiles i with i % kRingCs == r
+  f32x4 lg[RT];
+  tile_logits_all<T, D, RT, false>(kr[0], qreg, q_lds, c, quad, lg);
+  load_k_row<T, D>(a, w.kbase, s0, key_of(kRingCs), g, quad, kr[0]);
+  for (int i = 0; i < n_tiles; i += kRingCs) {
 #pragma unroll
-    for (int r = 0; r < kRing; ++r) {
-      consume(kr[r], i + r);
-      load_k_row<T, D>(a, w.kbase, s0, key_of(i + r + kRing), g, quad, kr[r]);
+    for (int r = 0; r < kRingCs; ++r) {
+      const int rn = (r + 1) % kRingCs;   // slot of tile i + r + 1
+      f32x4 lg_next[RT];
+      tile_logits_all<T, D, RT, false>(kr[rn], qreg, q_lds, c, quad, lg_next);
+      load_k_row<T, D>(a, w.kbase, s0, key_of(i + r + 1 + kRingCs), g, quad, kr[rn]);
+      finish_tile(lg, i + r);
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) lg[rt] = lg_next[rt];
     }
-    if ((i + kRing) % tpc == 0) pool(i / tpc);   // loads of the next chunk are in flight
+    if ((i + kRingCs) % tpc == 0) pool(i / tpc);   // loads of the next chunk are in flight
   }
   flush_hist<NT>(hist_s,
                  a.hist + w.layer * a.hist_layer + ((int64_t)w.b * a.Hkv + g) * kHistBins);
