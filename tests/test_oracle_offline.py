@@ -217,6 +217,10 @@ def test_budget_closed_forms():
     # exact proportional split when nothing is capped and shares are integral
     assert OO.allocate_budgets(np.array([0.1, 0.2, 0.3, 0.4]), 4 * 32 + 100, 32, 1000).tolist() \
         == [42, 52, 62, 72]
+    # rounding: shares 10/7, 20/7, 40/7 floor to 1, 2, 5; the two units left go
+    # to the largest fractional parts (6/7 and 5/7), not to the first layers
+    assert OO.allocate_budgets(np.array([1, 2, 4]) / 7, 3 * 32 + 10, 32, 1000).tolist() == \
+        [33, 35, 38]
     # equal errors: an even split, the remainder to the lowest layers
     assert OO.allocate_budgets(np.full(4, 0.25), 4 * 32 + 10, 32, 1000).tolist() == \
         [35, 35, 34, 34]
