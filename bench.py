@@ -41,6 +41,16 @@ MEASURED_TRAFFIC = {
     ("llama32", 32, "bf23299afca909b2"): (2 * (1053032.0 + 1105586.6) + 6248.0 + 33013.5) * 1024,
 }
 
+# MFMA work the score phase executes, from rocprofv3 on the same sources:
+# SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 FLOP of both kernels, and each kernel's
+# SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 XCDs x 1024 SIMDs).
+MEASURED_MFMA = {
+    ("llama32", 32, "bf23299afca909b2"): {
+        "executed_flops_per_launch": (275251200 + 288691200) * 512,
+        "busy_frac": {"stats_kernel": 137625600 / (6874478.8 / 8 * 1024),
+                      "colsum_kernel": 144345600 / (8506888.4 / 8 * 1024)}},
+}
+
 
 # The sources that decide what the score phase reads and writes: its kernels,
 # their device building blocks and the host plan (chunking, workspace).
@@ -339,7 +349,9 @@ def main():
     value = tokens * n_layers / (ms_per_step / 1e3)
     achieved = score_bytes_total / (score_ms / 1e3) / 1e9
     e2e_gbs = alg_bytes_total / (ms_per_step / 1e3) / 1e9
-    traffic = MEASURED_TRAFFIC.get((w.name, n_layers, kernel_source_hash()))
+    src_key = (w.name, n_layers, kernel_source_hash())
+    traffic = MEASURED_TRAFFIC.get(src_key)
+    counted = MEASURED_MFMA.get(src_key)
     dt = "bf16" if w.dtype == wl.BF16 else "f32"
     mfma_tflops = score_flops_total / (score_ms / 1e3) / 1e12
 
@@ -363,7 +375,14 @@ def main():
         "mfma": {"flops_per_launch": score_flops_total, "achieved": mfma_tflops,
                  "peak": MFMA_PEAK_TFLOPS[dt], "unit": "TFLOP/s",
                  "frac": mfma_tflops / MFMA_PEAK_TFLOPS[dt],
-                 "note": "algorithmic Q.K^T FLOPs of the score phase (one pass)"},
+                 "note": "algorithmic Q.K^T FLOPs of the score phase (one pass)",
+                 "counters": None if counted is None else {
+                     "executed_flops_per_launch": counted["executed_flops_per_launch"],
+                     "executed_frac": counted["executed_flops_per_launch"] / (score_ms / 1e3)
+                                      / 1e12 / MFMA_PEAK_TFLOPS[dt],
+                     "busy_frac": counted["busy_frac"],
+                     "note": "both passes' MFMA FLOPs from SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 "
+                             "over the same HIP-event time; MFMA busy cycles per kernel"}},
         "end_to_end": {"algorithmic_bytes_per_step": alg_bytes_total, "achieved_gbs": e2e_gbs,
                        "frac": e2e_gbs / HBM_PEAK_GBS},
     }

@@ -139,3 +139,39 @@ def test_full_32_layer_stack(gpu):
                              H.raw_bits(kos[l]), H.raw_bits(vos[l]))
         _check_needles(x, budgets[l], idxs[l].cpu().numpy())
         _say(f"  layer {l} matches the oracle, boundary swaps {swaps}")
+
+
+@pytest.mark.parametrize("name,sampled", [("qwen128k", (0, 19)), ("ragged8", (0, 23))])
+def test_full_stack_other_shapes(gpu, scoring_path, name, sampled):
+    """The Qwen-shaped stack (28 layers, 28q/4kv heads, L = 131072, W = 64,
+    Dirichlet budgets) and the ragged batch (32 layers, 8 sequences of
+    4096-16384 tokens) at full size: one multi-layer call, bit-identical to
+    per-layer calls on every layer, and sampled layers against the oracle in
+    full."""
+    w = wl.get(name)
+    if scoring_path == "single" and name == "qwen128k":
+        pytest.skip("the single-pass kernel does not apply at L = 131072 (512 units per "
+                    "group); that call runs the two-pass case again")
+    layers = [wl.make_layer_device(w, l, 0, gpu) for l in range(w.n_layers)]
+    _say(f"case {name} full stack, lengths {np.diff(layers[0]['cu_seqlens_host']).tolist()}, "
+         f"budgets {[d['budget'] for d in layers]}")
+    q = [d["q_win"] for d in layers]
+    k = [d["k"] for d in layers]
+    v = [d["v"] for d in layers]
+    cu, cu_host = layers[0]["cu_seqlens"], layers[0]["cu_seqlens_host"]
+    ps = [_problem(q[l], k[l], v[l], cu, cu_host, w) for l in range(w.n_layers)]
+    masks = np.stack([d["srh_mask"] for d in layers])
+    budgets = [d["budget"] for d in layers]
+    idxs, kos, vos, scores = C.compress_layers(ps[0], q, k, v, masks, budgets, want_scores=True)
+    ref = _per_layer(ps, q, k, v, masks, budgets)
+    torch.cuda.synchronize()
+    for l in range(w.n_layers):
+        for got, want in zip((idxs[l], kos[l], vos[l], scores[l]), ref[l]):
+            assert torch.equal(got, want), f"layer {l} differs from the per-layer call"
+    del ref
+    for l in sampled:
+        x = _host_inputs(w, l, layers[l])
+        swaps = _check_layer(x, budgets[l], scores[l].cpu().numpy(), idxs[l].cpu().numpy(),
+                             H.raw_bits(kos[l]), H.raw_bits(vos[l]))
+        _check_needles(x, budgets[l], idxs[l].cpu().numpy())
+        _say(f"  layer {l} matches the oracle, boundary swaps {swaps}")
