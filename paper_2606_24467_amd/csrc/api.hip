@@ -38,7 +38,8 @@ struct Plan {
   int rt_max = 0;      // max row tiles of a group (over the layers)
   int chunk1 = 0, max_chunks1 = 0;
   int chunk2 = 0, max_chunks2 = 0;
-  int cpw1 = 1, cpw2 = 1;  // consecutive chunks per scoring workgroup
+  int cpw1 = 1, cpw2 = 1;  // consecutive chunks per leading scoring workgroup
+  int lead1 = 1, lead2 = 1;  // leading workgroups per (sequence, group) and layer
   uint32_t head_end_mask = 0;
   // single-layer workspace: scores | stats | counters | histograms
   // multi-layer workspace:  table | scores | stats | histograms (all per layer)
@@ -223,6 +224,16 @@ void set_chunks(const ckv_problem *p, Plan &pl) {
   pl.max_chunks2 = std::max(1, (pl.lmax + c2 - 1) / c2);
 }
 
+// Workgroups of cpw chunks first, then at least `tail` chunks of every
+// (sequence, group) one per workgroup, so the end of each scoring grid is made
+// of short workgroups.
+void set_lead(Plan &pl, int tail1, int tail2) {
+  tail1 = env_int("CKV_TAIL1", tail1);
+  tail2 = env_int("CKV_TAIL2", tail2);
+  pl.lead1 = pl.cpw1 > 1 ? std::max(0, (pl.max_chunks1 - tail1) / pl.cpw1) : pl.max_chunks1;
+  pl.lead2 = pl.cpw2 > 1 ? std::max(0, (pl.max_chunks2 - tail2) / pl.cpw2) : pl.max_chunks2;
+}
+
 // The block the single-pass kernel zeroes before it runs, from `start`:
 // [0] ticket, [1] fallbacks, [64 ..) arrivals per (layer, group), then the
 // published (normaliser, marker) pairs per (layer, group, row slot), then the
@@ -247,6 +258,7 @@ int partial_slots(const Plan &pl) {
 // kernel), scores, partial row statistics, then the counters block.
 void make_plan(const ckv_problem *p, Plan &pl, bool decide_path) {
   set_chunks(p, pl);
+  set_lead(pl, 0, 0);
   pl.n_layers = 1;
   if (decide_path) choose_path(p, pl);
   pl.max_parts = partial_slots(pl);
@@ -263,6 +275,10 @@ void make_plan(const ckv_problem *p, Plan &pl, bool decide_path) {
   pl.hist_layer = 0;
 }
 
+// One-chunk workgroups at the end of the multi-layer scoring grids, per
+// (sequence, group) and layer.
+constexpr int kTail1 = 4, kTail2 = 4;
+
 // Multi-layer workspace: the layer table, then per layer the scores and the
 // partial row statistics, then the counters block (per layer inside).
 void make_plan_layers(const ckv_problem *p, int n_layers, Plan &pl, bool decide_path) {
@@ -278,6 +294,7 @@ void make_plan_layers(const ckv_problem *p, int n_layers, Plan &pl, bool decide_
   const int e1 = env_int("CKV_CPW1", 0), e2 = env_int("CKV_CPW2", 0);
   if (e1 > 0) pl.cpw1 = std::min(e1, 64);
   if (e2 > 0) pl.cpw2 = std::min(e2, 64);
+  set_lead(pl, kTail1, kTail2);
   pl.fused = false;
   if (decide_path) choose_path(p, pl);
   pl.max_parts = partial_slots(pl);
@@ -316,6 +333,9 @@ ckv::ScoreArgs score_args(const ckv_problem *p, const Plan &pl, void *ws) {
   a.parts_stride = pl.max_parts;   // partial slots between groups
   a.cpw1 = pl.cpw1;
   a.cpw2 = pl.cpw2;
+  a.lead1 = pl.lead1;
+  a.lead2 = pl.lead2;
+  a.nz = 0;   // set by the launcher
   a.chunk2 = pl.chunk2;
   a.max_chunks2 = pl.max_chunks2;
   const double scale = p->scale > 0.f ? (double)p->scale : 1.0 / std::sqrt((double)p->head_dim);

@@ -137,7 +137,10 @@ struct ScoreArgs {
   int32_t chunk1, max_chunks1;   // keys per statistics chunk, chunks of the longest sequence
   int32_t parts_stride;          // partial slots per (sequence, group) in stats
   int32_t chunk2, max_chunks2;   // keys per column-sum chunk, chunks of the longest sequence
-  int32_t cpw1, cpw2;            // consecutive chunks per workgroup (statistics, column sums)
+  int32_t cpw1, cpw2;            // consecutive chunks per leading workgroup (statistics, column sums)
+  int32_t lead1, lead2;          // leading workgroups per (sequence, group) and layer; the
+                                 // chunks after lead * cpw go one per workgroup
+  int32_t nz;                    // sequences x layers of the launch (set by the launcher)
   float c1;               // softmax scale * log2(e): logits in base-2 units
   int32_t pool_kernel, pool_type, reduce_order;
   uint32_t head_end_mask;  // bit rt set if row tile rt is the last tile of an SRH

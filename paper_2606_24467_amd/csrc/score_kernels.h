@@ -43,12 +43,46 @@ struct Work {
   int layer, b, g, s0, L, P, c0, n_chunks, rt_n;
 };
 
+// Launch order of both scoring grids (one dimension).  The first part holds,
+// for every (layer, sequence) and group, `lead` workgroups of cpw consecutive
+// chunks; the second part holds the chunks after lead * cpw, one per
+// workgroup.  The long workgroups start first and the last ones to start are
+// short, so the grid drains with little idle time at its end.  In both parts
+// the groups are fastest, then the key range, then the (layer, sequence) pair.
+// Consecutive workgroups go to the 8 XCDs in turn, so with 8 groups a plain
+// group index would give each XCD one group of every layer, and the XCDs
+// would get unequal work (the number of SRHs differs between groups).  The
+// group is therefore rotated by the key-range index: each XCD gets a mix of
+// the groups.
+struct BlockRange {
+  int g, z, first, count;   // group, (layer, sequence) pair, first chunk, chunks
+};
+
+__device__ __forceinline__ BlockRange block_range(const ScoreArgs &a, int lead, int cpw,
+                                                  int max_chunks) {
+  const int beta = blockIdx.x;
+  const int n_lead = a.Hkv * lead * a.nz;
+  const bool in_lead = beta < n_lead;
+  const int t = in_lead ? beta : beta - n_lead;
+  const int per_z = in_lead ? lead : max_chunks - lead * cpw;   // >= 1 where reached
+  const int u = t / a.Hkv;
+  const int g = (t - u * a.Hkv + u) % a.Hkv;
+  const int y = u % per_z, z = u / per_z;
+  return in_lead ? BlockRange{g, z, y * cpw, cpw} : BlockRange{g, z, lead * cpw + y, 1};
+}
+
+// Workgroups of a scoring grid.
+__host__ __device__ inline int64_t grid_blocks(int Hkv, int nz, int lead, int cpw,
+                                               int max_chunks) {
+  return (int64_t)Hkv * nz * (lead + (max_chunks - lead * cpw));
+}
+
 // ---------------------------------------------------------------------------
-// S1+S2 partial statistics.  Grid (Hkv, ceil(max_chunks1 / cpw1), batch
-// [x layers]), 64 * kStatsWaves threads; a workgroup covers cpw1 consecutive
-// chunks of one (sequence, group) and writes one partial per chunk.  The
-// groups of one key range are neighbours in launch order, so the workgroups in
-// flight read whole token rows of K ([T, Hkv, D]) rather than 1/Hkv of each.
+// S1+S2 partial statistics.  A workgroup (64 * kStatsWaves threads) covers
+// consecutive chunks of one (sequence, group), as block_range assigns them,
+// and writes one partial per chunk.  The groups of one key range are
+// neighbours in launch order, so the workgroups in flight read whole token
+// rows of K ([T, Hkv, D]) rather than 1/Hkv of each.
 // MFMA operands: A = 16 keys, B = 16 window rows, so lane (quad, c) holds the
 // logits of row c against keys 4*quad .. 4*quad+3 of the tile and keeps one
 // running (ref, sum) pair per row tile.  Wave w handles the key tiles
@@ -135,7 +169,7 @@ __device__ __forceinline__ void stats_body(const ScoreArgs &a, const Work &w, ui
       sum[rt] = 0.f;
     }
   };
-  int chunk = (int)blockIdx.y * a.cpw1;
+  int chunk = c0 / a.chunk1;
   for (int i = 0; i < n_tiles; i += kRing) {
 #pragma unroll
     for (int r = 0; r < kRing; ++r) {
@@ -148,15 +182,16 @@ __device__ __forceinline__ void stats_body(const ScoreArgs &a, const Work &w, ui
 
 template <typename T, int D, int RTM, bool ML>
 __global__ __launch_bounds__(64 * kStatsWaves) void stats_kernel(const ScoreArgs a) {
+  const BlockRange r = block_range(a, a.lead1, a.cpw1, a.max_chunks1);
   Work w;
-  w.g = blockIdx.x;
-  w.layer = ML ? (int)blockIdx.z / a.batch : 0;
-  w.b = (int)blockIdx.z - w.layer * a.batch;
+  w.g = r.g;
+  w.layer = ML ? r.z / a.batch : 0;
+  w.b = r.z - w.layer * a.batch;
   w.lv = layer_view<ML>(a, w.layer, w.g);
   w.kbase = w.lv.k;
   w.s0 = a.cu[w.b];
   w.L = a.cu[w.b + 1] - w.s0;
-  const int chunk0 = (int)blockIdx.y * a.cpw1;
+  const int chunk0 = r.first;
   if (chunk0 == 0) {   // the column-sum kernel accumulates this histogram afterwards
     int *h = a.hist + w.layer * a.hist_layer + ((int64_t)w.b * a.Hkv + w.g) * kHistBins;
     for (int i = threadIdx.x; i < kHistBins; i += 64 * kStatsWaves) h[i] = 0;
@@ -165,7 +200,7 @@ __global__ __launch_bounds__(64 * kStatsWaves) void stats_kernel(const ScoreArgs
   // uniform for the whole workgroup (a group without an SRH is not scored:
   // the layer-shared index set ignores it)
   if (w.c0 >= w.L || w.lv.nsrh == 0) return;
-  w.n_chunks = min(a.cpw1, (w.L - w.c0 + a.chunk1 - 1) / a.chunk1);
+  w.n_chunks = min(r.count, (w.L - w.c0 + a.chunk1 - 1) / a.chunk1);
   w.P = w.L - a.W;
   w.rt_n = w.lv.nsrh * a.th;
 
@@ -175,8 +210,8 @@ __global__ __launch_bounds__(64 * kStatsWaves) void stats_kernel(const ScoreArgs
 }
 
 // ---------------------------------------------------------------------------
-// S2+S3+S4.  Grid (Hkv, ceil(max_chunks2 / cpw2), batch [x layers]), 256
-// threads; a workgroup covers cpw2 consecutive chunks of chunk2 keys.
+// S2+S3+S4.  256 threads; a workgroup covers consecutive chunks of chunk2
+// keys of one (sequence, group), as block_range assigns them.
 // MFMA operands: A = 16 window rows, B = 16 keys, so lane (quad, c) holds
 // rows 4*quad .. 4*quad+3 of the tile against key c.  The tiles of a chunk
 // plus one halo tile on each side, e = -1 .. chunk2/16, go to the waves
@@ -285,24 +320,25 @@ template <typename T, int D, int RTM, bool ML>
 __global__ __launch_bounds__(64 * kWaves) void colsum_kernel(const ScoreArgs a) {
   constexpr int NT = 64 * kWaves;
   constexpr int CSW = kMaxChunk2 + 32;
+  const BlockRange r = block_range(a, a.lead2, a.cpw2, a.max_chunks2);
   Work w;
-  w.g = blockIdx.x;
-  w.layer = ML ? (int)blockIdx.z / a.batch : 0;
-  w.b = (int)blockIdx.z - w.layer * a.batch;
+  w.g = r.g;
+  w.layer = ML ? r.z / a.batch : 0;
+  w.b = r.z - w.layer * a.batch;
   w.lv = layer_view<ML>(a, w.layer, w.g);
   w.kbase = w.lv.k;
   w.s0 = a.cu[w.b];
   w.L = a.cu[w.b + 1] - w.s0;
-  w.c0 = (int)blockIdx.y * a.cpw2 * a.chunk2;
+  w.c0 = r.first * a.chunk2;
   if (w.c0 >= w.L || w.lv.nsrh == 0) return;
   w.P = w.L - a.W;
-  const int c_end = min(w.L, w.c0 + a.cpw2 * a.chunk2);
+  const int c_end = min(w.L, w.c0 + r.count * a.chunk2);
   // Window positions of this range are always kept: +inf.
   const gptr<float> out = w.lv.scores + (int64_t)w.g * a.T + w.s0;
   for (int j = max(w.c0, w.P) + (int)threadIdx.x; j < c_end; j += NT) out[j] = INFINITY;
   if (w.c0 >= w.P) return;                   // no prefix key in this range
   // chunks of the range that hold prefix keys
-  w.n_chunks = min(a.cpw2, (w.P - w.c0 + a.chunk2 - 1) / a.chunk2);
+  w.n_chunks = min(r.count, (w.P - w.c0 + a.chunk2 - 1) / a.chunk2);
   w.rt_n = w.lv.nsrh * a.th;
 
   // The staging buffer of the pooled scores is left out where it would not fit
@@ -324,14 +360,17 @@ __global__ __launch_bounds__(64 * kWaves) void colsum_kernel(const ScoreArgs a) 
 // Host-side launcher template; grid z = batch * n_layers (n_layers = 1 unless ML).
 // ---------------------------------------------------------------------------
 template <typename T, int D, int RTM, bool ML>
-static hipError_t launch_score_t(const ScoreArgs &a, int nz, hipStream_t stream) {
-  const int y1 = (a.max_chunks1 + a.cpw1 - 1) / a.cpw1;
-  const int y2 = (a.max_chunks2 + a.cpw2 - 1) / a.cpw2;
-  hipLaunchKernelGGL((stats_kernel<T, D, RTM, ML>), dim3(a.Hkv, y1, nz), dim3(64 * kStatsWaves),
+static hipError_t launch_score_t(const ScoreArgs &args, int nz, hipStream_t stream) {
+  ScoreArgs a = args;
+  a.nz = nz;
+  const int64_t n1 = grid_blocks(a.Hkv, nz, a.lead1, a.cpw1, a.max_chunks1);
+  const int64_t n2 = grid_blocks(a.Hkv, nz, a.lead2, a.cpw2, a.max_chunks2);
+  if (n1 < 1 || n2 < 1 || n1 > INT32_MAX || n2 > INT32_MAX) return hipErrorInvalidConfiguration;
+  hipLaunchKernelGGL((stats_kernel<T, D, RTM, ML>), dim3((unsigned)n1), dim3(64 * kStatsWaves),
                      0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((colsum_kernel<T, D, RTM, ML>), dim3(a.Hkv, y2, nz), dim3(64 * kWaves), 0,
+  hipLaunchKernelGGL((colsum_kernel<T, D, RTM, ML>), dim3((unsigned)n2), dim3(64 * kWaves), 0,
                      stream, a);
   return hipGetLastError();
 }
