@@ -8,7 +8,9 @@
 // chosen bucket are collected in LDS, and digits 2 (bits 19..9) and 3 (bits
 // 8..0) are resolved on that candidate list.  An ordered compaction then
 // writes the kept positions.  Integer work only, so the result does not
-// depend on scheduling.
+// depend on scheduling.  Every wave holds a contiguous run of positions with
+// its lanes on neighbouring positions, so the score loads are coalesced and
+// the compaction orders kept positions with wave ballots.
 //
 // S6 copies the kept K and V rows (section 3.3: the retained KV pairs form the
 // compressed cache) with 16-byte lanes; rows whose index is -1 become zeros.
@@ -88,13 +90,31 @@ __device__ __forceinline__ void find_bucket(const int *hist, int nb, int remain,
   __syncthreads();
 }
 
-// Scores [r0 + t*kEpt, r0 + (t+1)*kEpt) of thread t into registers (all loads
-// issued together); positions >= P read as 0 and are masked by the callers.
+// Position of a thread's element e in the round starting at r0: every wave
+// owns a run of kWaveRun consecutive positions and its lanes take
+// consecutive positions for each e, so a load instruction reads 256
+// contiguous bytes and the position order is (wave, e, lane).
+constexpr int kWaveRun = 64 * kEpt;
+__device__ __forceinline__ int elem_pos(int r0, int e) {
+  return r0 + (int)(threadIdx.x >> 6) * kWaveRun + e * 64 + (int)(threadIdx.x & 63);
+}
+
+// Lanes below this one whose bit is set in m.
+__device__ __forceinline__ int lanes_below(unsigned long long m) {
+  return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                        __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+// A thread's kEpt scores of the round starting at r0 into registers (all
+// loads issued together); positions >= P read as 0 and are masked by the
+// callers.
 __device__ __forceinline__ void load_round(gptr<const uint32_t> sc, int P, int r0,
                                            uint32_t (&v)[kEpt]) {
-  const int j0 = r0 + (int)threadIdx.x * kEpt;
 #pragma unroll
-  for (int e = 0; e < kEpt; ++e) v[e] = (j0 + e < P) ? sc[j0 + e] : 0u;
+  for (int e = 0; e < kEpt; ++e) {
+    const int j = elem_pos(r0, e);
+    v[e] = (j < P) ? sc[j] : 0u;
+  }
 }
 
 // Grid (Hkv, batch [x layers]), 1024 threads.
@@ -128,6 +148,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a)
 
   __shared__ int hist[kHistBins];
   __shared__ int scan_tmp[kSelThreads / 64];
+  __shared__ int wave_cnt[2][kSelThreads / 64];
   __shared__ int bucket_s, remain_s, ncand_s;
   __shared__ uint32_t cand_u[kCandCap];
   __shared__ int cand_j[kCandCap];
@@ -144,9 +165,8 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a)
     __syncthreads();
     for (int r = 0; r < nrounds; ++r) {
       if (!resident) load_round(sc, P, r * kRound, v);
-      const int j0 = r * kRound + tid * kEpt;
 #pragma unroll
-      for (int e = 0; e < kEpt; ++e) hist_add(hist, hist_bin(v[e]), j0 + e < P);
+      for (int e = 0; e < kEpt; ++e) hist_add(hist, hist_bin(v[e]), elem_pos(r * kRound, e) < P);
     }
   }
   if (tid == 0) ncand_s = 0;
@@ -159,14 +179,14 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a)
   // Candidates: prefix elements whose first digit equals the chosen bucket.
   for (int r = 0; r < nrounds; ++r) {
     if (!resident) load_round(sc, P, r * kRound, v);
-    const int j0 = r * kRound + tid * kEpt;
 #pragma unroll
     for (int e = 0; e < kEpt; ++e) {
-      if (j0 + e < P && (v[e] & pmask) == prefix) {
+      const int j = elem_pos(r * kRound, e);
+      if (j < P && (v[e] & pmask) == prefix) {
         const int slot = atomicAdd(&ncand_s, 1);
         if (slot < kCandCap) {
           cand_u[slot] = v[e];
-          cand_j[slot] = j0 + e;
+          cand_j[slot] = j;
         }
       }
     }
@@ -193,10 +213,10 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a)
     } else {
       for (int r = 0; r < nrounds; ++r) {
         if (!resident) load_round(sc, P, r * kRound, v);
-        const int j0 = r * kRound + tid * kEpt;
 #pragma unroll
         for (int e = 0; e < kEpt; ++e)
-          hist_add(hist, (int)((v[e] >> sh) & dmask), j0 + e < P && (v[e] & pmask) == prefix);
+          hist_add(hist, (int)((v[e] >> sh) & dmask),
+                   elem_pos(r * kRound, e) < P && (v[e] & pmask) == prefix);
       }
     }
     __syncthreads();
@@ -209,36 +229,61 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a)
 
   // prefix is the exact bit pattern of the k-th largest score; `remain` of the
   // positions holding it are kept (the lowest ones), plus every larger score.
-  // Ordered compaction, round by round: thread t owns a contiguous run.
+  // Ordered compaction, round by round: each wave counts its elements above
+  // and at the threshold, every wave forms the prefix over the waves before
+  // it, and the kept positions are written in (wave, e, lane) order.
   const uint32_t thr = prefix;
+  const int lane = tid & 63, wave = tid >> 6;
   int pos_base = 0, eq_base = 0;
   for (int r = 0; r < nrounds; ++r) {
     if (!resident) load_round(sc, P, r * kRound, v);
-    const int j0 = r * kRound + tid * kEpt;
-    int n_gt = 0, n_eq = 0;
+    int n_gt = 0, n_eq = 0;   // this thread's counts, then the wave's
 #pragma unroll
     for (int e = 0; e < kEpt; ++e) {
       const uint32_t u = v[e] & 0x7FFFFFFFu;
-      const bool ok = j0 + e < P;
-      n_gt += ok && (u > thr);
-      n_eq += ok && (u == thr);
+      const bool ok = elem_pos(r * kRound, e) < P;
+      n_gt += ok && u > thr;
+      n_eq += ok && u == thr;
     }
-    int eq_total, sel_total;
-    const int eq_before = eq_base + block_inclusive_scan(n_eq, scan_tmp, &eq_total) - n_eq;
-    const int take_eq = max(0, min(n_eq, remain - eq_before));
-    const int n_sel = n_gt + take_eq;
-    int pos = pos_base + block_inclusive_scan(n_sel, scan_tmp, &sel_total) - n_sel;
-    int eq_left = take_eq;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      n_gt += __shfl_xor(n_gt, o);
+      n_eq += __shfl_xor(n_eq, o);
+    }
+    if (lane == 0) {
+      wave_cnt[0][wave] = n_gt;
+      wave_cnt[1][wave] = n_eq;
+    }
+    __syncthreads();
+    int eq_before = 0, sel_before = 0, eq_total = 0, sel_total = 0;
+#pragma unroll
+    for (int x = 0; x < kSelThreads / 64; ++x) {
+      const int c_gt = wave_cnt[0][x], c_eq = wave_cnt[1][x];
+      const int take = max(0, min(c_eq, remain - (eq_base + eq_total)));   // wave x's kept ties
+      if (x < wave) {
+        eq_before += c_eq;
+        sel_before += c_gt + take;
+      }
+      eq_total += c_eq;
+      sel_total += c_gt + take;
+    }
+    __syncthreads();   // wave_cnt is rewritten by the next round
+    int pos = pos_base + sel_before;
+    int eq_rank = eq_base + eq_before;
 #pragma unroll
     for (int e = 0; e < kEpt; ++e) {
+      const int j = elem_pos(r * kRound, e);
       const uint32_t u = v[e] & 0x7FFFFFFFu;
-      const bool ok = j0 + e < P;
-      bool keep = ok && (u > thr);
-      if (ok && u == thr && eq_left > 0) {
-        keep = true;
-        --eq_left;
-      }
-      if (keep && pos < k) put(pos++, j0 + e);   // bound holds for finite scores; guards NaN
+      const bool ok = j < P;
+      const bool gt = ok && u > thr, eq = ok && u == thr;
+      const unsigned long long m_gt = __ballot(gt), m_eq = __ballot(eq);
+      if ((m_gt | m_eq) == 0ull) continue;   // nothing kept at this e (uniform; most e)
+      const bool keep = gt || (eq && eq_rank + lanes_below(m_eq) < remain);
+      const unsigned long long m_keep = __ballot(keep);
+      const int my_pos = pos + lanes_below(m_keep);
+      if (keep && my_pos < k) put(my_pos, j);   // bound holds for finite scores; guards NaN
+      pos += __popcll(m_keep);
+      eq_rank += __popcll(m_eq);
     }
     eq_base += eq_total;
     pos_base += sel_total;
