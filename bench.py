@@ -207,8 +207,8 @@ def bench_offline(dev, C, wl, torch, np):
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=30)
     ap.add_argument("--workload", default="llama32",
                     help="tiny | llama1 | llama32 | qwen128k | ragged8")
     ap.add_argument("--layers", type=int, default=0, help="limit the layer count (0: all)")
