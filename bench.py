@@ -157,7 +157,12 @@ def bench_offline(dev, C, wl, torch, np):
     gen = torch.full((S, N), 40000, device=dev, dtype=torch.int32)
     for s in range(S):
         gen[s, ::2] = ctx[s, spans[s, 0]]
-    ms = _time_ms(torch, lambda: C.srh_scores(attn, gen, ctx, spans))
+    # inputs resident on the device before the timed calls (the convenience
+    # wrapper would copy the spans from the host on every call)
+    sp, spans_np = C.srh_problem(attn, spans)
+    spans_dev = torch.from_numpy(spans_np).to(dev)
+    srh_out = torch.empty(H, dtype=torch.float32, device=dev)
+    ms = _time_ms(torch, lambda: C.compresskv_srh_scores(sp, attn, gen, ctx, spans_dev, srh_out))
     hit_bytes = S * (N // 2) * H * span * 4
     print(json.dumps({"metric": "SRH score (equation 1)", "workload":
                       f"{S} samples x {N} steps, {H} heads, context {Lc}, span {span}",
@@ -179,7 +184,12 @@ def bench_offline(dev, C, wl, torch, np):
     cu = torch.from_numpy(cu_host).to(dev)
     p = C.Problem(torch.zeros((1, 1, Hq, D), dtype=bf, device=dev), k, v, cu,
                   cu_seqlens_host=cu_host, pool_kernel=1)
-    ms = _time_ms(torch, lambda: C.layer_error(p, q_dec, k, v, k_out, v_out, w_o))
+    e = C.CkvErrorProblem(n_steps=T, d_model=dm, budget=B, eps=1e-6)
+    err_ws = torch.empty(C.compresskv_layer_error_workspace_bytes(p, e), dtype=torch.uint8,
+                         device=dev)
+    err = torch.empty(1, dtype=torch.float32, device=dev)
+    ms = _time_ms(torch, lambda: C.compresskv_layer_error(p, e, q_dec, k, v, k_out, v_out, w_o,
+                                                          err, err_ws))
     nbytes = 2 * L * Hkv * D * 2 + 2 * Hkv * B * D * 2 + dm * Hq * D * 2 + T * Hq * D * 2
     print(json.dumps({"metric": "layer eviction error (equations 2-4)", "workload":
                       f"L={L}, {Hq}q/{Hkv}kv heads, D={D}, bf16, {T} steps, budget {B}, "

@@ -20,32 +20,87 @@ struct SrhArgs {
   int32_t S, N, H, L;
 };
 
-// One wave per head; a workgroup of 4 waves covers 4 consecutive heads.  Per
-// (sample, step) the wave tests whether the generated token is one of the
-// span's tokens and, if so, sums the head's weights over the span (lanes over
-// positions, then a fixed butterfly); the step sums accumulate in fp64.
-__global__ __launch_bounds__(256) void srh_score_kernel(const SrhArgs a) {
+constexpr int kSrhHeads = 4;        // heads per workgroup
+constexpr int kSrhSplit = 4;        // waves per head
+constexpr int kSrhBatch = 8;        // answer steps whose span loads a wave issues together
+constexpr int kSrhPairs = 2048;     // (sample, step) pairs tested per pass
+
+// A workgroup of 16 waves covers 4 consecutive heads.  Per block of (sample,
+// step) pairs it first records in LDS whether each step generated one of its
+// span's tokens (one thread per pair, looping over the span); the four
+// waves of a head then take every fourth answer step of the block, load
+// kSrhBatch spans together, sum each over the span (lanes over positions,
+// then a fixed butterfly) and accumulate the step sums in fp64 in step
+// order.  The four waves' totals are added in wave order, so the result does
+// not depend on scheduling.
+__global__ __launch_bounds__(64 * kSrhHeads * kSrhSplit) void srh_score_kernel(const SrhArgs a) {
+  constexpr int NW = kSrhHeads * kSrhSplit;
+  __shared__ unsigned char hit_s[kSrhPairs];
+  __shared__ double part_s[NW];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int h = blockIdx.x * 4 + wave;
-  if (h >= a.H) return;   // whole waves; the kernel has no barrier
+  const int h = blockIdx.x * kSrhHeads + wave / kSrhSplit, sub = wave % kSrhSplit;
+  const int SN = a.S * a.N;
   double acc = 0.0;
-  for (int s = 0; s < a.S; ++s) {
-    const int a0 = a.spans[2 * s], n = a.spans[2 * s + 1];
-    const int32_t *span_tok = a.ctx + (int64_t)s * a.L + a0;
-    for (int t = 0; t < a.N; ++t) {
-      const int32_t y = a.gen[(int64_t)s * a.N + t];
+  for (int p0 = 0; p0 < SN; p0 += kSrhPairs) {
+    const int np = min(kSrhPairs, SN - p0);
+    for (int q = (int)threadIdx.x; q < np; q += 64 * NW) {
+      const int p = p0 + q, s = p / a.N;
+      const int a0 = a.spans[2 * s], n = a.spans[2 * s + 1];
+      const int32_t y = a.gen[p];
+      const int32_t *tok = a.ctx + (int64_t)s * a.L + a0;
       bool hit = false;
-      for (int j = lane; j < n; j += 64) hit |= (span_tok[j] == y);
-      if (!__any(hit)) continue;   // uniform over the wave
-      const float *row = a.attn + (((int64_t)s * a.N + t) * a.H + h) * (int64_t)a.L + a0;
-      float v = 0.f;
-      for (int j = lane; j < n; j += 64) v += row[j];
-#pragma unroll
-      for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
-      acc += (double)v;
+      for (int j = 0; j < n; ++j) hit |= (tok[j] == y);
+      hit_s[q] = hit ? 1 : 0;
     }
+    __syncthreads();
+    if (h < a.H) {
+      int q = sub;
+      for (;;) {
+        // the wave's next kSrhBatch answer steps of the block (uniform)
+        int qb[kSrhBatch], nb = 0;
+        while (nb < kSrhBatch && q < np) {
+          if (hit_s[q]) qb[nb++] = q;
+          q += kSrhSplit;
+        }
+        if (nb == 0) break;
+        const float *row[kSrhBatch];
+        int len[kSrhBatch], nmax = 0;
+#pragma unroll
+        for (int b = 0; b < kSrhBatch; ++b) {
+          const int p = p0 + (b < nb ? qb[b] : qb[0]), s = p / a.N;
+          const int a0 = a.spans[2 * s];
+          len[b] = b < nb ? a.spans[2 * s + 1] : 0;
+          row[b] = a.attn + ((int64_t)p * a.H + h) * (int64_t)a.L + a0;
+          nmax = max(nmax, len[b]);
+        }
+        float v[kSrhBatch];
+#pragma unroll
+        for (int b = 0; b < kSrhBatch; ++b) v[b] = 0.f;
+        for (int j = lane; j < nmax; j += 64) {
+          float x[kSrhBatch];
+#pragma unroll
+          for (int b = 0; b < kSrhBatch; ++b) x[b] = (j < len[b]) ? row[b][j] : 0.f;
+#pragma unroll
+          for (int b = 0; b < kSrhBatch; ++b) v[b] += x[b];
+        }
+#pragma unroll
+        for (int b = 0; b < kSrhBatch; ++b) {
+#pragma unroll
+          for (int o = 32; o >= 1; o >>= 1) v[b] += __shfl_xor(v[b], o);
+          if (b < nb) acc += (double)v[b];
+        }
+      }
+    }
+    __syncthreads();   // hit_s is rewritten by the next block
   }
-  if (lane == 0) a.scores[h] = (float)acc;
+  if (lane == 0) part_s[wave] = acc;
+  __syncthreads();
+  if (sub == 0 && lane == 0 && h < a.H) {
+    double t = 0.0;
+#pragma unroll
+    for (int w = 0; w < kSrhSplit; ++w) t += part_s[wave + w];
+    a.scores[h] = (float)t;
+  }
 }
 
 // One workgroup per layer, one thread per head: a head's rank is the number of
@@ -93,8 +148,8 @@ int compresskv_srh_scores(const ckv_srh_problem *p, const float *attn, const int
   }
   ckv::SrhArgs a{attn, gen_tokens, ctx_tokens, spans, scores,
                  p->n_samples, p->n_steps, p->n_heads, p->ctx_len};
-  hipLaunchKernelGGL(ckv::srh_score_kernel, dim3((p->n_heads + 3) / 4), dim3(256), 0,
-                     (hipStream_t)stream, a);
+  hipLaunchKernelGGL(ckv::srh_score_kernel, dim3((p->n_heads + ckv::kSrhHeads - 1) / ckv::kSrhHeads),
+                     dim3(64 * ckv::kSrhHeads * ckv::kSrhSplit), 0, (hipStream_t)stream, a);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess)
     return fail(CKV_HIP_ERROR, "srh score launch failed: %s", hipGetErrorString(e));
