@@ -127,18 +127,37 @@ __global__ __launch_bounds__(256) void dec_attn_kernel(const DecArgs a) {
 #pragma unroll
     for (int d = 0; d < 4; ++d) acc[i][d] = 0.f;
 
-  for (int k0 = c0; k0 < c_end; k0 += kDecSub) {
-    // S: logits of the step's key tiles (kDecSub / 64 per wave), in log2 units
+  // The K fragments and V rows of a step are loaded into registers one step
+  // ahead: the next step's loads are in flight during this step's softmax and
+  // P.V.
+  constexpr int KT = kDecSub / 64;                   // key tiles per wave and step
+  constexpr int V4 = D * (int)sizeof(T) / 16;        // 16-byte units per V row
+  constexpr int VPT = kDecSub * V4 / 256;            // V units per thread and step
+  static_assert(kDecSub * V4 % 256 == 0, "V units");
+  uint4 kf[KT][NS], vr[VPT];
+  auto issue = [&](int k0) {
 #pragma unroll
-    for (int i = 0; i < kDecSub / 64; ++i) {
-      const int e = wave + 4 * i;
-      const int key = min(k0 + 16 * e + c, cc.n_keys - 1);
-      uint4 kf[NS];
+    for (int i = 0; i < KT; ++i) {
+      const int key = min(k0 + 16 * (wave + 4 * i) + c, cc.n_keys - 1);
       const gptr<const char> p = to_global(cc.kb) + key * cc.k_row + 16 * quad;
 #pragma unroll
-      for (int s = 0; s < NS; ++s) kf[s] = load16(p + 64 * s);
+      for (int s = 0; s < NS; ++s) kf[i][s] = load16(p + 64 * s);
+    }
+#pragma unroll
+    for (int u = 0; u < VPT; ++u) {
+      const int idx = tid + 256 * u, j = idx / V4, uu = idx - j * V4;
+      const int key = min(k0 + j, cc.n_keys - 1);
+      vr[u] = load16(to_global(cc.vb) + key * cc.v_row + 16 * uu);
+    }
+  };
+  issue(c0);
+  for (int k0 = c0; k0 < c_end; k0 += kDecSub) {
+    // S: logits of the step's key tiles (KT per wave), in log2 units
+#pragma unroll
+    for (int i = 0; i < KT; ++i) {
+      const int e = wave + 4 * i;
       f32x4 lg[RT];
-      tile_logits_all<T, D, RT, true>(kf, qreg, q_lds, c, quad, lg);
+      tile_logits_all<T, D, RT, true>(kf[i], qreg, q_lds, c, quad, lg);
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
@@ -148,15 +167,9 @@ __global__ __launch_bounds__(256) void dec_attn_kernel(const DecArgs a) {
         }
     }
     // V rows of the step
-    {
-      constexpr int V4 = D * (int)sizeof(T) / 16;   // 16-byte units per row
-      for (int i = tid; i < kDecSub * V4; i += 256) {
-        const int j = i / V4, u = i - j * V4;
-        const int key = min(k0 + j, cc.n_keys - 1);
-        const uint4 val = load16(to_global(cc.vb) + key * cc.v_row + 16 * u);
-        vs4[i] = val;
-      }
-    }
+#pragma unroll
+    for (int u = 0; u < VPT; ++u) vs4[tid + 256 * u] = vr[u];
+    if (k0 + kDecSub < c_end) issue(k0 + kDecSub);   // uniform
     __syncthreads();
     // online softmax: four threads per row, kDecSub / 4 keys each
     {
