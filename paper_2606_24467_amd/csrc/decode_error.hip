@@ -5,7 +5,7 @@
 //
 //   dec_attn_kernel     split-K attention of every (sequence, group, cache):
 //                       the group's rows (decoding step x query head of the
-//                       group) against one 512-key chunk, QK^T on MFMA, online
+//                       group) against one 256-key chunk, QK^T on MFMA, online
 //                       softmax in LDS, P.V on the VALU; partial (max, sum, O)
 //   dec_combine_kernel  merges the chunks of every row into A (fp32)
 //   dec_proj_kernel     y = W_O x for x = A_full and A_full - A_comp on fp32
