@@ -69,7 +69,8 @@ def test_srh_scores_hand_worked(gpu):
     assert mask[0].tolist() == [1, 0]
 
 
-@pytest.mark.parametrize("S,N,H,Lc", [(3, 20, 64, 300), (2, 9, 1024, 700), (1, 1, 5, 41)])
+@pytest.mark.parametrize("S,N,H,Lc", [(3, 20, 64, 300), (2, 9, 1024, 700), (1, 1, 5, 41),
+                                      (3, 800, 6, 48)])   # last: more pairs than one LDS block
 def test_srh_scores_match_oracle(gpu, S, N, H, Lc):
     _say(f"case srh S={S} N={N} H={H} L={Lc}")
     attn, gen, ctx, spans = _calibration(S * 100 + H, S, N, H, Lc, max_span=min(40, Lc - 1))
@@ -196,3 +197,19 @@ def test_errors_to_layer_budgets(gpu):
     want = OO.allocate_budgets(OO.normalize_errors(np.array(errs_ora)), 4 * per, 32, 3 * per)
     assert got.sum() == 4 * per
     assert np.all(np.abs(got - want) <= 1)   # equal up to the rounding of nearly equal shares
+
+
+def test_offline_kernels_are_deterministic(gpu):
+    """Every sum of the SRH score and of the eviction error runs in a fixed
+    order, so repeated calls give the same bits (here with several span
+    lengths, answer steps spread over the waves of a head, and a ragged
+    error case)."""
+    attn, gen, ctx, spans = _calibration(21, 3, 40, 70, 600, max_span=150)
+    first = _run(gpu, attn, gen, ctx, spans)
+    for _ in range(3):
+        assert np.array_equal(_run(gpu, attn, gen, ctx, spans), first)
+    c = _error_case(12, lens=(2100, 900), Hq=16, Hkv=4, D=128, T=4, B=200, d_model=256,
+                    dtype=C.BF16)
+    e0 = _gpu_error(c, gpu)
+    for _ in range(3):
+        assert _gpu_error(c, gpu) == e0
