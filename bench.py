@@ -124,8 +124,17 @@ def cpu_baseline(layers, w, seconds):
             break
     group_tokens_layer = tokens_layer * w.n_kv_heads
     t_layer = t_total * group_tokens_layer / done_tokens
+    cpu_model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu_model = next((ln.split(":", 1)[1].strip() for ln in f
+                              if ln.startswith("model name")), "")
+    except OSError:
+        pass
     return {"value": tokens_layer / t_layer, "unit": "tokens/s/layer", "cores": int(threads),
-            "kind": "oracle",
+            "kind": "oracle", "blas_threads": int(threads), "host_cpus": os.cpu_count(),
+            "cpu_model": cpu_model,
+            "note": "numpy fp64; its element-wise exp and max run on one thread",
             "sample": f"{n} (layer, sequence, KV group) units from layer 0 on "
                       f"({done_tokens} group-tokens, {done_tokens / group_tokens_layer:.2f} "
                       f"layers' worth), {t_total:.1f} s of oracle time, scaled to one layer"}
