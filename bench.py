@@ -38,17 +38,17 @@ MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # dense, MI355X
 # on this GPU) + WRITE_SIZE, in separate runs (profiles/).  A figure is valid
 # only for the kernel sources it was taken with: keyed by their hash.
 MEASURED_TRAFFIC = {
-    ("llama32", 32, "699bf5ffab9f8267"): (2 * (1080720.0 + 1168704.6) + 6248.0 + 33069.2) * 1024,
+    ("llama32", 32, "b44e85fa86dcbab4"): (2 * (1080865.7 + 1168537.7) + 6248.0 + 33069.2) * 1024,
 }
 
 # MFMA work the score phase executes, from rocprofv3 on the same sources:
 # SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 FLOP of both kernels, and each kernel's
 # SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 XCDs x 1024 SIMDs).
 MEASURED_MFMA = {
-    ("llama32", 32, "699bf5ffab9f8267"): {
+    ("llama32", 32, "b44e85fa86dcbab4"): {
         "executed_flops_per_launch": (275251200 + 290304000) * 512,
-        "busy_frac": {"stats_kernel": 137625600 / (6219681.6 / 8 * 1024),
-                      "colsum_kernel": 145152000 / (7663306.8 / 8 * 1024)}},
+        "busy_frac": {"stats_kernel": 137625600 / (6572285.6 / 8 * 1024),
+                      "colsum_kernel": 145152000 / (7954866.6 / 8 * 1024)}},
 }
 
 

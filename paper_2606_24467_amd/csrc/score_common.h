@@ -121,7 +121,11 @@ __device__ __forceinline__ f32x4 tile_logits(const uint4 (&kf)[Slices<T, D>::n],
 // accumulation chains are independent, so the matrix pipeline interleaves
 // them instead of waiting on one chain at a time.  Each tile accumulates its
 // slices in the same order as tile_logits.
-template <typename T, int D, int RT, bool KEYS_AS_A, bool QR = true>
+// SB (slice barrier): no instruction moves across the end of a slice, so only
+// one slice's query fragments are read ahead from LDS at a time; kernels
+// compiled for many row tiles use it to keep their register count at two
+// waves per SIMD.
+template <typename T, int D, int RT, bool KEYS_AS_A, bool QR = true, bool SB = false>
 __device__ __forceinline__ void tile_logits_all(const uint4 (&kf)[Slices<T, D>::n],
                                                 const uint4 (&qreg)[RegTiles<T, D, RT, QR>::n]
                                                                    [Slices<T, D>::n],
@@ -142,6 +146,7 @@ __device__ __forceinline__ void tile_logits_all(const uint4 (&kf)[Slices<T, D>::
       }
       acc[rt] = KEYS_AS_A ? mfma_slice<T>(kf[s], qv, acc[rt]) : mfma_slice<T>(qv, kf[s], acc[rt]);
     }
+    if constexpr (SB && RQ < RT) __builtin_amdgcn_sched_barrier(0);
   }
 }
 

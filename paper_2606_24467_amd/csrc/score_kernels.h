@@ -92,7 +92,17 @@ __host__ __device__ inline int64_t grid_blocks(int Hkv, int nz, int lead, int cp
 // ---------------------------------------------------------------------------
 constexpr int kStatsWaves = 4;
 
-template <typename T, int D, int RT>
+// Kernels compiled for 8 or more row tiles read the query fragments one slice
+// at a time (see tile_logits_all): without it they need about 296 VGPRs and
+// run one wave per SIMD.  Where a row is 4 or more slices per lane, the
+// statistics kernel is also held to three waves per SIMD (a few spilled
+// registers); kernels for fewer row tiles are faster without either.
+template <int RTM>
+constexpr bool kSliceBarrier = RTM >= 8;
+template <typename T, int D, int RTM>
+constexpr int kStatsMinWaves = RTM >= 8 && Slices<T, D>::n >= 4 ? 3 : 1;
+
+template <typename T, int D, int RT, bool SB>
 __device__ __forceinline__ void stats_body(const ScoreArgs &a, const Work &w, uint4 *q_lds,
                                            float2 (*part)[16 * 12]) {
   constexpr int NW = kStatsWaves;
@@ -135,7 +145,7 @@ __device__ __forceinline__ void stats_body(const ScoreArgs &a, const Work &w, ui
   }
   auto consume = [&](const uint4 (&kf)[NS], int i) {
     f32x4 acc[RT];
-    tile_logits_all<T, D, RT, true>(kf, qreg, q_lds, c, quad, acc);
+    tile_logits_all<T, D, RT, true, true, SB>(kf, qreg, q_lds, c, quad, acc);
     stats_update<RT>(a, acc, ref, sum, ready, c0 + 16 * (wave + NW * i), L, P, c, quad);
   };
   // The chunk's partial: merge the four quads (same row c, different keys),
@@ -181,7 +191,8 @@ __device__ __forceinline__ void stats_body(const ScoreArgs &a, const Work &w, ui
 }
 
 template <typename T, int D, int RTM, bool ML>
-__global__ __launch_bounds__(64 * kStatsWaves) void stats_kernel(const ScoreArgs a) {
+__global__ __launch_bounds__(64 * kStatsWaves)
+__attribute__((amdgpu_waves_per_eu(kStatsMinWaves<T, D, RTM>))) void stats_kernel(const ScoreArgs a) {
   const BlockRange r = block_range(a, a.lead1, a.cpw1, a.max_chunks1);
   Work w;
   w.g = r.g;
@@ -206,7 +217,7 @@ __global__ __launch_bounds__(64 * kStatsWaves) void stats_kernel(const ScoreArgs
 
   __shared__ uint4 q_lds[RTM * 16 * QLayout<T, D>::STRIDE];
   __shared__ float2 part[kStatsWaves][16 * 12];
-  dispatch_rt<RTM>(w.rt_n, [&]<int RT>() { stats_body<T, D, RT>(a, w, q_lds, part); });
+  dispatch_rt<RTM>(w.rt_n, [&]<int RT>() { stats_body<T, D, RT, kSliceBarrier<RTM>>(a, w, q_lds, part); });
 }
 
 // ---------------------------------------------------------------------------
@@ -224,7 +235,7 @@ __global__ __launch_bounds__(64 * kStatsWaves) void stats_kernel(const ScoreArgs
 // waves per SIMD); four slots measured slower (268 VGPRs, one wave).
 constexpr int kRingCs = 2;
 
-template <typename T, int D, int RT, int CSW>
+template <typename T, int D, int RT, int CSW, bool SB>
 __device__ __forceinline__ void colsum_body(const ScoreArgs &a, const Work &w, uint4 *q_lds,
                                             float *bias_s, float (*cs)[CSW], float *stage,
                                             int *hist_s) {
@@ -297,14 +308,14 @@ __device__ __forceinline__ void colsum_body(const ScoreArgs &a, const Work &w, u
   };
   // slot r of the ring holds the tiles i with i % kRingCs == r
   f32x4 lg[RT];
-  tile_logits_all<T, D, RT, false>(kr[0], qreg, q_lds, c, quad, lg);
+  tile_logits_all<T, D, RT, false, true, SB>(kr[0], qreg, q_lds, c, quad, lg);
   load_k_row<T, D>(a, w.kbase, s0, key_of(kRingCs), g, quad, kr[0]);
   for (int i = 0; i < n_tiles; i += kRingCs) {
 #pragma unroll
     for (int r = 0; r < kRingCs; ++r) {
       const int rn = (r + 1) % kRingCs;   // slot of tile i + r + 1
       f32x4 lg_next[RT];
-      tile_logits_all<T, D, RT, false>(kr[rn], qreg, q_lds, c, quad, lg_next);
+      tile_logits_all<T, D, RT, false, true, SB>(kr[rn], qreg, q_lds, c, quad, lg_next);
       load_k_row<T, D>(a, w.kbase, s0, key_of(i + r + 1 + kRingCs), g, quad, kr[rn]);
       finish_tile(lg, i + r);
 #pragma unroll
@@ -352,7 +363,8 @@ __global__ __launch_bounds__(64 * kWaves) void colsum_kernel(const ScoreArgs a) 
   __shared__ float stage[kStage > 0 ? kStage : 1];   // one chunk's pooled scores
   __shared__ int hist_s[kHistBins];
   dispatch_rt<RTM>(w.rt_n, [&]<int RT>() {
-    colsum_body<T, D, RT, CSW>(a, w, q_lds, bias_s, cs, kStage > 0 ? stage : nullptr, hist_s);
+    colsum_body<T, D, RT, CSW, kSliceBarrier<RTM>>(a, w, q_lds, bias_s, cs,
+                                                  kStage > 0 ? stage : nullptr, hist_s);
   });
 }
 
