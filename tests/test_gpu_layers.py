@@ -175,3 +175,32 @@ def test_full_stack_other_shapes(gpu, scoring_path, name, sampled):
                              H.raw_bits(kos[l]), H.raw_bits(vos[l]))
         _check_needles(x, budgets[l], idxs[l].cpu().numpy())
         _say(f"  layer {l} matches the oracle, boundary swaps {swaps}")
+
+
+def test_many_layers_short_sequences(gpu, scoring_path):
+    """32 layers x 8 sequences of 2000-3000 tokens: enough units for
+    several chunks per workgroup, but fewer chunks per sequence than the
+    one-chunk tail, so every chunk goes one per workgroup in its own order;
+    bit-identical to per-layer calls, two layers against the oracle."""
+    w = wl.get("ragged8", ragged=(2000, 3000), n_needle=4)
+    layers = [wl.make_layer_device(w, l, 0, gpu) for l in range(w.n_layers)]
+    _say(f"case many short sequences, lengths {np.diff(layers[0]['cu_seqlens_host']).tolist()}")
+    q = [d["q_win"] for d in layers]
+    k = [d["k"] for d in layers]
+    v = [d["v"] for d in layers]
+    cu, cu_host = layers[0]["cu_seqlens"], layers[0]["cu_seqlens_host"]
+    ps = [_problem(q[l], k[l], v[l], cu, cu_host, w) for l in range(w.n_layers)]
+    masks = np.stack([d["srh_mask"] for d in layers])
+    budgets = [d["budget"] for d in layers]
+    idxs, kos, vos, scores = C.compress_layers(ps[0], q, k, v, masks, budgets, want_scores=True)
+    ref = _per_layer(ps, q, k, v, masks, budgets)
+    torch.cuda.synchronize()
+    for l in range(w.n_layers):
+        for got, want in zip((idxs[l], kos[l], vos[l], scores[l]), ref[l]):
+            assert torch.equal(got, want), f"layer {l} differs from the per-layer call"
+    del ref
+    for l in (0, 31):
+        x = _host_inputs(w, l, layers[l])
+        swaps = _check_layer(x, budgets[l], scores[l].cpu().numpy(), idxs[l].cpu().numpy(),
+                             H.raw_bits(kos[l]), H.raw_bits(vos[l]))
+        _say(f"  layer {l} matches the oracle, boundary swaps {swaps}")
