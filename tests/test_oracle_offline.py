@@ -208,6 +208,10 @@ def test_layer_error_invariants():
 def test_budget_hand_worked_example():
     g = _golden("budget_worked.txt")
     e = np.array([float(x) for x in g["errors"][0]])
+    # equation 4's normalisation: each error over the sum of all of them
+    want = [Fraction(x) for x in g["normalised"][0]]
+    got_n = OO.normalize_errors(e)
+    assert np.allclose(got_n, [float(x) for x in want], rtol=0, atol=1e-15)
     got = OO.allocate_budgets(OO.normalize_errors(e), int(g["total"][0][0]),
                               int(g["min"][0][0]), int(g["max"][0][0]))
     assert got.tolist() == [int(x) for x in g["budgets"][0]]
@@ -227,6 +231,21 @@ def test_budget_closed_forms():
     # total at the bounds
     assert OO.allocate_budgets(np.array([0.7, 0.2, 0.1]), 3 * 32, 32, 96).tolist() == [32] * 3
     assert OO.allocate_budgets(np.array([0.7, 0.2, 0.1]), 3 * 96, 32, 96).tolist() == [96] * 3
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_normalised_errors_are_shares(seed):
+    """e~ is a distribution over the layers: non-negative, summing to one, in
+    the same ratios as e (exactly, for integer errors, via fractions)."""
+    rng = np.random.default_rng(100 + seed)
+    e = rng.integers(1, 1000, size=int(rng.integers(2, 40))).astype(np.float64)
+    got = OO.normalize_errors(e)
+    assert abs(got.sum() - 1.0) < 1e-12 and np.all(got >= 0)
+    tot = sum(Fraction(int(x)) for x in e)
+    for x, y in zip(e, got):
+        assert abs(Fraction(int(x)) / tot - Fraction(float(y))) < Fraction(1, 10**14)
+    # scaling every error leaves the shares unchanged
+    np.testing.assert_allclose(OO.normalize_errors(7.5 * e), got, rtol=1e-14)
 
 
 @pytest.mark.parametrize("seed", range(6))

@@ -113,8 +113,17 @@ def _budget_remainder_to_first(e_norm, total, m, M_):
     return out
 
 
+def _normalise_by_max(e):
+    e = np.asarray(e, dtype=np.float64)
+    return e / e.max()                                                  # largest error -> 1
+
+
+def _normalise_identity(e):
+    return np.asarray(e, dtype=np.float64)                              # no normalisation
+
+
 _orig = {n: getattr(M, n) for n in ("srh_scores", "select_srh", "decode_attention", "layer_error",
-                                    "allocate_budgets")}
+                                    "allocate_budgets", "normalize_errors")}
 
 MUTANTS = {
     "every step counted": ("srh_scores", _srh_all_steps),
@@ -128,6 +137,8 @@ MUTANTS = {
     "cap excess dropped": ("allocate_budgets", _budget_clamp_only),
     "shares of the total, not of the rest": ("allocate_budgets", _budget_share_of_total),
     "rounding units to the lowest layers": ("allocate_budgets", _budget_remainder_to_first),
+    "errors normalised by their maximum": ("normalize_errors", _normalise_by_max),
+    "errors not normalised": ("normalize_errors", _normalise_identity),
 }
 
 PINS = [
@@ -141,6 +152,7 @@ PINS = [
     pins.test_layer_error_invariants,
     pins.test_budget_hand_worked_example,
     pins.test_budget_closed_forms,
+    lambda: [pins.test_normalised_errors_are_shares(s) for s in range(4)],
     lambda: [pins.test_budget_invariants(s) for s in range(6)],
 ]
 
