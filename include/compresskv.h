@@ -72,6 +72,13 @@ extern "C" {
                                  (each against its own group's keys), kept by every group;
                                  groups without an SRH are allowed; CKV_POOL_THEN_MEAN only */
 
+/* how S1-S4 are computed (the results agree within the scores' tolerance;
+   each choice is deterministic) */
+#define CKV_SCORE_AUTO 0     /* single pass where it applies (see compresskv_scoring_path) */
+#define CKV_SCORE_TWO_PASS 1 /* two passes over K: row statistics, then window sums */
+#define CKV_SCORE_ONE_PASS 2 /* K read once; CKV_UNSUPPORTED where it does not apply */
+#define CKV_SPIN_CATCHUP_ALL (-2) /* ckv_problem.spin_limit: see there */
+
 /* Sizes and options of one layer.  head_dim must be 64 or 128. */
 typedef struct ckv_problem {
   int32_t batch;        /* number of packed sequences, >= 1 */
@@ -86,9 +93,17 @@ typedef struct ckv_problem {
   float scale;          /* softmax scale; <= 0 selects 1/sqrt(head_dim) */
   const int32_t *cu_seqlens;      /* device [batch+1], cu[0] = 0, non-decreasing */
   const int32_t *cu_seqlens_host; /* host copy of the same offsets */
-  int64_t k_stride_tok, k_stride_head; /* elements; >= D, 16-byte aligned rows */
+  int64_t k_stride_tok, k_stride_head; /* elements; each >= D (CKV_INVALID_ARGUMENT otherwise),
+                                          multiples of 16 bytes (CKV_UNSUPPORTED otherwise) */
   int64_t v_stride_tok, v_stride_head;
   int32_t index_mode;   /* CKV_INDEX_PER_GROUP (0) or CKV_INDEX_LAYER */
+  int32_t scoring;      /* CKV_SCORE_AUTO (0), CKV_SCORE_TWO_PASS or CKV_SCORE_ONE_PASS */
+  int32_t spin_limit;   /* single pass: how many times a unit polls for its segment's row
+                           normalisers before it is left to the catch-up kernel that
+                           follows on the same stream (about 1 us per poll); -1 (or any
+                           other negative value) selects the default (64), 0 never waits,
+                           CKV_SPIN_CATCHUP_ALL leaves every unit to the catch-up kernel
+                           (to exercise that path).  Results do not depend on it. */
   int32_t reserved;     /* must be 0 */
 } ckv_problem;
 
@@ -214,12 +229,13 @@ int compresskv_compress_layer_heads(const ckv_problem *p, const void *q_win, con
 
 /*
  * Which scoring implementation compresskv_score / _compress_layer will use for
- * this problem: 2 = two passes over K (the default), 1 = single pass (each key
- * read once from HBM), used when the environment variable CKV_PATH=single is
- * set and the problem allows it (the units of every (sequence, group), 256
- * keys each, fit in half of the workgroups the device can hold at once, and
- * batch <= 64).  Negative on invalid arguments.  Queries the device
- * (occupancy), so it needs a GPU.
+ * this problem: 1 = single pass (each key read once from HBM), 2 = two passes
+ * over K.  The single pass needs bf16 inputs, CKV_INDEX_PER_GROUP, batch <= 64
+ * and at most 6 row tiles per group (ceil(W/16) * SRHs); CKV_SCORE_AUTO also
+ * needs the 256-key units of the longest sequence to number no more than the
+ * device's CUs.  The multi-layer calls make the same choice layer by layer.
+ * Negative on invalid arguments (minus the status).  With CKV_SCORE_AUTO it
+ * queries the device, so it needs a GPU.
  */
 int compresskv_scoring_path(const ckv_problem *p, const uint8_t *srh_mask_host);
 

@@ -15,7 +15,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIBDIR = os.path.join(HERE, "lib")
 LIBNAME = "libcompresskv.so"
-SOURCES = ["api.hip", "score_kernels.hip", "score_layers.hip", "fused_score.hip",
+SOURCES = ["api.hip", "score_kernels.hip", "score_layers.hip", "onepass_score.hip",
            "select_gather_kernels.hip", "offline.hip", "decode_error.hip"]
 ARCH = "gfx950"
 FLAGS = [

@@ -22,6 +22,8 @@ F32, BF16 = 0, 1
 POOL_MAX, POOL_AVG = 0, 1
 POOL_THEN_MEAN, MEAN_THEN_POOL = 0, 1
 INDEX_PER_GROUP, INDEX_LAYER = 0, 1
+SCORE_AUTO, SCORE_TWO_PASS, SCORE_ONE_PASS = 0, 1, 2
+SPIN_DEFAULT, SPIN_CATCHUP_ALL = -1, -2
 
 _INCLUDE = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
 _HEADERS = [os.path.join(_INCLUDE, h) for h in ("compresskv.h", "compresskv_offline.h")]
@@ -46,6 +48,8 @@ class CkvProblem(ctypes.Structure):
         ("v_stride_tok", ctypes.c_int64),
         ("v_stride_head", ctypes.c_int64),
         ("index_mode", ctypes.c_int32),
+        ("scoring", ctypes.c_int32),
+        ("spin_limit", ctypes.c_int32),
         ("reserved", ctypes.c_int32),
     ]
 
@@ -179,7 +183,8 @@ class Problem:
     def __init__(self, q_win: torch.Tensor, k: torch.Tensor, v: torch.Tensor,
                  cu_seqlens: torch.Tensor, *, cu_seqlens_host=None, pool_kernel: int = 7,
                  pool_type: int = POOL_MAX, reduce_order: int = POOL_THEN_MEAN,
-                 scale: float | None = None, index_mode: int = INDEX_PER_GROUP):
+                 scale: float | None = None, index_mode: int = INDEX_PER_GROUP,
+                 scoring: int = SCORE_AUTO, spin_limit: int = -1):
         if q_win.dim() != 4 or k.dim() != 3 or v.dim() != 3:
             raise ValueError("q_win must be [batch, W, Hq, D], k and v [T, Hkv, D]")
         if q_win.dtype not in _DTYPES or k.dtype != q_win.dtype or v.dtype != q_win.dtype:
@@ -207,7 +212,7 @@ class Problem:
             cu_seqlens=cu_seqlens.data_ptr(), cu_seqlens_host=self._cu_host.ctypes.data,
             k_stride_tok=k.stride(0), k_stride_head=k.stride(1),
             v_stride_tok=v.stride(0), v_stride_head=v.stride(1), index_mode=index_mode,
-            reserved=0)
+            scoring=scoring, spin_limit=spin_limit, reserved=0)
 
     @property
     def lengths(self) -> np.ndarray:

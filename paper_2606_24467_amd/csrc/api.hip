@@ -29,37 +29,36 @@ struct LayerSrh {
   int nmax = 0;                // most SRHs in one group
 };
 
-// Everything derived from a validated problem.
+// Everything derived from a validated problem and its SRH masks.
 struct Plan {
   int64_t T = 0;
   int lmax = 0;
-  int n_layers = 1;    // layers of a multi-layer call (1 otherwise)
+  int n_layers = 1;    // layers of the call (1 for single-layer calls)
   int th = 0;          // row tiles per SRH
   int rt_max = 0;      // max row tiles of a group (over the layers)
+  int nmax = 0;        // most SRHs in one group (over the layers)
+  std::vector<int> rt_layer;   // max row tiles of a group, per layer
   int chunk1 = 0, max_chunks1 = 0;
   int chunk2 = 0, max_chunks2 = 0;
   int cpw1 = 1, cpw2 = 1;  // consecutive chunks per leading scoring workgroup
   int lead1 = 1, lead2 = 1;  // leading workgroups per (sequence, group) and layer
   uint32_t head_end_mask = 0;
-  // single-layer workspace: scores | stats | counters | histograms
-  // multi-layer workspace:  table | scores | stats | histograms (all per layer)
-  size_t table_off = 0, scores_off = 0, stats_off = 0, counters_off = 0, bias_off = 0,
-         hist_off = 0, total = 0;
+  // workspace: table | scores | counters (ticket, arrivals, normalisers,
+  // histograms) | partial statistics | skip list | edge window sums
+  size_t table_off = 0, scores_off = 0, counters_off = 0, arrive_off = 0, bias_off = 0,
+         hist_off = 0, stats_off = 0, skip_off = 0, edges_off = 0, total = 0;
   int64_t stats_layer = 0, hist_layer = 0;   // elements per layer
-  bool fused = false;      // single-pass scoring kernel
-  int n_units_max = 0;     // its units per (sequence, group), largest
-  int fused_grid = 0;      // its persistent workgroups
-  int n_counters = 0;      // ints zeroed before it (ticket, fallbacks, arrivals,
-                           // published normalisers, histograms)
   int max_parts = 0;       // partial-statistics slots per group in the workspace
+  // single-pass scoring
+  bool op_shape = false;   // the problem's shape allows it (its workspace is reserved)
+  int units_layer = 0;     // its units per layer
+  int ew = 0;              // window sums kept at each end of a unit
+  int n_op = 0;            // layers scored in a single pass: the first n_op table entries
+  int op_rt_max = 0, tp_rt_max = 0;   // row tiles of those layers / of the others
+  int op_grid = 0;         // persistent workgroups of the single-pass kernel
+  std::vector<int> order;  // table entry -> caller's layer (single-pass layers first)
   LayerSrh srh;            // single-layer calls
 };
-
-int env_int(const char *name, int dflt) {
-  const char *s = std::getenv(name);
-  if (!s || !*s) return dflt;
-  return std::atoi(s);
-}
 
 // Keys per workgroup: the smallest power of two >= lo such that doubling it
 // would leave fewer than `target` workgroups for one layer, capped at hi.  It
@@ -110,6 +109,10 @@ int check_problem(const ckv_problem *p) {
     return fail(CKV_INVALID_ARGUMENT, "scale must be finite");
   if (p->index_mode != CKV_INDEX_PER_GROUP && p->index_mode != CKV_INDEX_LAYER)
     return fail(CKV_INVALID_ARGUMENT, "index_mode must be CKV_INDEX_PER_GROUP or CKV_INDEX_LAYER");
+  if (p->scoring != CKV_SCORE_AUTO && p->scoring != CKV_SCORE_TWO_PASS &&
+      p->scoring != CKV_SCORE_ONE_PASS)
+    return fail(CKV_INVALID_ARGUMENT,
+                "scoring must be CKV_SCORE_AUTO, CKV_SCORE_TWO_PASS or CKV_SCORE_ONE_PASS");
   if (p->reserved != 0) return fail(CKV_INVALID_ARGUMENT, "reserved must be 0");
   if (p->index_mode == CKV_INDEX_LAYER && p->reduce_order != CKV_POOL_THEN_MEAN)
     return fail(CKV_UNSUPPORTED, "CKV_INDEX_LAYER needs reduce_order CKV_POOL_THEN_MEAN");
@@ -125,8 +128,12 @@ int check_problem(const ckv_problem *p) {
   }
   const int es = elem_size(p);
   const int64_t strides[4] = {p->k_stride_tok, p->k_stride_head, p->v_stride_tok, p->v_stride_head};
+  static const char *const names[4] = {"k_stride_tok", "k_stride_head", "v_stride_tok",
+                                       "v_stride_head"};
   for (int i = 0; i < 4; ++i) {
-    if (strides[i] < 1) return fail(CKV_INVALID_ARGUMENT, "K/V strides must be >= 1");
+    if (strides[i] < p->head_dim)
+      return fail(CKV_INVALID_ARGUMENT, "%s (%lld) must be >= head_dim (%d)", names[i],
+                  (long long)strides[i], p->head_dim);
     if ((strides[i] * es) % 16 != 0)
       return fail(CKV_UNSUPPORTED, "K/V strides must be multiples of 16 bytes");
   }
@@ -164,6 +171,7 @@ int layer_srh(const ckv_problem *p, const uint8_t *mask, int layer, LayerSrh &ls
 // Row tiles per SRH, the largest group, and the SRH-end bits of the row tiles.
 int set_row_tiles(const ckv_problem *p, int nmax, Plan &pl) {
   pl.th = (p->window + 15) / 16;
+  pl.nmax = nmax;
   pl.rt_max = nmax * pl.th;
   if (pl.rt_max > 12)
     return fail(CKV_UNSUPPORTED,
@@ -178,136 +186,168 @@ int set_row_tiles(const ckv_problem *p, int nmax, Plan &pl) {
 int check_mask(const ckv_problem *p, const uint8_t *mask, Plan &pl) {
   int st;
   if ((st = layer_srh(p, mask, 0, pl.srh))) return st;
-  return set_row_tiles(p, pl.srh.nmax, pl);
+  if ((st = set_row_tiles(p, pl.srh.nmax, pl))) return st;
+  pl.rt_layer.assign(1, pl.rt_max);
+  return CKV_OK;
 }
 
-// Units of the single-pass kernel in a sequence of L keys.
-int fused_units(int L) { return (L + ckv::fused_unit_keys() - 1) / ckv::fused_unit_keys(); }
-
-// The two-kernel path is the default.  CKV_PATH=single selects the
-// single-pass kernel where it applies: every group's units must fit in half of
-// the workgroups that can be resident at once (its progress condition is that
-// one group per concurrently running launch fits; the margin covers two
-// launches on different streams) and the batch must fit its ticket table.
-void choose_path(const ckv_problem *p, Plan &pl) {
-  pl.fused = false;
-  const char *path = std::getenv("CKV_PATH");
-  if (!path || std::string(path) != "single") return;
-  if (p->index_mode == CKV_INDEX_LAYER) return;   // its groups may have no SRH
-  if (p->batch > ckv::kFusedMaxBatch || p->dtype != CKV_BF16) return;
-  const int resident = ckv::fused_resident_workgroups(1, p->head_dim, pl.rt_max);
-  if (resident <= 0) return;
-  int nmax = 0;
-  for (int b = 0; b < p->batch; ++b)
-    nmax = std::max(nmax, fused_units(p->cu_seqlens_host[b + 1] - p->cu_seqlens_host[b]));
-  if (2 * nmax <= resident) {
-    pl.fused = true;
-    pl.n_units_max = nmax;
-    pl.fused_grid = resident;
-  }
-}
-
-// Chunk sizes of the two-kernel path: multiples of 512 keys (statistics: an
+// Chunk sizes of the two-pass kernels: multiples of 512 keys (statistics: an
 // even number of 2-tile groups for each of the 4 waves) and 992 + 32 halo keys
-// (column sums: an even number of 2-tile groups for each of the 8 waves).
+// (column sums: an even number of 2-tile groups for each of the 4 waves).
+// Both depend on the layer's shape only.
 void set_chunks(const ckv_problem *p, Plan &pl) {
   pl.T = p->cu_seqlens_host[p->batch];
   pl.lmax = 0;
   for (int b = 0; b < p->batch; ++b)
     pl.lmax = std::max(pl.lmax, p->cu_seqlens_host[b + 1] - p->cu_seqlens_host[b]);
-  int c1 = env_int("CKV_CHUNK1", 0), c2 = env_int("CKV_CHUNK2", 0);
-  if (c1 <= 0 || c1 % 512 != 0) c1 = pick_chunk(p, 512, 4096, 256);
-  if (c2 <= 0 || (c2 + 32) % 512 != 0 || c2 > ckv::kMaxChunk2) c2 = 992;   // even groups per chunk
-  pl.chunk1 = c1;
-  pl.chunk2 = c2;
-  pl.max_chunks1 = std::max(1, (pl.lmax + c1 - 1) / c1);
-  pl.max_chunks2 = std::max(1, (pl.lmax + c2 - 1) / c2);
+  pl.chunk1 = pick_chunk(p, 512, 4096, 256);
+  pl.chunk2 = 992;
+  pl.max_chunks1 = std::max(1, (pl.lmax + pl.chunk1 - 1) / pl.chunk1);
+  pl.max_chunks2 = std::max(1, (pl.lmax + pl.chunk2 - 1) / pl.chunk2);
 }
 
 // Workgroups of cpw chunks first, then at least `tail` chunks of every
 // (sequence, group) one per workgroup, so the end of each scoring grid is made
 // of short workgroups.
 void set_lead(Plan &pl, int tail1, int tail2) {
-  tail1 = env_int("CKV_TAIL1", tail1);
-  tail2 = env_int("CKV_TAIL2", tail2);
   pl.lead1 = pl.cpw1 > 1 ? std::max(0, (pl.max_chunks1 - tail1) / pl.cpw1) : pl.max_chunks1;
   pl.lead2 = pl.cpw2 > 1 ? std::max(0, (pl.max_chunks2 - tail2) / pl.cpw2) : pl.max_chunks2;
 }
 
-// The block the single-pass kernel zeroes before it runs, from `start`:
-// [0] ticket, [1] fallbacks, [64 ..) arrivals per (layer, group), then the
-// published (normaliser, marker) pairs per (layer, group, row slot), then the
-// first-digit histograms per (layer, group) (also used by the two-pass path).
-void set_counters(const ckv_problem *p, Plan &pl, size_t start, int n_layers) {
-  const size_t lg = (size_t)p->batch * p->n_kv_heads * n_layers;
-  pl.counters_off = start;
-  pl.bias_off = start + round_up((64 + lg) * sizeof(int), 256);
-  pl.hist_off = pl.bias_off + round_up(lg * pl.rt_max * 16 * sizeof(float2), 256);
-  pl.n_counters = (int)((pl.hist_off - pl.counters_off) / sizeof(int) + lg * ckv::kHistBins);
-  pl.total = pl.hist_off + round_up(lg * ckv::kHistBins * sizeof(int), 256);
+// Units of the single-pass kernel in a sequence of L keys.
+int op_units(int L) { return (L + ckv::kOnePassUnitKeys - 1) / ckv::kOnePassUnitKeys; }
+
+// Row tiles a layer may have to be scored in a single pass.
+constexpr int kOnePassMaxRowTiles = 6;
+// Polls of a late normaliser before a unit is left to the catch-up kernel.
+constexpr int kDefaultSpinLimit = 64;
+
+// Whether the problem's shape allows single-pass scoring at all (bf16 keys,
+// per-group selections, a batch that fits the kernel's ticket table); the
+// workspace of such problems always has room for it.
+bool op_shape(const ckv_problem *p) {
+  return p->scoring != CKV_SCORE_TWO_PASS && p->dtype == CKV_BF16 &&
+         p->index_mode == CKV_INDEX_PER_GROUP && p->batch <= ckv::kOnePassMaxBatch;
 }
 
-// Partial-statistics slots per group: enough for either path's chunking.
-int partial_slots(const Plan &pl) {
-  int parts = pl.max_chunks1;
-  parts = std::max(parts, fused_units(pl.lmax));
-  return parts;
+// CUs of the current device (0 if the query fails).
+int device_cus() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return 0;
+  return cus;
 }
 
-// Single-layer workspace: a one-entry layer table (for the single-pass
-// kernel), scores, partial row statistics, then the counters block.
-void make_plan(const ckv_problem *p, Plan &pl, bool decide_path) {
-  set_chunks(p, pl);
-  set_lead(pl, 0, 0);
-  pl.n_layers = 1;
-  if (decide_path) choose_path(p, pl);
-  pl.max_parts = partial_slots(pl);
+// Which layers are scored in a single pass, and the table order (those
+// layers first).  A layer qualifies if its groups have at most 6 row tiles;
+// CKV_SCORE_AUTO also needs every segment's units to fit in one round of the
+// persistent workgroups (one per CU), so that a segment's units are in flight
+// together; CKV_SCORE_ONE_PASS asks for it on every layer (CKV_UNSUPPORTED
+// where a layer does not qualify).  The choice for a layer depends only on the
+// problem and that layer's masks, so multi-layer calls score every layer as
+// the single-layer call would.
+int choose_paths(const ckv_problem *p, Plan &pl) {
+  const int n = pl.n_layers;
+  std::vector<uint8_t> op(n, 0);
+  pl.op_grid = 0;
+  if (pl.op_shape) {
+    bool fits = true;
+    if (p->scoring == CKV_SCORE_AUTO) {
+      pl.op_grid = device_cus();
+      fits = pl.op_grid > 0 && op_units(pl.lmax) <= pl.op_grid;
+    }
+    for (int l = 0; l < n; ++l) op[l] = fits && pl.rt_layer[l] <= kOnePassMaxRowTiles;
+  }
+  if (p->scoring == CKV_SCORE_ONE_PASS) {
+    if (!pl.op_shape)
+      return fail(CKV_UNSUPPORTED, "single-pass scoring needs bf16 inputs, CKV_INDEX_PER_GROUP "
+                                   "and batch <= %d", ckv::kOnePassMaxBatch);
+    for (int l = 0; l < n; ++l)
+      if (!op[l])
+        return fail(CKV_UNSUPPORTED, "layer %d: single-pass scoring needs at most %d row tiles "
+                                     "per group (ceil(W/16) * SRHs)", l, kOnePassMaxRowTiles);
+  }
+  pl.order.clear();
+  pl.n_op = 0;
+  pl.op_rt_max = pl.tp_rt_max = 0;
+  for (int l = 0; l < n; ++l)
+    if (op[l]) {
+      pl.order.push_back(l);
+      pl.op_rt_max = std::max(pl.op_rt_max, pl.rt_layer[l]);
+    }
+  pl.n_op = (int)pl.order.size();
+  for (int l = 0; l < n; ++l)
+    if (!op[l]) {
+      pl.order.push_back(l);
+      pl.tp_rt_max = std::max(pl.tp_rt_max, pl.rt_layer[l]);
+    }
+  if (pl.n_op > 0 && pl.op_grid == 0) pl.op_grid = device_cus();
+  if (pl.n_op > 0 && pl.op_grid == 0)
+    return fail(CKV_HIP_ERROR, "no HIP device for the single-pass kernel");
+  return CKV_OK;
+}
+
+// Workspace layout (see Plan).  The counters block and the partial statistics
+// of the single-pass layers are contiguous: the single-pass launch zeroes them.
+void set_layout(const ckv_problem *p, Plan &pl) {
+  const int n = pl.n_layers;
   const size_t groups = (size_t)p->batch * p->n_kv_heads;
+  const size_t lg = groups * n;
+  pl.op_shape = op_shape(p);
+  pl.units_layer = 0;
+  for (int b = 0; b < p->batch; ++b)
+    pl.units_layer += p->n_kv_heads * op_units(p->cu_seqlens_host[b + 1] - p->cu_seqlens_host[b]);
+  pl.ew = p->pool_kernel - 1;
+  pl.max_parts = pl.max_chunks1;
+  if (pl.op_shape) pl.max_parts = std::max(pl.max_parts, op_units(pl.lmax));
+  const int row_slots = pl.rt_max * 16;
+  pl.stats_layer = (int64_t)(groups * pl.max_parts * (size_t)row_slots);
+  pl.hist_layer = (int64_t)(groups * ckv::kHistBins);
   pl.table_off = 0;
-  pl.scores_off = round_up(sizeof(ckv::LayerDesc), 256);
-  pl.stats_off =
-      pl.scores_off + round_up((size_t)p->n_kv_heads * pl.T * sizeof(float), 256);
-  set_counters(p, pl,
-               pl.stats_off +
-                   round_up(groups * pl.max_parts * (size_t)pl.rt_max * 16 * sizeof(float2), 256),
-               1);
-  pl.stats_layer = 0;
-  pl.hist_layer = 0;
+  pl.scores_off = round_up((size_t)n * sizeof(ckv::LayerDesc), 256);
+  pl.counters_off = pl.scores_off + round_up((size_t)n * p->n_kv_heads * pl.T * sizeof(float), 256);
+  pl.arrive_off = pl.counters_off + 256;
+  pl.bias_off = pl.arrive_off + round_up(lg * sizeof(int), 256);
+  pl.hist_off = pl.bias_off + round_up(lg * row_slots * sizeof(float2), 256);
+  pl.stats_off = pl.hist_off + round_up(lg * ckv::kHistBins * sizeof(int), 256);
+  pl.skip_off = pl.stats_off + round_up((size_t)n * pl.stats_layer * sizeof(float2), 256);
+  pl.edges_off = pl.skip_off;
+  pl.total = pl.skip_off;
+  if (pl.op_shape) {
+    const size_t units = (size_t)n * pl.units_layer;
+    pl.edges_off = pl.skip_off + round_up(units * sizeof(int), 256);
+    pl.total = pl.edges_off +
+               round_up(units * (size_t)pl.nmax * 2 * pl.ew * sizeof(float), 256);
+  }
 }
 
 // One-chunk workgroups at the end of the multi-layer scoring grids, per
 // (sequence, group) and layer.
 constexpr int kTail1 = 4, kTail2 = 4;
 
-// Multi-layer workspace: the layer table, then per layer the scores and the
-// partial row statistics, then the counters block (per layer inside).
-void make_plan_layers(const ckv_problem *p, int n_layers, Plan &pl, bool decide_path) {
+// The plan of a call over n_layers layers (rt_layer set): chunking, grid
+// shapes and workspace layout; with decide_path also the scoring path of
+// every layer (may query the device, may fail with CKV_UNSUPPORTED).
+int make_plan(const ckv_problem *p, int n_layers, Plan &pl, bool decide_path) {
   set_chunks(p, pl);
   pl.n_layers = n_layers;
-  // Longer workgroups once there are enough of them: a few rounds of the
-  // resident workgroups keep the tail short, and every round keeps its key
-  // stream going across chunk boundaries.
-  const int64_t units1 = (int64_t)p->batch * p->n_kv_heads * n_layers * pl.max_chunks1;
-  const int64_t units2 = (int64_t)p->batch * p->n_kv_heads * n_layers * pl.max_chunks2;
-  pl.cpw1 = (int)std::max<int64_t>(1, std::min<int64_t>(8, units1 / 3072));
-  pl.cpw2 = (int)std::max<int64_t>(1, std::min<int64_t>(8, units2 / 2048));
-  const int e1 = env_int("CKV_CPW1", 0), e2 = env_int("CKV_CPW2", 0);
-  if (e1 > 0) pl.cpw1 = std::min(e1, 64);
-  if (e2 > 0) pl.cpw2 = std::min(e2, 64);
-  set_lead(pl, kTail1, kTail2);
-  pl.fused = false;
-  if (decide_path) choose_path(p, pl);
-  pl.max_parts = partial_slots(pl);
-  const size_t groups = (size_t)p->batch * p->n_kv_heads;
-  pl.stats_layer = (int64_t)(groups * pl.max_parts * (size_t)pl.rt_max * 16);
-  pl.hist_layer = (int64_t)(groups * ckv::kHistBins);
-  pl.table_off = 0;
-  pl.scores_off = round_up((size_t)n_layers * sizeof(ckv::LayerDesc), 256);
-  pl.stats_off = pl.scores_off +
-                 round_up((size_t)n_layers * p->n_kv_heads * pl.T * sizeof(float), 256);
-  set_counters(p, pl,
-               pl.stats_off + round_up((size_t)n_layers * pl.stats_layer * sizeof(float2), 256),
-               n_layers);
+  if (n_layers > 1) {
+    // Longer workgroups once there are enough of them: a few rounds of the
+    // resident workgroups keep the tail short, and every round keeps its key
+    // stream going across chunk boundaries.
+    const int64_t units1 = (int64_t)p->batch * p->n_kv_heads * n_layers * pl.max_chunks1;
+    const int64_t units2 = (int64_t)p->batch * p->n_kv_heads * n_layers * pl.max_chunks2;
+    pl.cpw1 = (int)std::max<int64_t>(1, std::min<int64_t>(8, units1 / 3072));
+    pl.cpw2 = (int)std::max<int64_t>(1, std::min<int64_t>(8, units2 / 2048));
+    set_lead(pl, kTail1, kTail2);
+  } else {
+    pl.cpw1 = pl.cpw2 = 1;
+    set_lead(pl, 0, 0);
+  }
+  set_layout(p, pl);
+  if (!decide_path) return CKV_OK;
+  return choose_paths(p, pl);
 }
 
 // Fields of the scoring arguments shared by every layer.
@@ -327,7 +367,7 @@ ckv::ScoreArgs score_args(const ckv_problem *p, const Plan &pl, void *ws) {
   a.Hkv = p->n_kv_heads;
   a.W = p->window;
   a.th = pl.th;
-  a.row_slots = pl.rt_max * 16;
+  a.row_slots = pl.rt_max * 16;   // partial and normaliser slots per group
   a.chunk1 = pl.chunk1;
   a.max_chunks1 = pl.max_chunks1;
   a.parts_stride = pl.max_parts;   // partial slots between groups
@@ -461,16 +501,20 @@ int check_layers(const ckv_problem *p, int n_layers, const uint8_t *masks, const
   if (!masks) return fail(CKV_INVALID_ARGUMENT, "srh_masks_host is NULL");
   int nmax = 0, st;
   LayerSrh ls;
+  std::vector<int> nmax_layer(n_layers);
   if (bits) bits->assign((size_t)n_layers * (ckv::kMaxQHeads / 32), 0u);
   for (int l = 0; l < n_layers; ++l) {
     const uint8_t *m = masks + (size_t)l * p->n_q_heads;
     if ((st = layer_srh(p, m, l, ls))) return st;
     nmax = std::max(nmax, ls.nmax);
+    nmax_layer[l] = ls.nmax;
     if (bits)
       for (int h = 0; h < p->n_q_heads; ++h)
         if (m[h]) (*bits)[(size_t)l * (ckv::kMaxQHeads / 32) + h / 32] |= 1u << (h % 32);
   }
   if ((st = set_row_tiles(p, nmax, pl))) return st;
+  pl.rt_layer.resize(n_layers);
+  for (int l = 0; l < n_layers; ++l) pl.rt_layer[l] = nmax_layer[l] * pl.th;
   char name[64];
   for (int l = 0; l < n_layers; ++l) {
     if (lp.budgets) {
@@ -498,13 +542,15 @@ int check_layers(const ckv_problem *p, int n_layers, const uint8_t *masks, const
   return CKV_OK;
 }
 
-// Enqueue the table writes of a multi-layer call.
-hipError_t put_layers(const ckv_problem *p, const Plan &pl, int n_layers, const LayerPtrs &lp,
+// Enqueue the writes of the layer table: entry i describes the caller's layer
+// pl.order[i] (its scores at scores + that layer's slice).
+hipError_t put_layers(const ckv_problem *p, const Plan &pl, const LayerPtrs &lp,
                       const std::vector<uint32_t> &bits, float *scores, void *ws,
                       hipStream_t stream) {
   ckv::LayerDesc *table =
       reinterpret_cast<ckv::LayerDesc *>(static_cast<char *>(ws) + pl.table_off);
   const size_t per_layer_scores = (size_t)p->n_kv_heads * pl.T;
+  const int n_layers = pl.n_layers;
   for (int first = 0; first < n_layers; first += ckv::kPutLayers) {
     ckv::PutArgs a{};
     a.table = table;
@@ -513,7 +559,7 @@ hipError_t put_layers(const ckv_problem *p, const Plan &pl, int n_layers, const 
     a.Hq = p->n_q_heads;
     a.Hkv = p->n_kv_heads;
     for (int i = 0; i < a.count; ++i) {
-      const int l = first + i;
+      const int l = pl.order[first + i];
       ckv::PutEntry &e = a.e[i];
       e.q = lp.q ? lp.q[l] : nullptr;
       e.k = lp.k ? lp.k[l] : nullptr;
@@ -532,55 +578,68 @@ hipError_t put_layers(const ckv_problem *p, const Plan &pl, int n_layers, const 
   return hipSuccess;
 }
 
-// The single-pass kernel over n_layers layers of the table a.layers.
-hipError_t launch_fused(const ckv_problem *p, const Plan &pl, const ckv::ScoreArgs &a, void *ws,
-                        int n_layers, hipStream_t stream) {
-  ckv::FusedArgs f{};
+// The single-pass kernels over table entries 0 .. n_op - 1.
+hipError_t launch_onepass(const ckv_problem *p, const Plan &pl, const ckv::ScoreArgs &a,
+                          void *ws, hipStream_t stream) {
+  ckv::OnePassArgs f{};
   f.s = a;
-  int *ctr = reinterpret_cast<int *>(static_cast<char *>(ws) + pl.counters_off);
-  f.ticket = ctr;
-  f.fallbacks = ctr + 1;
-  f.arrive = ctr + 64;
-  f.bias = reinterpret_cast<float2 *>(static_cast<char *>(ws) + pl.bias_off);
+  char *w = static_cast<char *>(ws);
+  f.fill_base = reinterpret_cast<int *>(w + pl.counters_off);
+  f.ticket = f.fill_base;
+  f.skip_count = f.fill_base + 1;
+  f.arrive = reinterpret_cast<int *>(w + pl.arrive_off);
+  f.bias = reinterpret_cast<float2 *>(w + pl.bias_off);
+  f.skip_list = reinterpret_cast<int *>(w + pl.skip_off);
+  f.edges = reinterpret_cast<float *>(w + pl.edges_off);
   int acc = 0;
   for (int b = 0; b <= p->batch; ++b) {
     f.seq_units[b] = acc;
     if (b < p->batch)
-      acc += p->n_kv_heads * fused_units(p->cu_seqlens_host[b + 1] - p->cu_seqlens_host[b]);
+      acc += p->n_kv_heads * op_units(p->cu_seqlens_host[b + 1] - p->cu_seqlens_host[b]);
   }
   f.units_per_layer = acc;
-  f.n_units_total = acc * n_layers;
-  const int grid = std::min(pl.fused_grid, f.n_units_total);
-  return ckv::launch_fused_score(f, p->dtype == CKV_BF16, p->head_dim, pl.rt_max, pl.n_counters,
-                                 grid, stream);
+  f.n_units_total = acc * pl.n_op;
+  f.spin_limit = p->spin_limit == CKV_SPIN_CATCHUP_ALL ? -1
+                 : p->spin_limit < 0                 ? kDefaultSpinLimit
+                                                     : p->spin_limit;
+  f.ew = pl.ew;
+  f.heads_max = pl.nmax;
+  const size_t fill_end = pl.stats_off + (size_t)pl.n_op * pl.stats_layer * sizeof(float2);
+  const int64_t fill_ints = (int64_t)((fill_end - pl.counters_off) / sizeof(int));
+  return ckv::launch_onepass(f, p->head_dim, pl.op_rt_max, pl.op_grid, fill_ints, stream);
+}
+
+// The two-pass kernels over table entries n_op .. n_layers - 1.
+hipError_t launch_twopass_table(const ckv_problem *p, const Plan &pl, const ckv::ScoreArgs &a,
+                                hipStream_t stream) {
+  const int n_tp = pl.n_layers - pl.n_op;
+  if (n_tp == 0) return hipSuccess;
+  ckv::ScoreArgs b = a;
+  b.layers = a.layers + pl.n_op;
+  b.stats = a.stats + pl.n_op * a.stats_layer;
+  b.hist = a.hist + pl.n_op * a.hist_layer;
+  return ckv::launch_score_layers(b, p->dtype == CKV_BF16, p->head_dim, pl.tp_rt_max, p->batch,
+                                  n_tp, stream);
 }
 
 // S1-S4 of a single-layer call on the path the plan chose.
 hipError_t launch_scoring(const ckv_problem *p, const Plan &pl, const void *q, const void *k,
                           float *scores, void *ws, hipStream_t stream) {
   ckv::ScoreArgs a = score_args(p, pl, ws);
-  a.l0 = layer_desc(&pl.srh, q, k, nullptr, scores, nullptr, nullptr, nullptr, 0);
-  if (!pl.fused)
+  if (pl.n_op == 0) {
+    a.l0 = layer_desc(&pl.srh, q, k, nullptr, scores, nullptr, nullptr, nullptr, 0);
     return ckv::launch_score(a, p->dtype == CKV_BF16, p->head_dim, pl.rt_max, p->batch, stream);
+  }
   // the single-pass kernel reads its operands from a layer table
   LayerPtrs lp;
   lp.q = &q;
   lp.k = &k;
   std::vector<uint32_t> bits(ckv::kMaxQHeads / 32, 0u);
   for (uint8_t h : pl.srh.head) bits[h / 32] |= 1u << (h % 32);
-  hipError_t e = put_layers(p, pl, 1, lp, bits, scores, ws, stream);
+  hipError_t e = put_layers(p, pl, lp, bits, scores, ws, stream);
   if (e != hipSuccess) return e;
   a.layers = reinterpret_cast<const ckv::LayerDesc *>(static_cast<char *>(ws) + pl.table_off);
-  return launch_fused(p, pl, a, ws, 1, stream);
-}
-
-// S1-S4 of a multi-layer call on the path the plan chose.
-hipError_t launch_scoring_layers(const ckv_problem *p, const Plan &pl, const ckv::ScoreArgs &a,
-                                 void *ws, int n_layers, hipStream_t stream) {
-  if (!pl.fused)
-    return ckv::launch_score_layers(a, p->dtype == CKV_BF16, p->head_dim, pl.rt_max, p->batch,
-                                    n_layers, stream);
-  return launch_fused(p, pl, a, ws, n_layers, stream);
+  return launch_onepass(p, pl, a, ws, stream);
 }
 
 // S1-S4 (and, with budgets, S5-S6) of a multi-layer call.
@@ -593,20 +652,20 @@ int run_layers(const ckv_problem *p, int n_layers, const LayerPtrs &lp, const ui
   if ((st = check_layers(p, n_layers, masks, lp, pl, &bits))) return st;
   if (!full && (st = check_ptr(scores_or_null, "scores", 4))) return st;
   if (scores_or_null && (st = check_ptr(scores_or_null, "scores", 4))) return st;
-  make_plan_layers(p, n_layers, pl, false);
+  make_plan(p, n_layers, pl, false);
   if ((st = check_ws(pl, ws, ws_bytes))) return st;
-  make_plan_layers(p, n_layers, pl, true);
+  if ((st = make_plan(p, n_layers, pl, true))) return st;
   float *scores = scores_or_null
                       ? scores_or_null
                       : reinterpret_cast<float *>(static_cast<char *>(ws) + pl.scores_off);
   hipStream_t s = (hipStream_t)stream;
-  if ((st = hip_status(put_layers(p, pl, n_layers, lp, bits, scores, ws, s), "layer table")))
-    return st;
+  if ((st = hip_status(put_layers(p, pl, lp, bits, scores, ws, s), "layer table"))) return st;
   const ckv::LayerDesc *table =
       reinterpret_cast<const ckv::LayerDesc *>(static_cast<char *>(ws) + pl.table_off);
   ckv::ScoreArgs a = score_args(p, pl, ws);
   a.layers = table;
-  if ((st = hip_status(launch_scoring_layers(p, pl, a, ws, n_layers, s), "score"))) return st;
+  if (pl.n_op > 0 && (st = hip_status(launch_onepass(p, pl, a, ws, s), "score"))) return st;
+  if ((st = hip_status(launch_twopass_table(p, pl, a, s), "score"))) return st;
   if ((st = hip_status(launch_combine_if_shared(p, pl, nullptr, nullptr, table, n_layers, s),
                        "combine")))
     return st;
@@ -670,16 +729,16 @@ int compresskv_scoring_path(const ckv_problem *p, const uint8_t *srh_mask_host) 
   int st;
   if ((st = check_problem(p))) return -st;
   if ((st = check_mask(p, srh_mask_host, pl))) return -st;
-  make_plan(p, pl, true);
+  if ((st = make_plan(p, 1, pl, true))) return -st;
   ok();
-  return pl.fused ? 1 : 2;
+  return pl.n_op > 0 ? 1 : 2;
 }
 
 size_t compresskv_workspace_bytes(const ckv_problem *p, const uint8_t *srh_mask_host,
                                   int32_t budget) {
   Plan pl;
   if (check_problem(p) || check_mask(p, srh_mask_host, pl) || check_budget(p, budget)) return 0;
-  make_plan(p, pl, false);
+  make_plan(p, 1, pl, false);
   ok();
   return pl.total;
 }
@@ -694,9 +753,9 @@ int compresskv_score(const ckv_problem *p, const void *q_win, const void *k,
   if ((st = check_ptr(q_win, "q_win", 16)) || (st = check_ptr(k, "k", 16)) ||
       (st = check_ptr(scores, "scores", 4)))
     return st;
-  make_plan(p, pl, false);
+  make_plan(p, 1, pl, false);
   if ((st = check_ws(pl, ws, ws_bytes))) return st;
-  make_plan(p, pl, true);
+  if ((st = make_plan(p, 1, pl, true))) return st;
   if ((st = hip_status(launch_scoring(p, pl, q_win, k, scores, ws, (hipStream_t)stream),
                        "score")))
     return st;
@@ -755,9 +814,9 @@ int compresskv_compress_layer(const ckv_problem *p, const void *q_win, const voi
       (st = check_ptr(k_out, "k_out", 16)) || (st = check_ptr(v_out, "v_out", 16)))
     return st;
   if (scores_or_null && (st = check_ptr(scores_or_null, "scores", 4))) return st;
-  make_plan(p, pl, false);
+  make_plan(p, 1, pl, false);
   if ((st = check_ws(pl, ws, ws_bytes))) return st;
-  make_plan(p, pl, true);
+  if ((st = make_plan(p, 1, pl, true))) return st;
   float *scores = scores_or_null
                       ? scores_or_null
                       : reinterpret_cast<float *>(static_cast<char *>(ws) + pl.scores_off);
@@ -781,7 +840,7 @@ size_t compresskv_layers_workspace_bytes(const ckv_problem *p, int32_t n_layers,
   Plan pl;
   if (check_problem(p) || check_layers(p, n_layers, srh_masks_host, LayerPtrs{}, pl, nullptr))
     return 0;
-  make_plan_layers(p, n_layers, pl, false);
+  make_plan(p, n_layers, pl, false);
   ok();
   return pl.total;
 }
@@ -871,9 +930,9 @@ int compresskv_compress_layer_heads(const ckv_problem *p, const void *q_win, con
       (st = check_ptr(k_out, "k_out", 16)) || (st = check_ptr(v_out, "v_out", 16)))
     return st;
   if (scores_or_null && (st = check_ptr(scores_or_null, "scores", 4))) return st;
-  make_plan(p, pl, false);
+  make_plan(p, 1, pl, false);
   if ((st = check_ws(pl, ws, ws_bytes))) return st;
-  make_plan(p, pl, true);
+  if ((st = make_plan(p, 1, pl, true))) return st;
   float *scores = scores_or_null
                       ? scores_or_null
                       : reinterpret_cast<float *>(static_cast<char *>(ws) + pl.scores_off);

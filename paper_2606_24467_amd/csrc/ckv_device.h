@@ -146,16 +146,25 @@ struct ScoreArgs {
   uint32_t head_end_mask;  // bit rt set if row tile rt is the last tile of an SRH
 };
 
-// Arguments of the single-pass scoring kernel (single-layer calls).
-struct FusedArgs {
-  ScoreArgs s;             // s.stats holds the published partials: [layer][group][unit][row]
-  int *ticket;             // one counter
-  int *fallbacks;          // waits that hit their bound (diagnostic)
-  int *arrive;             // [layers][batch * Hkv] units of each group that have published
-  float2 *bias;            // [layers][batch * Hkv][row_slots] (normaliser, marker) pairs
-  int n_units_total;       // units of all layers
+// Arguments of the single-pass scoring kernels (operands in the layer table:
+// the launch covers table layers 0 .. n_layers - 1).
+constexpr int kOnePassUnitKeys = 256;   // keys of one unit
+constexpr int kOnePassMaxBatch = 64;
+struct OnePassArgs {
+  ScoreArgs s;             // s.stats: unit partials [layer][group][unit][row] (max, -sum)
+  int *fill_base;          // start of the block zeroed before the launch
+  int *ticket;             // next unit to take
+  int *skip_count;         // units left to the catch-up kernel
+  int *arrive;             // [layers][batch * Hkv] units of each segment that have published
+  float2 *bias;            // [layers][batch * Hkv][row_slots] (normaliser, 1) once published
+  int *skip_list;          // [n_units_total]
+  float *edges;            // [n_units_total][heads_max][2][ew] window sums at each unit's ends
+  int n_units_total;       // units of all layers of the launch
   int units_per_layer;     // seq_units[batch]
-  int seq_units[65];       // first ticket of sequence b within a layer (group-major), b <= batch
+  int seq_units[kOnePassMaxBatch + 1];   // first ticket of sequence b within a layer
+  int spin_limit;          // polls of a late normaliser before the unit is left to catch-up
+  int ew;                  // pool_kernel - 1: window sums kept at each end of a unit
+  int heads_max;           // most SRHs in one group
 };
 
 // Per-group budgets (head-level allocation): group g keeps budget[g] rows,

@@ -19,13 +19,11 @@ hipError_t launch_combine(const CombineArgs &a, int n_layers, int lmax, hipStrea
 // Writes table entries [first, first + count) from a.e (count <= kPutLayers).
 hipError_t launch_put_layers(const PutArgs &a, hipStream_t stream);
 
-// Single-pass scoring (fused_score.hip): bf16 keys, operands in the layer table.
-struct FusedArgs;
-constexpr int kFusedMaxBatch = 64;
-hipError_t launch_fused_score(const FusedArgs &f, int dtype_bf16, int head_dim, int rt_max,
-                              int counters, int grid, hipStream_t stream);
-int fused_resident_workgroups(int dtype_bf16, int head_dim, int rt_max);
-int fused_unit_keys();
+// Single-pass scoring (onepass_score.hip): bf16 keys, operands in the layer
+// table.  Zeroes fill_ints ints from f.fill_base, then runs the main kernel on
+// `grid` persistent workgroups, the catch-up kernel and the boundary kernel.
+hipError_t launch_onepass(const OnePassArgs &f, int head_dim, int rt_max, int grid,
+                          int64_t fill_ints, hipStream_t stream);
 // max_budget: the largest budget over the layers (sizes the grid).
 hipError_t launch_gather(const GatherArgs &a, int n_layers, int max_budget, hipStream_t stream);
 

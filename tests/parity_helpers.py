@@ -21,6 +21,28 @@ from paper_2606_24467_amd import workloads as wl
 SCORE_RTOL = 2e-3
 BOUNDARY_RTOL = 1e-5
 
+# Scoring path of the problems the GPU tests build (ckv_problem.scoring); the
+# parametrised fixtures of the parity test files set it per case.
+SCORING = 0
+
+
+def problem(q, k, v, cu, *, masks=None, **kw):
+    """A C.Problem on the scoring path SCORING.  With the single pass forced,
+    a problem (or a layer mask) it does not apply to skips the case."""
+    import pytest
+    from paper_2606_24467_amd import compresskv as C
+    kw.setdefault("scoring", SCORING)
+    p = C.Problem(q, k, v, cu, **kw)
+    if masks is not None and p.c.scoring == C.SCORE_ONE_PASS:
+        for m in np.atleast_2d(np.asarray(masks)):
+            try:
+                C.compresskv_scoring_path(p, m)
+            except C.CompressKVError as e:
+                if e.status != C.UNSUPPORTED:
+                    raise
+                pytest.skip(f"the single pass does not apply: {e}")
+    return p
+
 
 def device_tensors(x: wl.LayerInputs, dev):
     """q_win, k, v, cu_seqlens as device tensors holding exactly x's values."""

@@ -102,8 +102,11 @@ INVALID = [
     ("order", dict(reduce_order=2), C.INVALID_ARGUMENT),
     ("cu null", dict(cu_seqlens=None), C.INVALID_ARGUMENT),
     ("cu misaligned", dict(cu_seqlens=FAKE + 2), C.UNSUPPORTED),
-    ("stride", dict(k_stride_tok=100), C.UNSUPPORTED),
+    ("stride not 16-byte multiple", dict(k_stride_tok=2 * 128 + 4), C.UNSUPPORTED),
     ("stride zero", dict(v_stride_head=0), C.INVALID_ARGUMENT),
+    ("head stride below head_dim", dict(k_stride_head=120), C.INVALID_ARGUMENT),
+    ("token stride below head_dim", dict(v_stride_tok=64), C.INVALID_ARGUMENT),
+    ("scoring", dict(scoring=3), C.INVALID_ARGUMENT),
     ("too many kv heads", dict(n_kv_heads=256, n_q_heads=256), C.UNSUPPORTED),
     ("index mode", dict(index_mode=2), C.INVALID_ARGUMENT),
     ("reserved", dict(reserved=1), C.INVALID_ARGUMENT),
@@ -283,3 +286,28 @@ def test_group_budget_rules(L):
     assert f_all(gb.ctypes.data, ws=need - 1) == C.WORKSPACE_TOO_SMALL
     assert L.compresskv_gather_heads(ctypes.byref(c.p), FAKE, FAKE, FAKE + 2, gb.ctypes.data,
                                      FAKE, FAKE, None) == C.UNSUPPORTED
+
+
+@pytest.mark.parametrize("name,fields,mask_heads", [
+    ("fp32 inputs", dict(dtype=C.F32), None),
+    ("layer-shared index set", dict(index_mode=C.INDEX_LAYER), None),
+    ("more than 6 row tiles per group", dict(n_q_heads=8, n_kv_heads=1, window=16), 7),
+])
+def test_forced_single_pass_where_it_does_not_apply(L, name, fields, mask_heads):
+    """CKV_SCORE_ONE_PASS on a problem the single pass does not cover is
+    refused on the host with CKV_UNSUPPORTED (nothing is enqueued); the
+    workspace size does not depend on the scoring field."""
+    c = Case()
+    if "n_q_heads" in fields:
+        c = Case(Hq=8, Hkv=1)
+    _mutate(c, **fields)
+    if mask_heads:
+        c.mask[:] = 0
+        c.mask[:mask_heads] = 1
+    n_auto = c.ws_bytes(L)
+    _mutate(c, scoring=C.SCORE_ONE_PASS)
+    assert c.ws_bytes(L) == n_auto > 0
+    for call in ("score", "compress"):
+        st = getattr(c, call)(L)
+        assert st == C.UNSUPPORTED, (call, st, L.compresskv_last_error())
+        assert "single-pass" in L.compresskv_last_error().decode()

@@ -14,15 +14,16 @@ from tests import parity_helpers as H
 pytestmark = pytest.mark.gpu
 
 
-@pytest.fixture(autouse=True, params=["two", "single"])
+PATHS = {"two": C.SCORE_TWO_PASS, "one": C.SCORE_ONE_PASS, "auto": C.SCORE_AUTO}
+
+
+@pytest.fixture(autouse=True, params=sorted(PATHS))
 def scoring_path(request, monkeypatch):
-    """Every case runs on the two-pass path (the default) and on the
-    single-pass kernel (where it applies); the per-layer calls it is compared
-    with take the same path."""
-    if request.param == "single":
-        monkeypatch.setenv("CKV_PATH", "single")
-    else:
-        monkeypatch.delenv("CKV_PATH", raising=False)
+    """Every case runs on the two-pass path, on the single pass (skipped, with
+    the library's reason, where it does not apply to some layer) and on the
+    library's own choice (which may mix the two over the layers); the
+    per-layer calls it is compared with use the same scoring field."""
+    monkeypatch.setattr(H, "SCORING", PATHS[request.param])
     return request.param
 
 
@@ -30,9 +31,9 @@ def _say(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def _problem(q, k, v, cu, cu_host, w):
-    return C.Problem(q, k, v, cu, cu_seqlens_host=cu_host, pool_kernel=w.pool_kernel,
-                     pool_type=w.pool_type)
+def _problem(q, k, v, cu, cu_host, w, masks=None):
+    return H.problem(q, k, v, cu, masks=masks, cu_seqlens_host=cu_host,
+                     pool_kernel=w.pool_kernel, pool_type=w.pool_type)
 
 
 def _host_inputs(w, layer, d) -> wl.LayerInputs:
@@ -80,8 +81,8 @@ def test_compress_layers_matches_oracle_ragged(gpu):
     dts = [H.device_tensors(x, gpu) for x in xs]
     q, k, v = [d[0] for d in dts], [d[1] for d in dts], [d[2] for d in dts]
     cu = dts[0][3]
-    ps = [_problem(q[l], k[l], v[l], cu, xs[0].cu_seqlens, w) for l in range(w.n_layers)]
     masks = np.stack([x.srh_mask for x in xs])
+    ps = [_problem(q[l], k[l], v[l], cu, xs[0].cu_seqlens, w, masks) for l in range(w.n_layers)]
     idxs, kos, vos, scores = C.compress_layers(ps[0], q, k, v, masks, budgets, want_scores=True)
     ref = _per_layer(ps, q, k, v, masks, budgets)
     only_scores = C.score_layers(ps[0], q, k, masks)
@@ -102,8 +103,8 @@ def test_compress_layers_qwen_shape_reduced(gpu):
     _say(f"case qwen stack L={w.seq_len} budgets={budgets}")
     dts = [H.device_tensors(x, gpu) for x in xs]
     q, k, v = [d[0] for d in dts], [d[1] for d in dts], [d[2] for d in dts]
-    p = _problem(q[0], k[0], v[0], dts[0][3], xs[0].cu_seqlens, w)
     masks = np.stack([x.srh_mask for x in xs])
+    p = _problem(q[0], k[0], v[0], dts[0][3], xs[0].cu_seqlens, w, masks)
     idxs, kos, vos, scores = C.compress_layers(p, q, k, v, masks, budgets, want_scores=True)
     torch.cuda.synchronize()
     for l, x in enumerate(xs):
@@ -112,10 +113,12 @@ def test_compress_layers_qwen_shape_reduced(gpu):
         _check_needles(x, budgets[l], idxs[l].cpu().numpy())
 
 
-def test_full_32_layer_stack(gpu):
+def test_full_32_layer_stack(gpu, scoring_path):
     """The 32-layer Llama-3-8B-shaped stack at L = 32768 as the benchmark runs
     it: one multi-layer call, bit-identical to per-layer calls on every layer,
-    and two sampled layers checked against the oracle in full."""
+    and checked against the oracle in full: every layer on the library's own
+    choice of path (the benchmarked one), two sampled layers on the forced
+    paths."""
     w = wl.get("llama32")
     layers = [wl.make_layer_device(w, l, 0, gpu) for l in range(w.n_layers)]
     _say(f"case llama32 full stack, budgets {[d['budget'] for d in layers]}")
@@ -123,8 +126,8 @@ def test_full_32_layer_stack(gpu):
     k = [d["k"] for d in layers]
     v = [d["v"] for d in layers]
     cu, cu_host = layers[0]["cu_seqlens"], layers[0]["cu_seqlens_host"]
-    ps = [_problem(q[l], k[l], v[l], cu, cu_host, w) for l in range(w.n_layers)]
     masks = np.stack([d["srh_mask"] for d in layers])
+    ps = [_problem(q[l], k[l], v[l], cu, cu_host, w, masks) for l in range(w.n_layers)]
     budgets = [d["budget"] for d in layers]
     idxs, kos, vos, scores = C.compress_layers(ps[0], q, k, v, masks, budgets, want_scores=True)
     ref = _per_layer(ps, q, k, v, masks, budgets)
@@ -133,7 +136,7 @@ def test_full_32_layer_stack(gpu):
         for got, want in zip((idxs[l], kos[l], vos[l], scores[l]), ref[l]):
             assert torch.equal(got, want), f"layer {l} differs from the per-layer call"
     del ref
-    for l in (0, 17):
+    for l in (range(w.n_layers) if scoring_path == "auto" else (0, 17)):
         x = _host_inputs(w, l, layers[l])
         swaps = _check_layer(x, budgets[l], scores[l].cpu().numpy(), idxs[l].cpu().numpy(),
                              H.raw_bits(kos[l]), H.raw_bits(vos[l]))
@@ -149,9 +152,6 @@ def test_full_stack_other_shapes(gpu, scoring_path, name, sampled):
     per-layer calls on every layer, and sampled layers against the oracle in
     full."""
     w = wl.get(name)
-    if scoring_path == "single" and name == "qwen128k":
-        pytest.skip("the single-pass kernel does not apply at L = 131072 (512 units per "
-                    "group); that call runs the two-pass case again")
     layers = [wl.make_layer_device(w, l, 0, gpu) for l in range(w.n_layers)]
     _say(f"case {name} full stack, lengths {np.diff(layers[0]['cu_seqlens_host']).tolist()}, "
          f"budgets {[d['budget'] for d in layers]}")
@@ -159,8 +159,8 @@ def test_full_stack_other_shapes(gpu, scoring_path, name, sampled):
     k = [d["k"] for d in layers]
     v = [d["v"] for d in layers]
     cu, cu_host = layers[0]["cu_seqlens"], layers[0]["cu_seqlens_host"]
-    ps = [_problem(q[l], k[l], v[l], cu, cu_host, w) for l in range(w.n_layers)]
     masks = np.stack([d["srh_mask"] for d in layers])
+    ps = [_problem(q[l], k[l], v[l], cu, cu_host, w, masks) for l in range(w.n_layers)]
     budgets = [d["budget"] for d in layers]
     idxs, kos, vos, scores = C.compress_layers(ps[0], q, k, v, masks, budgets, want_scores=True)
     ref = _per_layer(ps, q, k, v, masks, budgets)
@@ -189,8 +189,8 @@ def test_many_layers_short_sequences(gpu, scoring_path):
     k = [d["k"] for d in layers]
     v = [d["v"] for d in layers]
     cu, cu_host = layers[0]["cu_seqlens"], layers[0]["cu_seqlens_host"]
-    ps = [_problem(q[l], k[l], v[l], cu, cu_host, w) for l in range(w.n_layers)]
     masks = np.stack([d["srh_mask"] for d in layers])
+    ps = [_problem(q[l], k[l], v[l], cu, cu_host, w, masks) for l in range(w.n_layers)]
     budgets = [d["budget"] for d in layers]
     idxs, kos, vos, scores = C.compress_layers(ps[0], q, k, v, masks, budgets, want_scores=True)
     ref = _per_layer(ps, q, k, v, masks, budgets)

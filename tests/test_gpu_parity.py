@@ -14,14 +14,15 @@ from tests import parity_helpers as H
 pytestmark = pytest.mark.gpu
 
 
-@pytest.fixture(autouse=True, params=["two", "single"])
+PATHS = {"two": C.SCORE_TWO_PASS, "one": C.SCORE_ONE_PASS}
+
+
+@pytest.fixture(autouse=True, params=sorted(PATHS))
 def scoring_path(request, monkeypatch):
-    """Every case runs on the two-pass path (the default) and on the
-    single-pass kernel (where it applies)."""
-    if request.param == "single":
-        monkeypatch.setenv("CKV_PATH", "single")
-    else:
-        monkeypatch.delenv("CKV_PATH", raising=False)
+    """Every case runs on the two-pass path and on the single pass (skipped,
+    with the library's reason, where the single pass does not apply): the
+    path is the problem's scoring field."""
+    monkeypatch.setattr(H, "SCORING", PATHS[request.param])
     return request.param
 
 
@@ -38,8 +39,8 @@ def run_case(x: wl.LayerInputs, dev, *, budget=None, pool_kernel=None, pool_type
     _say(f"case {w.name} L={np.diff(x.cu_seqlens).tolist()[:8]} budget={budget} pool={pk}/{pt} "
          f"order={reduce_order}")
     q, k, v, cu = H.device_tensors(x, dev)
-    p = C.Problem(q, k, v, cu, cu_seqlens_host=x.cu_seqlens, pool_kernel=pk, pool_type=pt,
-                  reduce_order=reduce_order, scale=scale)
+    p = H.problem(q, k, v, cu, masks=x.srh_mask, cu_seqlens_host=x.cu_seqlens, pool_kernel=pk,
+                  pool_type=pt, reduce_order=reduce_order, scale=scale)
     idx, k_out, v_out, scores = C.compress_layer(p, q, k, v, x.srh_mask, budget, want_scores=True)
     torch.cuda.synchronize()
     res = dict(idx=idx.cpu().numpy(), k_out=H.raw_bits(k_out), v_out=H.raw_bits(v_out),
@@ -148,7 +149,7 @@ def test_select_alone_matches_oracle_on_same_fp32_scores(gpu):
     s32 = ora.scores.astype(np.float32)
     s32[:, :] = np.where(np.isinf(ora.scores), np.inf, s32)
     q, k, v, cu = H.device_tensors(x, gpu)
-    p = C.Problem(q, k, v, cu, cu_seqlens_host=x.cu_seqlens)
+    p = H.problem(q, k, v, cu, masks=x.srh_mask, cu_seqlens_host=x.cu_seqlens)
     for budget in (32, 33, 256, 1000, 5000):
         idx = C.select(p, torch.from_numpy(s32).to(gpu), budget).cpu().numpy()
         for b in range(3):
@@ -167,7 +168,7 @@ def test_select_ties_go_to_lowest_position(gpu):
     w = wl.get("llama1", seq_len=5000, n_needle=0)
     x = wl.make_layer(w, 0, seed=11)
     q, k, v, cu = H.device_tensors(x, gpu)
-    p = C.Problem(q, k, v, cu, cu_seqlens_host=x.cu_seqlens)
+    p = H.problem(q, k, v, cu, masks=x.srh_mask, cu_seqlens_host=x.cu_seqlens)
     s = np.full((8, 5000), 0.25, dtype=np.float32)
     s[:, 4968:] = np.inf
     s[3, 3000:3010] = 0.5
@@ -182,7 +183,7 @@ def test_gather_alone_is_bit_exact_with_oracle_indices(gpu):
     x = wl.make_layer(w, 0, seed=12)
     ora = H.run_oracle(x, budget=600)
     q, k, v, cu = H.device_tensors(x, gpu)
-    p = C.Problem(q, k, v, cu, cu_seqlens_host=x.cu_seqlens)
+    p = H.problem(q, k, v, cu, masks=x.srh_mask, cu_seqlens_host=x.cu_seqlens)
     idx = torch.from_numpy(ora.idx.astype(np.int32)).to(gpu)
     k_out, v_out = C.gather(p, k, v, idx, 600)
     np.testing.assert_array_equal(H.raw_bits(k_out), ora.k_out)
@@ -197,8 +198,8 @@ def test_strided_kv_layout(gpu):
     kh = k.permute(1, 0, 2).contiguous().permute(1, 0, 2)
     vh = v.permute(1, 0, 2).contiguous().permute(1, 0, 2)
     assert kh.stride() != k.stride()
-    p1 = C.Problem(q, k, v, cu, cu_seqlens_host=x.cu_seqlens)
-    p2 = C.Problem(q, kh, vh, cu, cu_seqlens_host=x.cu_seqlens)
+    p1 = H.problem(q, k, v, cu, masks=x.srh_mask, cu_seqlens_host=x.cu_seqlens)
+    p2 = H.problem(q, kh, vh, cu, masks=x.srh_mask, cu_seqlens_host=x.cu_seqlens)
     a = C.compress_layer(p1, q, k, v, x.srh_mask, 512, want_scores=True)
     b = C.compress_layer(p2, q, kh, vh, x.srh_mask, 512, want_scores=True)
     for t1, t2 in zip(a, b):
@@ -215,6 +216,11 @@ def test_deterministic_bits(gpu):
 
 
 def test_scoring_path_choice_for_the_benchmark_shapes(gpu, scoring_path):
+    """Which path each workload's layer 0 takes under CKV_SCORE_AUTO, and that
+    the forced paths are honoured or refused (CKV_UNSUPPORTED)."""
+    one_pass = {"llama1": True, "llama32": True, "ragged8": True,
+                "tiny": False,        # fp32
+                "qwen128k": False}    # W = 64 with 2 SRHs: 8 row tiles per group
     for name, kw in [("llama1", {}), ("llama32", {}), ("ragged8", {}), ("tiny", {}),
                      ("qwen128k", dict(seq_len=32768))]:
         w = wl.get(name, **kw)
@@ -223,17 +229,49 @@ def test_scoring_path_choice_for_the_benchmark_shapes(gpu, scoring_path):
         q = torch.empty((w.batch, w.window, w.n_q_heads, w.head_dim), device=gpu,
                         dtype=torch.bfloat16 if w.dtype == wl.BF16 else torch.float32)
         k = torch.empty((16, w.n_kv_heads, w.head_dim), device=gpu, dtype=q.dtype)
-        p = C.Problem(q, k, k, torch.from_numpy(cu).to(gpu), cu_seqlens_host=cu)
-        path = C.compresskv_scoring_path(p, wl.srh_mask(w, 0))
-        # the single-pass kernel is built for bf16 keys
-        single = scoring_path == "single" and w.dtype == wl.BF16
-        assert path == (1 if single else 2), (name, path)
+        cud = torch.from_numpy(cu).to(gpu)
+        mask = wl.srh_mask(w, 0)
+        auto = C.Problem(q, k, k, cud, cu_seqlens_host=cu, scoring=C.SCORE_AUTO)
+        assert C.compresskv_scoring_path(auto, mask) == (1 if one_pass[name] else 2), name
+        forced = C.Problem(q, k, k, cud, cu_seqlens_host=cu, scoring=PATHS[scoring_path])
+        if scoring_path == "two":
+            assert C.compresskv_scoring_path(forced, mask) == 2, name
+        elif one_pass[name]:
+            assert C.compresskv_scoring_path(forced, mask) == 1, name
+        else:
+            with pytest.raises(C.CompressKVError) as e:
+                C.compresskv_scoring_path(forced, mask)
+            assert e.value.status == C.UNSUPPORTED, name
 
 
 def test_score_entry_point_alone(gpu):
     w = wl.get("llama1", seq_len=2048 + 3, n_needle=4)
     x = wl.make_layer(w, 0, seed=15)
     q, k, v, cu = H.device_tensors(x, gpu)
-    p = C.Problem(q, k, v, cu, cu_seqlens_host=x.cu_seqlens)
+    p = H.problem(q, k, v, cu, masks=x.srh_mask, cu_seqlens_host=x.cu_seqlens)
     s = C.score(p, q, k, x.srh_mask).cpu().numpy()
     H.check_scores(s, H.run_oracle(x), x.cu_seqlens, 32)
+
+
+def test_single_pass_catch_up_kernel_gives_the_same_bits(gpu, scoring_path):
+    """Every unit left to the catch-up kernel (CKV_SPIN_CATCHUP_ALL), a unit
+    never waiting (spin_limit 0) and the default bound give bit-identical
+    results, which match the oracle: a late normaliser never changes a
+    result."""
+    if scoring_path != "one":
+        pytest.skip("single-pass case")
+    w = wl.get("ragged8", batch=3, ragged=(1500, 7000), n_needle=4)
+    x = wl.make_layer(w, 0, seed=16)
+    q, k, v, cu = H.device_tensors(x, gpu)
+    outs = []
+    for spin in (C.SPIN_DEFAULT, 0, C.SPIN_CATCHUP_ALL):
+        p = H.problem(q, k, v, cu, masks=x.srh_mask, cu_seqlens_host=x.cu_seqlens,
+                      spin_limit=spin)
+        outs.append(C.compress_layer(p, q, k, v, x.srh_mask, 300, want_scores=True))
+    torch.cuda.synchronize()
+    for other in outs[1:]:
+        for a, b in zip(outs[0], other):
+            assert torch.equal(a, b)
+    ora = H.run_oracle(x, 300)
+    H.check_scores(outs[2][3].cpu().numpy(), ora, x.cu_seqlens, w.window)
+    H.check_indices(outs[2][0].cpu().numpy(), ora, x.cu_seqlens, w.window, 300)
