@@ -74,7 +74,7 @@ extern "C" {
 
 /* how S1-S4 are computed (the results agree within the scores' tolerance;
    each choice is deterministic) */
-#define CKV_SCORE_AUTO 0     /* single pass where it applies (see compresskv_scoring_path) */
+#define CKV_SCORE_AUTO 0     /* the library's choice (see compresskv_scoring_path) */
 #define CKV_SCORE_TWO_PASS 1 /* two passes over K: row statistics, then window sums */
 #define CKV_SCORE_ONE_PASS 2 /* K read once; CKV_UNSUPPORTED where it does not apply */
 #define CKV_SPIN_CATCHUP_ALL (-2) /* ckv_problem.spin_limit: see there */
@@ -230,12 +230,12 @@ int compresskv_compress_layer_heads(const ckv_problem *p, const void *q_win, con
 /*
  * Which scoring implementation compresskv_score / _compress_layer will use for
  * this problem: 1 = single pass (each key read once from HBM), 2 = two passes
- * over K.  The single pass needs bf16 inputs, CKV_INDEX_PER_GROUP, batch <= 64
- * and at most 6 row tiles per group (ceil(W/16) * SRHs); CKV_SCORE_AUTO also
- * needs the 256-key units of the longest sequence to number no more than the
- * device's CUs.  The multi-layer calls make the same choice layer by layer.
- * Negative on invalid arguments (minus the status).  With CKV_SCORE_AUTO it
- * queries the device, so it needs a GPU.
+ * over K.  CKV_SCORE_AUTO and CKV_SCORE_TWO_PASS use two passes (the faster
+ * of the two on the measured shapes); CKV_SCORE_ONE_PASS uses the single
+ * pass, which needs bf16 inputs, CKV_INDEX_PER_GROUP, batch <= 64 and at most
+ * 6 row tiles per group (ceil(W/16) * SRHs), and otherwise returns
+ * -CKV_UNSUPPORTED.  The multi-layer calls make the same choice layer by
+ * layer.  Negative on invalid arguments (minus the status).
  */
 int compresskv_scoring_path(const ckv_problem *p, const uint8_t *srh_mask_host);
 

@@ -240,25 +240,18 @@ int device_cus() {
 }
 
 // Which layers are scored in a single pass, and the table order (those
-// layers first).  A layer qualifies if its groups have at most 6 row tiles;
-// CKV_SCORE_AUTO also needs every segment's units to fit in one round of the
-// persistent workgroups (one per CU), so that a segment's units are in flight
-// together; CKV_SCORE_ONE_PASS asks for it on every layer (CKV_UNSUPPORTED
-// where a layer does not qualify).  The choice for a layer depends only on the
-// problem and that layer's masks, so multi-layer calls score every layer as
-// the single-layer call would.
+// layers first).  CKV_SCORE_AUTO picks the two-pass kernels, which are the
+// faster of the two on the shapes measured; CKV_SCORE_ONE_PASS asks for the
+// single pass on every layer (CKV_UNSUPPORTED where a layer does not
+// qualify: more than 6 row tiles in a group).  The choice for a layer depends
+// only on the problem and that layer's masks, so multi-layer calls score
+// every layer as the single-layer call would.
 int choose_paths(const ckv_problem *p, Plan &pl) {
   const int n = pl.n_layers;
   std::vector<uint8_t> op(n, 0);
   pl.op_grid = 0;
-  if (pl.op_shape) {
-    bool fits = true;
-    if (p->scoring == CKV_SCORE_AUTO) {
-      pl.op_grid = device_cus();
-      fits = pl.op_grid > 0 && op_units(pl.lmax) <= pl.op_grid;
-    }
-    for (int l = 0; l < n; ++l) op[l] = fits && pl.rt_layer[l] <= kOnePassMaxRowTiles;
-  }
+  if (pl.op_shape && p->scoring == CKV_SCORE_ONE_PASS)
+    for (int l = 0; l < n; ++l) op[l] = pl.rt_layer[l] <= kOnePassMaxRowTiles;
   if (p->scoring == CKV_SCORE_ONE_PASS) {
     if (!pl.op_shape)
       return fail(CKV_UNSUPPORTED, "single-pass scoring needs bf16 inputs, CKV_INDEX_PER_GROUP "

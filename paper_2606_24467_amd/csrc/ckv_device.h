@@ -12,6 +12,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <stddef.h>
 #include <stdint.h>
 
 namespace ckv {
@@ -40,9 +41,11 @@ struct alignas(16) LayerDesc {
   void *k_out, *v_out;    // [batch][Hkv][budget][D]
   int32_t budget;
   int32_t reserved;
-  uint16_t srh_off[kMaxKvHeads + 1];   // SRHs of group g: srh_head[srh_off[g] .. srh_off[g+1])
+  uint16_t srh_off[kMaxKvHeads + 2];   // SRHs of group g: srh_head[srh_off[g] .. srh_off[g+1])
   uint8_t srh_head[kMaxQHeads];        // query-head indices, ascending within a group
 };
+static_assert(offsetof(LayerDesc, srh_off) % 4 == 0 && offsetof(LayerDesc, srh_head) % 4 == 0,
+              "table fields read as 32-bit words");
 
 // Pointers into global memory.  Pointers read from the layer table have no
 // address space the compiler can infer; generic (flat) accesses would share
@@ -61,6 +64,16 @@ using cptr = const __attribute__((address_space(4))) T *;
 template <typename T>
 __device__ __forceinline__ cptr<T> to_const(const T *p) {
   return (cptr<T>)p;
+}
+
+// srh_off[g] of a table entry through aligned 32-bit reads of the constant
+// address space (16-bit fields can not be read by scalar loads); for a
+// uniform (layer, g) these stay scalar and never wait on a kernel's vector
+// loads.
+__device__ __forceinline__ int srh_off_at(cptr<LayerDesc> d, int g) {
+  const cptr<uint32_t> w =
+      reinterpret_cast<cptr<uint32_t>>(reinterpret_cast<cptr<char>>(d) + offsetof(LayerDesc, srh_off));
+  return (int)((w[g >> 1] >> (16 * (g & 1))) & 0xFFFFu);
 }
 
 // What a workgroup uses of its layer, as global pointers; off / nsrh describe
@@ -89,8 +102,8 @@ __device__ __forceinline__ LayerView layer_view(const A &a, int layer, int g) {
     v.v_out = to_global(static_cast<char *>(d->v_out));
     v.srh_head = &(to_global(a.layers) + layer)->srh_head[0];
     v.budget = d->budget;
-    v.off = d->srh_off[g];
-    v.nsrh = d->srh_off[g + 1] - v.off;
+    v.off = srh_off_at(d, g);
+    v.nsrh = srh_off_at(d, g + 1) - v.off;
   } else {
     (void)layer;
     const LayerDesc &d = a.l0;
@@ -113,8 +126,8 @@ __device__ __forceinline__ LayerView layer_view(const A &a, int layer, int g) {
 template <bool ML, typename A>
 __device__ __forceinline__ int srh_count(const A &a, int layer, int g) {
   if constexpr (ML) {
-    gptr<const LayerDesc> d = to_global(a.layers) + layer;
-    return d->srh_off[g + 1] - d->srh_off[g];
+    cptr<LayerDesc> d = to_const(a.layers) + layer;
+    return srh_off_at(d, g + 1) - srh_off_at(d, g);
   } else {
     (void)layer;
     return a.l0.srh_off[g + 1] - a.l0.srh_off[g];

@@ -69,11 +69,13 @@ struct OpUnit {
 template <bool UNIFORM = true>
 __device__ __forceinline__ OpUnit op_decode(const OnePassArgs &f, int ticket_any) {
   const ScoreArgs &a = f.s;
-  const int tk = UNIFORM ? __builtin_amdgcn_readfirstlane(ticket_any) : ticket_any;
+  const int tk_in = UNIFORM ? __builtin_amdgcn_readfirstlane(ticket_any) : ticket_any;
   OpUnit x{};
-  x.valid = tk >= 0 && tk < f.n_units_total;
-  x.ticket = tk;
-  if (!x.valid) return x;
+  x.valid = tk_in >= 0 && tk_in < f.n_units_total;
+  // an invalid ticket decodes as unit 0 (valid addresses for the loads that
+  // every iteration issues unconditionally; nothing of it is used)
+  const int tk = x.valid ? tk_in : 0;
+  x.ticket = tk_in;
   x.layer = tk / f.units_per_layer;
   const int t = tk - x.layer * f.units_per_layer;
   int b = 0;
@@ -104,20 +106,49 @@ __device__ __forceinline__ float2 *op_partials(const ScoreArgs &a, const OpUnit 
   return a.stats + x.layer * a.stats_layer + (int64_t)x.gi * a.parts_stride * a.row_slots;
 }
 
-// Issue the global loads of unit x: its keys (tiles wave and wave + 8 of the
-// unit; key indices clamped into the sequence) and its window queries.
+// The global loads of unit x (decoded from any ticket, valid or not): its
+// window queries, then its keys (tiles wave and wave + 8 of the unit).  Every
+// load is issued, with indices clamped into range, so that each wave issues
+// the same number of loads on every path; the values of rows a group does not
+// have, and of padding rows, are replaced by zeros.  The compiler can then
+// count exactly how many loads follow an earlier one, and a wait for an
+// earlier value never waits for these.
 template <typename T, int D, int RTM>
 __device__ __forceinline__ void op_unit_loads(const ScoreArgs &a, const OpUnit &x,
                                               uint4 (&kr)[kOpTiles][Slices<T, D>::n],
                                               uint4 (&qv)[QStage<T, D, RTM, kOpThreads>::n]) {
+  constexpr int U4 = QLayout<T, D>::U4;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int c = lane & 15, quad = lane >> 4;
   const LayerView lv = layer_view<true>(a, x.layer, x.g);
-  q_load<T, D, RTM, kOpThreads>(a, lv, x.b, x.rt_n, qv);
+  const int rt_n = max(x.rt_n, 1);
+  // the group's SRH heads (at most RTM) from the table's srh_head bytes,
+  // three aligned words read as scalars
+  const cptr<LayerDesc> d = to_const(a.layers) + x.layer;
+  const cptr<uint32_t> hw = reinterpret_cast<cptr<uint32_t>>(
+      reinterpret_cast<cptr<char>>(d) + offsetof(LayerDesc, srh_head));
+  const int w0 = min(lv.off >> 2, kMaxQHeads / 4 - 3);
+  const uint32_t hw0 = hw[w0], hw1 = hw[w0 + 1], hw2 = hw[w0 + 2];
+#pragma unroll
+  for (int it = 0; it < QStage<T, D, RTM, kOpThreads>::n; ++it) {
+    const int idx = (int)threadIdx.x + it * kOpThreads;
+    const int row = idx / U4, u = idx - row * U4;
+    const int rt = row >> 4;
+    const int rtc = min(rt, rt_n - 1);
+    const int i = (rtc % a.th) * 16 + (row & 15);
+    const int ic = min(i, a.W - 1);
+    const int byte = lv.off + rtc / a.th - 4 * w0;   // < 12 for at most 6 heads
+    const uint32_t word = byte < 4 ? hw0 : byte < 8 ? hw1 : hw2;
+    const int head = (int)((word >> (8 * (byte & 3))) & 0xFFu);
+    const uint4 v = load16(lv.q + (((int64_t)x.b * a.W + ic) * a.Hq + head) *
+                                      (int64_t)(D * sizeof(T)) + 16 * u);
+    const bool real = rt < x.rt_n && i < a.W && row < RTM * 16;
+    qv[it] = real ? v : make_uint4(0, 0, 0, 0);
+  }
 #pragma unroll
   for (int t = 0; t < kOpTiles; ++t)
-    load_k_row<T, D>(a, lv.k, x.s0, min(x.u0 + 16 * (wave + kOpWaves * t) + c, x.L - 1), x.g,
-                     quad, kr[t]);
+    load_k_row<T, D>(a, lv.k, x.s0, max(0, min(x.u0 + 16 * (wave + kOpWaves * t) + c, x.L - 1)),
+                     x.g, quad, kr[t]);
 }
 
 // Whether key j is visible to the window row of lane row c in row tile rt:
@@ -393,16 +424,19 @@ __device__ __forceinline__ float op_pool(const ScoreArgs &a, F cs_at, int nh, in
 }
 
 // S3 + S4 of unit x from its e-values and row maxima mu_s, with the segment's
-// normalisers in bias_s: window sums per SRH into cs, pooled scores of the
-// unit's interior positions (+inf on window positions), their first-digit
-// histogram (two 16-bit counts per word of hist2, at most 256 per unit), and
-// the window sums of the unit's first and last ew keys for the boundary
-// kernel.  Starts and ends with a barrier-separated use of cs.
+// normalisers in bias_s, into LDS only: window sums per SRH into cs, the
+// pooled scores of the unit's interior positions into stage (and their
+// first-digit histogram into hist2, two 16-bit counts per word, at most 256
+// per unit), and the window sums of the unit's first and last ew keys into
+// edge_s ([h][side][ew]: side 0 = keys u0 .. u0 + ew - 1, side 1 = the last ew
+// keys) for the boundary kernel.  op_unit_flush writes them out.  Starts and
+// ends with a barrier-separated use of cs.
 template <int RTM>
 __device__ __forceinline__ void op_unit_finish(const OnePassArgs &f, const OpUnit &x,
                                                const f32x4 (&e)[kOpTiles][RTM],
                                                const float *mu_s, const float *bias_s,
-                                               float (*cs)[kOpUnit], uint32_t *hist2) {
+                                               float (*cs)[kOpUnit], float *stage, float *edge_s,
+                                               uint32_t *hist2) {
   const ScoreArgs &a = f.s;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int c = lane & 15, quad = lane >> 4;
@@ -418,7 +452,7 @@ __device__ __forceinline__ void op_unit_finish(const OnePassArgs &f, const OpUni
       if (rt < rtu) {
         const float w = fast_exp2(mu_s[rt * 16 + c] - bias_s[rt * 16 + c]);
         const bool first = rt == 0 || ((a.head_end_mask >> (rt - 1)) & 1u);
-  #pragma unroll
+#pragma unroll
         for (int r = 0; r < 4; ++r)
           v[r] = first ? e[t][rt][r] * w : __builtin_fmaf(e[t][rt][r], w, v[r]);
         if ((a.head_end_mask >> rt) & 1u) {
@@ -430,38 +464,57 @@ __device__ __forceinline__ void op_unit_finish(const OnePassArgs &f, const OpUni
     }
   }
   __syncthreads();
+  const int rp = (a.pool_kernel - 1) >> 1;
+  auto cs_at = [&](int h, int pos) { return cs[h][pos - x.u0]; };
+  for (int j = tid; j < kOpUnit; j += kOpThreads) {
+    const int pos = x.u0 + j;
+    if (pos >= x.P) continue;
+    const bool left_ok = x.u == 0 || pos - rp >= x.u0;
+    const bool right_ok = pos + rp < x.u0 + kOpUnit || x.P <= x.u0 + kOpUnit;
+    if (!(left_ok && right_ok)) continue;   // pooled by the boundary kernel
+    const float score = op_pool(a, cs_at, x.nh, pos, x.P);
+    stage[j] = score;
+    const int bin = hist_bin(__float_as_uint(score));
+    atomicAdd(&hist2[bin >> 1], 1u << (16 * (bin & 1)));
+  }
+  const int ew = f.ew;
+  for (int i = tid; i < x.nh * 2 * ew; i += kOpThreads) {
+    const int h = i / (2 * ew), side = (i / ew) & 1, k = i % ew;
+    edge_s[i] = cs[h][side ? kOpUnit - ew + k : k];
+  }
+  __syncthreads();   // cs is reused
+}
+
+// The global writes of a unit: its scores (the interior positions op_unit_finish
+// pooled, +inf on window positions; WINDOW_ONLY: a unit without prefix
+// positions), its edge window sums and its histogram counts (which are
+// cleared in LDS).  The positions within r of a boundary with another unit
+// are written by the boundary kernel.
+template <bool WINDOW_ONLY>
+__device__ __forceinline__ void op_unit_flush(const OnePassArgs &f, const OpUnit &x,
+                                              const float *stage, const float *edge_s,
+                                              uint32_t *hist2) {
+  const ScoreArgs &a = f.s;
+  const int tid = threadIdx.x;
   const LayerView lv = layer_view<true>(a, x.layer, x.g);
   const gptr<float> out = lv.scores + (int64_t)x.g * a.T + x.s0;
   const int rp = (a.pool_kernel - 1) >> 1;
   const int u_end = min(x.u0 + kOpUnit, x.L);
-  auto cs_at = [&](int h, int pos) { return cs[h][pos - x.u0]; };
   for (int j = tid; j < kOpUnit; j += kOpThreads) {
     const int pos = x.u0 + j;
     if (pos >= u_end) continue;
-    if (pos >= x.P) {
+    if (WINDOW_ONLY || pos >= x.P) {
       out[pos] = INFINITY;
       continue;
     }
     const bool left_ok = x.u == 0 || pos - rp >= x.u0;
     const bool right_ok = pos + rp < x.u0 + kOpUnit || x.P <= x.u0 + kOpUnit;
-    if (!(left_ok && right_ok)) continue;   // pooled by the boundary kernel
-    const float score = op_pool(a, cs_at, x.nh, pos, x.P);
-    out[pos] = score;
-    const int bin = hist_bin(__float_as_uint(score));
-    atomicAdd(&hist2[bin >> 1], 1u << (16 * (bin & 1)));
+    if (left_ok && right_ok) out[pos] = stage[j];
   }
-  // window sums at both ends of the unit, for the positions around its
-  // boundaries: [h][side][ew], side 0 = keys u0 .. u0 + ew - 1, side 1 = the
-  // last ew keys of the unit
+  if constexpr (WINDOW_ONLY) return;
   const int ew = f.ew;
-  if (ew > 0) {
-    float *ed = f.edges + (int64_t)x.ticket * f.heads_max * 2 * ew;
-    for (int i = tid; i < x.nh * 2 * ew; i += kOpThreads) {
-      const int h = i / (2 * ew), side = (i / ew) & 1, k = i % ew;
-      ed[i] = cs[h][side ? kOpUnit - ew + k : k];
-    }
-  }
-  __syncthreads();
+  float *ed = f.edges + (int64_t)x.ticket * f.heads_max * 2 * ew;
+  for (int i = tid; i < x.nh * 2 * ew; i += kOpThreads) ed[i] = edge_s[i];
   int *hg = a.hist + x.layer * a.hist_layer + (int64_t)x.gi * kHistBins;
   for (int i = tid; i < kHistBins / 2; i += kOpThreads) {
     const uint32_t n = hist2[i];
@@ -471,7 +524,6 @@ __device__ __forceinline__ void op_unit_finish(const OnePassArgs &f, const OpUni
       hist2[i] = 0;
     }
   }
-  __syncthreads();   // cs and hist2 are reused
 }
 
 // LDS of the single-pass kernels, kept under 64 KiB so that every access is a
@@ -487,18 +539,11 @@ struct OpLds {
   } u;
   float bias_s[RTM * 16];
   float mu_s[2][RTM * 16];
+  float stage[kOpUnit];                          // pooled scores of the unit being finished
+  float edge_s[RTM * 2 * (kMaxPoolKernel - 1)];  // its edge window sums
   uint32_t hist2[kHistBins / 2];
   int tk_s[4];
 };
-
-// Window positions of a unit without prefix keys: +inf.
-__device__ __forceinline__ void op_window_only(const OnePassArgs &f, const OpUnit &x) {
-  const ScoreArgs &a = f.s;
-  const LayerView lv = layer_view<true>(a, x.layer, x.g);
-  const gptr<float> out = lv.scores + (int64_t)x.g * a.T + x.s0;
-  const int u_end = min(x.u0 + kOpUnit, x.L);
-  for (int pos = x.u0 + (int)threadIdx.x; pos < u_end; pos += kOpThreads) out[pos] = INFINITY;
-}
 
 // Main kernel: persistent workgroups (at most one per CU), see the header.
 // Iteration k: A = unit k - 2 is finished from e-value set k % 2, then
@@ -540,53 +585,17 @@ __global__ __launch_bounds__(kOpThreads) void onepass_kernel(const OnePassArgs f
   __syncthreads();
   int tA = -1, tA2 = -1, tB = tk_s[0];
   int t_pub = -1;   // unit published in the previous iteration (its arrival is checked next)
-  {
-    const OpUnit B = op_decode(f, tB);
-    if (B.valid) op_unit_loads<T, D, RTM>(a, B, kr, qv);
-  }
+  op_unit_loads<T, D, RTM>(a, op_decode(f, tB), kr, qv);
 
   auto iterate = [&]<int P>() __attribute__((always_inline)) -> bool {
-    // 1. finish A = unit k - 2 (its normalisers were polled an iteration ago)
-    const OpUnit A = op_decode(f, tA);
-    if (A.valid) {
-      if (A.u0 < A.P) {
-        const int rows = A.rt_n * 16;
-        // a unit this workgroup has not published yet can not arrive while it
-        // waits: A is finished later if B belongs to A's segment
-        const bool self = op_in_segment(A, tB);
-        int ok = __syncthreads_and((tid >= rows || pv.y == 1.f) && f.spin_limit >= 0);
-        for (int spins = 0; !ok && !self && spins < f.spin_limit; ++spins) {
-          __builtin_amdgcn_s_sleep(8);
-          if (tid < rows)
-            pv = load_partial_coherent(f.bias + (int64_t)A.seg * a.row_slots + tid);
-          ok = __syncthreads_and(tid >= rows || pv.y == 1.f);
-        }
-        if (ok) {
-          if (tid < rows) bias_s[tid] = pv.x;
-          for (int r = rows + tid; r < RTM * 16; r += kOpThreads) bias_s[r] = INFINITY;
-          __syncthreads();
-          op_unit_finish<RTM>(f, A, ev[P], mu_s[P], bias_s, cs, hist2);
-        } else if (tid == 0) {
-          f.skip_list[atomicAdd(f.skip_count, 1)] = A.ticket;
-        }
-      } else {
-        op_window_only(f, A);
-      }
-    }
-    // 2. poll the normalisers of unit k - 1 (finished in the next iteration)
-    {
-      const OpUnit A2 = op_decode(f, tA2);
-      if (A2.valid && tid < A2.rt_n * 16)
-        pv = load_partial_coherent(f.bias + (int64_t)A2.seg * a.row_slots + tid);
-    }
-    // 3. the previous publication: its last arrival merges and publishes the
-    //    segment's normalisers; the ticket of unit k + 1; B's queries to LDS
+    // 1. the previous publication: if it was its segment's last arrival, merge
+    //    and publish the segment's normalisers before anything that may wait
+    //    (so that no workgroup's wait delays another segment's merge); the
+    //    ticket of unit k + 1
     if (tid == 0) {
       tk_s[2] = (t_pub >= 0) ? arrived : -1;
       tk_s[3] = tk_req;
     }
-    const OpUnit B = op_decode(f, tB);
-    if (B.valid) q_store<T, D, RTM, kOpThreads>(qv, q_lds);
     __syncthreads();
     const int tC = tk_s[3];
     if (t_pub >= 0) {
@@ -599,26 +608,70 @@ __global__ __launch_bounds__(kOpThreads) void onepass_kernel(const OnePassArgs f
         }
       }
     }
-    // 4. B = unit k: logits, then unit k + 1's loads, then statistics,
-    //    published (the arrival is checked in the next iteration)
+    // 2. finish A = unit k - 2 (its normalisers were polled an iteration ago)
+    //    into LDS; its global writes follow B's logits (step 4), so that the
+    //    wait for B's keys does not wait for them
+    const OpUnit A = op_decode(f, tA);
+    int flush = 0;   // 1: A finished, 2: A has only window positions
+    if (A.valid) {
+      if (A.u0 < A.P) {
+        const int rows = A.rt_n * 16;
+        // a unit this workgroup has not published yet can not arrive while it
+        // waits: A is finished later if B or unit k + 1 belongs to A's segment
+        const bool self = op_in_segment(A, tB) || op_in_segment(A, tC);
+        int ok = __syncthreads_and((tid >= rows || pv.y == 1.f) && f.spin_limit >= 0);
+        for (int spins = 0; !ok && !self && spins < f.spin_limit; ++spins) {
+          __builtin_amdgcn_s_sleep(8);
+          if (tid < rows)
+            pv = load_partial_coherent(f.bias + (int64_t)A.seg * a.row_slots + tid);
+          ok = __syncthreads_and(tid >= rows || pv.y == 1.f);
+        }
+        if (ok) {
+          if (tid < rows) bias_s[tid] = pv.x;
+          for (int r = rows + tid; r < RTM * 16; r += kOpThreads) bias_s[r] = INFINITY;
+          __syncthreads();
+          op_unit_finish<RTM>(f, A, ev[P], mu_s[P], bias_s, cs, sm.stage, sm.edge_s, hist2);
+          flush = 1;
+        } else if (tid == 0) {
+          f.skip_list[atomicAdd(f.skip_count, 1)] = A.ticket;
+        }
+      } else {
+        flush = 2;
+      }
+    }
+    // 3. B's queries to LDS
+    const OpUnit B = op_decode(f, tB);
+    if (B.valid) q_store<T, D, RTM, kOpThreads>(qv, q_lds);
+    __syncthreads();
+    // 4. B = unit k: logits; A's global writes; the poll of unit k - 1's
+    //    normalisers (finished in the next iteration)
     t_pub = -1;
     if (B.valid) op_unit_logits<T, D, RTM>(B, kr, q_lds, ev[P]);
+    if (flush == 1) op_unit_flush<false>(f, A, sm.stage, sm.edge_s, hist2);
+    if (flush == 2) op_unit_flush<true>(f, A, sm.stage, sm.edge_s, hist2);
     {
-      const OpUnit C = op_decode(f, tC);
-      if (C.valid) op_unit_loads<T, D, RTM>(a, C, kr, qv);
+      const OpUnit A2 = op_decode(f, tA2);
+      pv = load_partial_coherent(f.bias + (int64_t)A2.seg * a.row_slots +
+                                 min(tid, max(A2.rt_n, 1) * 16 - 1));
     }
-    if (tid == 0) tk_req = atomicAdd(f.ticket, 1);
+    // 5. B's statistics, published; the arrival and the next ticket
     if (B.valid) {
       const float2 mine = op_unit_stats<RTM>(a, B, ev[P], mu_s[P], part);
       if (tid < B.rt_n * 16)
         store_partial_coherent(op_partials(a, B) + (int64_t)B.u * a.row_slots + tid,
                                make_float2(mine.x, -mine.y));
-      __syncthreads();   // every partial store is issued before the arrival
-      if (tid == 0)
-        arrived = __hip_atomic_fetch_add(&f.arrive[B.seg], 1, __ATOMIC_RELAXED,
-                                         __HIP_MEMORY_SCOPE_AGENT);
       t_pub = tB;
     }
+    __syncthreads();   // every partial store is issued before the arrival
+    if (tid == 0) {
+      if (t_pub >= 0)
+        arrived = __hip_atomic_fetch_add(&f.arrive[B.seg], 1, __ATOMIC_RELAXED,
+                                         __HIP_MEMORY_SCOPE_AGENT);
+      tk_req = atomicAdd(f.ticket, 1);
+    }
+    // 6. unit k + 1's loads into the registers B's operands came from (after
+    //    the atomics, so that reading their results does not wait for them)
+    op_unit_loads<T, D, RTM>(a, op_decode(f, tC), kr, qv);
     tA = tA2;
     tA2 = tB;
     tB = tC;
@@ -661,7 +714,8 @@ __global__ __launch_bounds__(kOpThreads) void onepass_catchup_kernel(const OnePa
     op_merge_segment(a, x, 0, RTM * 16, bias_s);   // ends with a barrier
     op_unit_logits<T, D, RTM>(x, kr, q_lds, e);
     op_unit_stats<RTM>(a, x, e, mu_s, part);
-    op_unit_finish<RTM>(f, x, e, mu_s, bias_s, cs, hist2);
+    op_unit_finish<RTM>(f, x, e, mu_s, bias_s, cs, sm.stage, sm.edge_s, hist2);
+    op_unit_flush<false>(f, x, sm.stage, sm.edge_s, hist2);
   }
 }
 

@@ -14,15 +14,15 @@ from tests import parity_helpers as H
 pytestmark = pytest.mark.gpu
 
 
-PATHS = {"two": C.SCORE_TWO_PASS, "one": C.SCORE_ONE_PASS, "auto": C.SCORE_AUTO}
+PATHS = {"two": C.SCORE_TWO_PASS, "one": C.SCORE_ONE_PASS}
 
 
 @pytest.fixture(autouse=True, params=sorted(PATHS))
 def scoring_path(request, monkeypatch):
-    """Every case runs on the two-pass path, on the single pass (skipped, with
-    the library's reason, where it does not apply to some layer) and on the
-    library's own choice (which may mix the two over the layers); the
-    per-layer calls it is compared with use the same scoring field."""
+    """Every case runs on the two-pass path (the library's own choice) and on
+    the single pass (skipped, with the library's reason, where it does not
+    apply to some layer); the per-layer calls it is compared with use the
+    same scoring field."""
     monkeypatch.setattr(H, "SCORING", PATHS[request.param])
     return request.param
 
@@ -116,9 +116,9 @@ def test_compress_layers_qwen_shape_reduced(gpu):
 def test_full_32_layer_stack(gpu, scoring_path):
     """The 32-layer Llama-3-8B-shaped stack at L = 32768 as the benchmark runs
     it: one multi-layer call, bit-identical to per-layer calls on every layer,
-    and checked against the oracle in full: every layer on the library's own
-    choice of path (the benchmarked one), two sampled layers on the forced
-    paths."""
+    and checked against the oracle in full: every layer on the two-pass path
+    (the library's own choice, the benchmarked one), two sampled layers on
+    the single pass."""
     w = wl.get("llama32")
     layers = [wl.make_layer_device(w, l, 0, gpu) for l in range(w.n_layers)]
     _say(f"case llama32 full stack, budgets {[d['budget'] for d in layers]}")
@@ -136,7 +136,7 @@ def test_full_32_layer_stack(gpu, scoring_path):
         for got, want in zip((idxs[l], kos[l], vos[l], scores[l]), ref[l]):
             assert torch.equal(got, want), f"layer {l} differs from the per-layer call"
     del ref
-    for l in (range(w.n_layers) if scoring_path == "auto" else (0, 17)):
+    for l in (range(w.n_layers) if scoring_path == "two" else (0, 17)):
         x = _host_inputs(w, l, layers[l])
         swaps = _check_layer(x, budgets[l], scores[l].cpu().numpy(), idxs[l].cpu().numpy(),
                              H.raw_bits(kos[l]), H.raw_bits(vos[l]))

@@ -216,9 +216,10 @@ def test_deterministic_bits(gpu):
 
 
 def test_scoring_path_choice_for_the_benchmark_shapes(gpu, scoring_path):
-    """Which path each workload's layer 0 takes under CKV_SCORE_AUTO, and that
-    the forced paths are honoured or refused (CKV_UNSUPPORTED)."""
-    one_pass = {"llama1": True, "llama32": True, "ragged8": True,
+    """CKV_SCORE_AUTO takes the two-pass kernels; the forced paths are
+    honoured, or refused with CKV_UNSUPPORTED where the single pass does not
+    apply."""
+    one_pass = {"llama1": True, "llama32": True, "ragged8": True,   # where it may be forced
                 "tiny": False,        # fp32
                 "qwen128k": False}    # W = 64 with 2 SRHs: 8 row tiles per group
     for name, kw in [("llama1", {}), ("llama32", {}), ("ragged8", {}), ("tiny", {}),
@@ -232,7 +233,7 @@ def test_scoring_path_choice_for_the_benchmark_shapes(gpu, scoring_path):
         cud = torch.from_numpy(cu).to(gpu)
         mask = wl.srh_mask(w, 0)
         auto = C.Problem(q, k, k, cud, cu_seqlens_host=cu, scoring=C.SCORE_AUTO)
-        assert C.compresskv_scoring_path(auto, mask) == (1 if one_pass[name] else 2), name
+        assert C.compresskv_scoring_path(auto, mask) == 2, name
         forced = C.Problem(q, k, k, cud, cu_seqlens_host=cu, scoring=PATHS[scoring_path])
         if scoring_path == "two":
             assert C.compresskv_scoring_path(forced, mask) == 2, name
