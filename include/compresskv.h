@@ -160,6 +160,24 @@ int compresskv_compress_layer(const ckv_problem *p, const void *q_win, const voi
                               void *ws, size_t ws_bytes, void *stream);
 
 /*
+ * compresskv_compress_layer without a workspace argument and without any
+ * allocation, for callers that can not allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).
+ * The library's scratch is a fixed array of 32 MiB per device, held from the
+ * first call on that device until the process ends; a problem whose
+ * compresskv_workspace_bytes exceeds it returns CKV_WORKSPACE_TOO_SMALL (use
+ * compresskv_compress_layer with a workspace).  Every call on one device
+ * shares that device's array: calls that overlap in time on one device (other
+ * streams, other threads) race and must be serialised by the caller.  Results
+ * are identical to compresskv_compress_layer's.  The first call on a device
+ * looks up the array's address (hipGetSymbolAddress) with that device current.
+ */
+int compresskv_compress_layer_noalloc(const ckv_problem *p, const void *q_win, const void *k,
+                                      const void *v, const uint8_t *srh_mask_host,
+                                      int32_t budget, int32_t *idx, void *k_out, void *v_out,
+                                      float *scores_or_null, void *stream);
+
+/*
  * Multi-layer calls.  A model's layers share one problem (shapes, cu_seqlens,
  * strides, options) and differ in their operands, SRH masks and budgets
  * (section 3.4 gives every layer its own budget; section 3.2 every layer its

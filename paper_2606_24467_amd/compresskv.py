@@ -103,6 +103,8 @@ def lib() -> ctypes.CDLL:
     for f in ("compresskv_score", "compresskv_select", "compresskv_gather",
               "compresskv_compress_layer"):
         getattr(L, f).restype = ctypes.c_int
+    L.compresskv_compress_layer_noalloc.argtypes = [P, vp, vp, vp, u8p, i32, vp, vp, vp, vp, vp]
+    L.compresskv_compress_layer_noalloc.restype = ctypes.c_int
     L.compresskv_layers_workspace_bytes.argtypes = [P, i32, u8p]
     L.compresskv_layers_workspace_bytes.restype = sz
     L.compresskv_score_layers.argtypes = [P, i32, vp, vp, u8p, vp, vp, sz, vp]
@@ -259,6 +261,14 @@ def compresskv_compress_layer(p: Problem, q_win, k, v, srh_mask, budget: int, id
         ctypes.byref(p.c), _ptr(q_win), _ptr(k), _ptr(v), m.ctypes.data, int(budget), _ptr(idx),
         _ptr(k_out), _ptr(v_out), _ptr(scores_or_null), _ptr(ws),
         ws.numel() if ws is not None else 0, _stream(stream)))
+
+
+def compresskv_compress_layer_noalloc(p: Problem, q_win, k, v, srh_mask, budget: int, idx, k_out,
+                                      v_out, scores_or_null, stream=None) -> None:
+    m = _mask(srh_mask)
+    _check("compresskv_compress_layer_noalloc", lib().compresskv_compress_layer_noalloc(
+        ctypes.byref(p.c), _ptr(q_win), _ptr(k), _ptr(v), m.ctypes.data, int(budget), _ptr(idx),
+        _ptr(k_out), _ptr(v_out), _ptr(scores_or_null), _stream(stream)))
 
 
 def _masks(srh_masks, n_q_heads: int) -> np.ndarray:

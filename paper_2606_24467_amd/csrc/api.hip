@@ -6,6 +6,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -826,6 +827,72 @@ int compresskv_compress_layer(const ckv_problem *p, const void *q_win, const voi
   ga.l0 = layer_desc(nullptr, nullptr, k, v, nullptr, idx, k_out, v_out, budget);
   if ((st = hip_status(ckv::launch_gather(ga, 0, budget, s), "gather"))) return st;
   return ok();
+}
+
+}  // extern "C"
+
+namespace {
+
+// Scratch of compresskv_compress_layer_noalloc: one array per device, kept
+// until the process ends.  In host code `scratch` names a host-side stand-in;
+// its device address comes from hipGetSymbolAddress, once per device, with
+// that device current.
+constexpr size_t kScratchBytes = 32u << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices];
+
+// The current device's scratch address (nullptr and a failure message if the
+// lookup fails).
+void *device_scratch() {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    fail(CKV_HIP_ERROR, "hipGetDevice failed: %s", hipGetErrorString(e));
+    return nullptr;
+  }
+  if (dev < 0 || dev >= kMaxDevices) {
+    fail(CKV_UNSUPPORTED, "device %d: at most %d devices", dev, kMaxDevices);
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) {
+      fail(CKV_HIP_ERROR, "hipGetSymbolAddress(scratch) failed: %s", hipGetErrorString(e));
+      return nullptr;
+    }
+    g_scratch_ptr[dev] = ptr;
+  }
+  return g_scratch_ptr[dev];
+}
+
+}  // namespace
+
+extern "C" {
+
+int compresskv_compress_layer_noalloc(const ckv_problem *p, const void *q_win, const void *k,
+                                      const void *v, const uint8_t *srh_mask_host,
+                                      int32_t budget, int32_t *idx, void *k_out, void *v_out,
+                                      float *scores_or_null, void *stream) {
+  Plan pl;
+  int st;
+  if ((st = check_problem(p))) return st;
+  if ((st = check_mask(p, srh_mask_host, pl))) return st;
+  if ((st = check_budget(p, budget))) return st;
+  make_plan(p, 1, pl, false);
+  if (pl.total > kScratchBytes)
+    return fail(CKV_WORKSPACE_TOO_SMALL,
+                "the problem needs %zu bytes of scratch; the allocation-free entry point has "
+                "%zu (use compresskv_compress_layer with a workspace)",
+                pl.total, kScratchBytes);
+  void *ws = device_scratch();
+  if (!ws) return CKV_HIP_ERROR;
+  return compresskv_compress_layer(p, q_win, k, v, srh_mask_host, budget, idx, k_out, v_out,
+                                   scores_or_null, ws, kScratchBytes, stream);
 }
 
 size_t compresskv_layers_workspace_bytes(const ckv_problem *p, int32_t n_layers,
