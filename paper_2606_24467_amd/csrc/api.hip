@@ -49,6 +49,8 @@ struct Plan {
   size_t table_off = 0, scores_off = 0, counters_off = 0, arrive_off = 0, bias_off = 0,
          hist_off = 0, stats_off = 0, skip_off = 0, edges_off = 0, total = 0;
   int64_t stats_layer = 0, hist_layer = 0;   // elements per layer
+  int sel_slices = 0;      // slices of the split selection (0: one workgroup per selection)
+  size_t sel_meta_off = 0, sel_cand_off = 0;
   int max_parts = 0;       // partial-statistics slots per group in the workspace
   // single-pass scoring
   bool op_shape = false;   // the problem's shape allows it (its workspace is reserved)
@@ -314,6 +316,20 @@ void set_layout(const ckv_problem *p, Plan &pl) {
     pl.total = pl.edges_off +
                round_up(units * (size_t)pl.nmax * 2 * pl.ew * sizeof(float), 256);
   }
+  // Selections over more than one slice of prefix positions are split over
+  // their slices (per-group index sets, whose first digit the column sums
+  // count).
+  pl.sel_slices = 0;
+  const int pmax = pl.lmax - p->window;
+  if (p->index_mode == CKV_INDEX_PER_GROUP && pmax > ckv::kSelSlice &&
+      pmax <= ckv::kSelSlice * ckv::kMaxSelSlices) {
+    const int ns = (pmax + ckv::kSelSlice - 1) / ckv::kSelSlice;
+    pl.sel_slices = ns;
+    pl.sel_meta_off = round_up(pl.total, 256);
+    pl.sel_cand_off =
+        pl.sel_meta_off + round_up(lg * (ckv::kSelMetaHead + 4 * (size_t)ns) * sizeof(int), 256);
+    pl.total = pl.sel_cand_off + round_up(lg * ns * (size_t)ckv::kSelSliceCap * 4, 256);
+  }
 }
 
 // One-chunk workgroups at the end of the multi-layer scoring grids, per
@@ -428,7 +444,8 @@ int hip_status(hipError_t e, const char *what) {
   return CKV_OK;
 }
 
-ckv::SelectArgs select_args(const ckv_problem *p, const Plan &pl, const int *hist) {
+// ws: the call's workspace (NULL: no split selection).
+ckv::SelectArgs select_args(const ckv_problem *p, const Plan &pl, const int *hist, void *ws) {
   ckv::SelectArgs s{};
   s.layers = nullptr;
   s.hist = hist;
@@ -442,6 +459,12 @@ ckv::SelectArgs select_args(const ckv_problem *p, const Plan &pl, const int *his
   s.n_sel = shared ? 1 : p->n_kv_heads;
   s.out_groups = shared ? p->n_kv_heads : 1;
   if (shared) s.hist = nullptr;   // the histograms are per group: count the layer score
+  if (pl.sel_slices > 0 && s.hist && ws) {
+    s.sel_meta = reinterpret_cast<int *>(static_cast<char *>(ws) + pl.sel_meta_off);
+    s.sel_cand = reinterpret_cast<uint32_t *>(static_cast<char *>(ws) + pl.sel_cand_off);
+    s.n_slices = pl.sel_slices;
+    s.cand_cap = ckv::kSelSliceCap;
+  }
   return s;
 }
 
@@ -664,7 +687,7 @@ int run_layers(const ckv_problem *p, int n_layers, const LayerPtrs &lp, const ui
                        "combine")))
     return st;
   if (!full) return ok();
-  ckv::SelectArgs sa = select_args(p, pl, a.hist);
+  ckv::SelectArgs sa = select_args(p, pl, a.hist, ws);
   sa.layers = table;
   if ((st = hip_status(ckv::launch_select(sa, n_layers, s), "select"))) return st;
   ckv::GatherArgs ga = gather_args(p);
@@ -770,7 +793,7 @@ int compresskv_select(const ckv_problem *p, const float *scores, int32_t budget,
   if ((st = check_ptr(scores, "scores", 4)) || (st = check_ptr(idx, "idx", 4))) return st;
   Plan pl;
   pl.T = p->cu_seqlens_host[p->batch];
-  ckv::SelectArgs sa = select_args(p, pl, nullptr);
+  ckv::SelectArgs sa = select_args(p, pl, nullptr, nullptr);
   sa.l0 = layer_desc(nullptr, nullptr, nullptr, nullptr, const_cast<float *>(scores), idx,
                      nullptr, nullptr, budget);
   if ((st = hip_status(ckv::launch_select(sa, 0, (hipStream_t)stream), "select"))) return st;
@@ -820,7 +843,7 @@ int compresskv_compress_layer(const ckv_problem *p, const void *q_win, const voi
                        "combine")))
     return st;
   const int *hist = reinterpret_cast<const int *>(static_cast<char *>(ws) + pl.hist_off);
-  ckv::SelectArgs sa = select_args(p, pl, hist);
+  ckv::SelectArgs sa = select_args(p, pl, hist, ws);
   sa.l0 = layer_desc(nullptr, nullptr, nullptr, nullptr, scores, idx, nullptr, nullptr, budget);
   if ((st = hip_status(ckv::launch_select(sa, 0, s), "select"))) return st;
   ckv::GatherArgs ga = gather_args(p);
@@ -946,7 +969,7 @@ int compresskv_select_heads(const ckv_problem *p, const float *scores,
   if ((st = check_ptr(scores, "scores", 4)) || (st = check_ptr(idx, "idx", 4))) return st;
   Plan pl;
   pl.T = p->cu_seqlens_host[p->batch];
-  ckv::SelectArgs sa = select_args(p, pl, nullptr);
+  ckv::SelectArgs sa = select_args(p, pl, nullptr, nullptr);
   sa.gb = gb;
   sa.l0 = layer_desc(nullptr, nullptr, nullptr, nullptr, const_cast<float *>(scores), idx,
                      nullptr, nullptr, max_budget);
@@ -999,7 +1022,7 @@ int compresskv_compress_layer_heads(const ckv_problem *p, const void *q_win, con
   hipStream_t s = (hipStream_t)stream;
   if ((st = hip_status(launch_scoring(p, pl, q_win, k, scores, ws, s), "score"))) return st;
   const int *hist = reinterpret_cast<const int *>(static_cast<char *>(ws) + pl.hist_off);
-  ckv::SelectArgs sa = select_args(p, pl, hist);
+  ckv::SelectArgs sa = select_args(p, pl, hist, ws);
   sa.gb = gb;
   sa.l0 = layer_desc(nullptr, nullptr, nullptr, nullptr, scores, idx, nullptr, nullptr,
                      max_budget);

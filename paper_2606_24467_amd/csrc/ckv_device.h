@@ -206,7 +206,18 @@ struct SelectArgs {
   int32_t n_sel;           // selections per (layer, sequence): Hkv, or 1 (layer-shared set)
   int32_t out_groups;      // idx rows each selection writes: 1, or Hkv (layer-shared set)
   GroupBudgets gb;         // per-group budgets (single-layer calls), if gb.on
+  // Split selection (sequences longer than one slice; needs hist): per
+  // selection kSelMetaHead + 4 * n_slices meta words and n_slices lists of
+  // cand_cap candidates; NULL sel_meta selects one workgroup per selection.
+  int *sel_meta;
+  uint32_t *sel_cand;
+  int32_t n_slices, cand_cap;
 };
+
+constexpr int kSelSlice = 32768;       // positions per slice of the split selection
+constexpr int kMaxSelSlices = 64;      // longest prefix it takes: 64 slices
+constexpr int kSelSliceCap = kSelSlice;   // candidates kept per slice: all its positions
+constexpr int kSelMetaHead = 4;
 
 // Layer-shared index set: the layer score from the per-group scores.
 struct CombineArgs {

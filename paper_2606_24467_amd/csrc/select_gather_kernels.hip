@@ -22,9 +22,15 @@
 namespace ckv {
 
 constexpr int kSelThreads = 1024;
-constexpr int kCandCap = 4096;               // candidates of the first-digit bucket kept in LDS
-constexpr int kEpt = 32;                     // scores per thread held in registers per round
-constexpr int kRound = kSelThreads * kEpt;   // scores per round
+constexpr int kCandCap = 8192;               // candidates of the first-digit bucket kept in LDS
+// Scores per thread held in registers per round: the split selection's
+// slices are one round of kEpt; a whole selection in one workgroup uses
+// kEptWhole (fewer registers held across all its passes).
+constexpr int kEpt = 32;
+constexpr int kRound = kSelThreads * kEpt;
+static_assert(kRound == kSelSlice, "a slice of the split selection is one round");
+constexpr int kEptWhole = 16;
+constexpr int kRoundWhole = kSelThreads * kEptWhole;
 
 // Inclusive prefix sum over the 1024 threads of the block; *total gets the sum.
 __device__ __forceinline__ int block_inclusive_scan(int x, int *lds_waves, int *total) {
@@ -91,12 +97,12 @@ __device__ __forceinline__ void find_bucket(const int *hist, int nb, int remain,
 }
 
 // Position of a thread's element e in the round starting at r0: every wave
-// owns a run of kWaveRun consecutive positions and its lanes take
+// owns a run of 64 * EPT consecutive positions and its lanes take
 // consecutive positions for each e, so a load instruction reads 256
 // contiguous bytes and the position order is (wave, e, lane).
-constexpr int kWaveRun = 64 * kEpt;
+template <int EPT>
 __device__ __forceinline__ int elem_pos(int r0, int e) {
-  return r0 + (int)(threadIdx.x >> 6) * kWaveRun + e * 64 + (int)(threadIdx.x & 63);
+  return r0 + (int)(threadIdx.x >> 6) * (64 * EPT) + e * 64 + (int)(threadIdx.x & 63);
 }
 
 // Lanes below this one whose bit is set in m.
@@ -105,188 +111,564 @@ __device__ __forceinline__ int lanes_below(unsigned long long m) {
                                         __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
 }
 
-// A thread's kEpt scores of the round starting at r0 into registers (all
-// loads issued together); positions >= P read as 0 and are masked by the
-// callers.
+// A thread's EPT scores of the round starting at r0 into registers, all
+// loads issued together.  They go through a buffer resource whose range is
+// the P prefix scores, so positions >= P read as 0 without a branch or a
+// clamp (the callers mask them).
+template <int EPT>
 __device__ __forceinline__ void load_round(gptr<const uint32_t> sc, int P, int r0,
-                                           uint32_t (&v)[kEpt]) {
+                                           uint32_t (&v)[EPT]) {
+  // raw buffer (stride 0), 32-bit data format; range P * 4 bytes
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)sc, (short)0, P * 4, 0x00020000);
+  const int off = elem_pos<EPT>(r0, 0) * 4;
 #pragma unroll
-  for (int e = 0; e < kEpt; ++e) {
-    const int j = elem_pos(r0, e);
-    v[e] = (j < P) ? sc[j] : 0u;
+  for (int e = 0; e < EPT; ++e) v[e] = __builtin_amdgcn_raw_buffer_load_b32(rs, off + e * 256, 0, 0);
+}
+
+// One selection: (layer, sequence b, selection index g) with its operands.
+struct Sel {
+  LayerView lv;
+  int layer, b, g, budget, L, P, k;
+  int64_t id;                    // (layer * batch + b) * n_sel + g
+  gptr<int32_t> out;             // the kept list of (b, g)
+  gptr<const uint32_t> sc;       // the selection's scores, position 0 of the sequence
+};
+
+// lb = layer * batch + b.
+template <bool ML>
+__device__ __forceinline__ Sel sel_of(const SelectArgs &a, int g, int lb) {
+  Sel s;
+  s.g = g;
+  s.layer = ML ? lb / a.batch : 0;
+  s.b = lb - s.layer * a.batch;
+  s.lv = layer_view<ML>(a, s.layer, 0);
+  s.budget = a.gb.on ? a.gb.budget[g] : s.lv.budget;
+  const int s0 = a.cu[s.b];
+  s.L = a.cu[s.b + 1] - s0;
+  s.P = s.L - a.W;
+  s.k = s.budget - a.W;           // prefix tokens to keep when L > budget: 0 <= k < P
+  s.id = (int64_t)lb * a.n_sel + g;
+  s.out = s.lv.idx + kept_base(a.gb, s.b, g, a.Hkv, s.budget);
+  s.sc = reinterpret_cast<gptr<const uint32_t>>(s.lv.scores + (int64_t)g * a.T + s0);
+  return s;
+}
+
+// Position `pos` of the kept list, in every idx row this selection serves.
+__device__ __forceinline__ void sel_put(const SelectArgs &a, const Sel &s, int pos, int32_t val) {
+  for (int r = 0; r < a.out_groups; ++r) s.out[(int64_t)r * s.budget + pos] = val;
+}
+
+// The part of the kept list that needs no selection: everything when
+// L <= budget (slots past L get -1), else the window positions.  True when
+// nothing is left to select.
+__device__ __forceinline__ bool sel_trivial(const SelectArgs &a, const Sel &s) {
+  const int tid = threadIdx.x;
+  if (s.L <= s.budget) {
+    for (int j = tid; j < s.budget; j += kSelThreads) sel_put(a, s, j, (j < s.L) ? j : -1);
+    return true;
+  }
+  for (int w = tid; w < a.W; w += kSelThreads) sel_put(a, s, s.k + w, s.P + w);
+  return s.k == 0;
+}
+
+// The first-digit histogram of a selection into LDS: from the column-sum
+// kernel's, or counted over the prefix scores.
+__device__ __forceinline__ void sel_hist1(const SelectArgs &a, const Sel &s, int *hist,
+                                          uint32_t (&v)[kEptWhole], bool resident, int nrounds) {
+  const int tid = threadIdx.x;
+  if (a.hist) {
+    const int *hg = a.hist + s.layer * a.hist_layer + ((int64_t)s.b * a.Hkv + s.g) * kHistBins;
+    for (int i = tid; i < kHistBins; i += kSelThreads) hist[i] = hg[i];
+    return;
+  }
+  for (int i = tid; i < kHistBins; i += kSelThreads) hist[i] = 0;
+  __syncthreads();
+  for (int r = 0; r < nrounds; ++r) {
+    if (!resident) load_round(s.sc, s.P, r * kRoundWhole, v);
+#pragma unroll
+    for (int e = 0; e < kEptWhole; ++e)
+      hist_add(hist, hist_bin(v[e]), elem_pos<kEptWhole>(r * kRoundWhole, e) < s.P);
   }
 }
 
-// Grid (Hkv, batch [x layers]), 1024 threads.
-template <bool ML>
-__global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a) {
-  const int g = blockIdx.x;         // selection index: the KV group, or 0 (layer-shared set)
-  const int layer = ML ? (int)blockIdx.y / a.batch : 0;
-  const int b = (int)blockIdx.y - layer * a.batch;
-  const LayerView lv = layer_view<ML>(a, layer, 0);
-  const int budget = a.gb.on ? a.gb.budget[g] : lv.budget;
+// Slot of this lane in a list that the wave appends its flagged lanes to
+// (one LDS atomic per wave); every lane of the wave must reach it.
+__device__ __forceinline__ int wave_append(int *count, bool flag) {
+  const unsigned long long m = __ballot(flag);
+  if (m == 0ull) return 0;
+  const int leader = __ffsll((unsigned long long)m) - 1;
+  int base = 0;
+  if ((int)(threadIdx.x & 63) == leader) base = atomicAdd(count, (int)__popcll(m));
+  base = __shfl(base, leader);
+  return base + lanes_below(m);
+}
+
+// Ordered compaction of the round starting at r0 (this thread's scores in v):
+// keeps the elements above thr and, of those equal to it, the ones whose rank
+// among the sequence's ties (eq_base ties come before this round) is below
+// `remain`; writes them from kept-list position pos_base on, in position
+// order.  Each wave counts its elements above and at the threshold, every
+// wave forms the prefix over the waves before it, and the kept positions are
+// written in (wave, e, lane) order.  Returns the kept count through *kept
+// and the tie count through *ties.
+template <int EPT>
+__device__ __forceinline__ void compact_round(const SelectArgs &a, const Sel &s,
+                                              const uint32_t (&v)[EPT], int r0, uint32_t thr,
+                                              int remain, int pos_base, int eq_base,
+                                              int (*wave_cnt)[kSelThreads / 64], int *kept,
+                                              int *ties) {
   const int tid = threadIdx.x;
-  const int s0 = a.cu[b];
-  const int L = a.cu[b + 1] - s0;
-  const gptr<int32_t> out = lv.idx + kept_base(a.gb, b, g, a.Hkv, budget);
-  // position `pos` of the kept list, in every idx row this selection serves
-  auto put = [&](int pos, int32_t val) {
-    for (int r = 0; r < a.out_groups; ++r) out[(int64_t)r * budget + pos] = val;
-  };
-  if (L <= budget) {
-    for (int j = tid; j < budget; j += kSelThreads) put(j, (j < L) ? j : -1);
-    return;
+  const int lane = tid & 63, wave = tid >> 6;
+  int n_gt = 0, n_eq = 0;   // this thread's counts, then the wave's
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    const uint32_t u = v[e] & 0x7FFFFFFFu;
+    const bool ok = elem_pos<EPT>(r0, e) < s.P;
+    n_gt += ok && u > thr;
+    n_eq += ok && u == thr;
   }
-  const int P = L - a.W;
-  const int k = budget - a.W;       // prefix tokens to keep, 0 <= k < P
-  for (int w = tid; w < a.W; w += kSelThreads) put(k + w, P + w);
-  if (k == 0) return;
-  const gptr<const uint32_t> sc =
-      reinterpret_cast<gptr<const uint32_t>>(lv.scores + (int64_t)g * a.T + s0);
-  const int nrounds = (P + kRound - 1) / kRound;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    n_gt += __shfl_xor(n_gt, o);
+    n_eq += __shfl_xor(n_eq, o);
+  }
+  if (lane == 0) {
+    wave_cnt[0][wave] = n_gt;
+    wave_cnt[1][wave] = n_eq;
+  }
+  __syncthreads();
+  int eq_before = 0, sel_before = 0, eq_total = 0, sel_total = 0;
+#pragma unroll
+  for (int x = 0; x < kSelThreads / 64; ++x) {
+    const int c_gt = wave_cnt[0][x], c_eq = wave_cnt[1][x];
+    const int take = max(0, min(c_eq, remain - (eq_base + eq_total)));   // wave x's kept ties
+    if (x < wave) {
+      eq_before += c_eq;
+      sel_before += c_gt + take;
+    }
+    eq_total += c_eq;
+    sel_total += c_gt + take;
+  }
+  __syncthreads();   // wave_cnt is rewritten by the next round
+  int pos = pos_base + sel_before;
+  int eq_rank = eq_base + eq_before;
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    const int j = elem_pos<EPT>(r0, e);
+    const uint32_t u = v[e] & 0x7FFFFFFFu;
+    const bool ok = j < s.P;
+    const bool gt = ok && u > thr, eq = ok && u == thr;
+    const unsigned long long m_gt = __ballot(gt), m_eq = __ballot(eq);
+    if ((m_gt | m_eq) == 0ull) continue;   // nothing kept at this e (uniform; most e)
+    const bool keep = gt || (eq && eq_rank + lanes_below(m_eq) < remain);
+    const unsigned long long m_keep = __ballot(keep);
+    const int my_pos = pos + lanes_below(m_keep);
+    if (keep && my_pos < s.k) sel_put(a, s, my_pos, j);   // bound holds for finite scores; guards NaN
+    pos += __popcll(m_keep);
+    eq_rank += __popcll(m_eq);
+  }
+  *kept = sel_total;
+  *ties = eq_total;
+}
+
+struct SelLds {
+  int hist[kHistBins];
+  int scan_tmp[kSelThreads / 64];
+  int wave_cnt[2][kSelThreads / 64];
+  int bucket, remain, ncand;
+  uint32_t cand_u[kCandCap];
+};
+
+// The whole selection in one workgroup (after sel_trivial): digit 1 from the
+// histogram, the elements of its bucket collected in LDS, digits 2 (bits
+// 19..9) and 3 (bits 8..0) on that list (or, if it overflows, on every
+// prefix element that matches so far), then the ordered compaction, round by
+// round.
+__device__ __forceinline__ void select_whole(const SelectArgs &a, const Sel &s, SelLds &lds) {
+  const int tid = threadIdx.x;
+  const int nrounds = (s.P + kRoundWhole - 1) / kRoundWhole;
   const bool resident = (nrounds == 1);   // scores stay in registers for every pass
-
-  __shared__ int hist[kHistBins];
-  __shared__ int scan_tmp[kSelThreads / 64];
-  __shared__ int wave_cnt[2][kSelThreads / 64];
-  __shared__ int bucket_s, remain_s, ncand_s;
-  __shared__ uint32_t cand_u[kCandCap];
-  __shared__ int cand_j[kCandCap];
-
-  uint32_t v[kEpt];
-  if (resident) load_round(sc, P, 0, v);
-
-  // Digit 1: bits 30..20.
-  if (a.hist) {
-    const int *hg = a.hist + layer * a.hist_layer + ((int64_t)b * a.Hkv + g) * kHistBins;
-    for (int i = tid; i < kHistBins; i += kSelThreads) hist[i] = hg[i];
-  } else {
-    for (int i = tid; i < kHistBins; i += kSelThreads) hist[i] = 0;
-    __syncthreads();
-    for (int r = 0; r < nrounds; ++r) {
-      if (!resident) load_round(sc, P, r * kRound, v);
-#pragma unroll
-      for (int e = 0; e < kEpt; ++e) hist_add(hist, hist_bin(v[e]), elem_pos(r * kRound, e) < P);
-    }
+  uint32_t v[kEptWhole];
+  if (resident) load_round(s.sc, s.P, 0, v);
+  sel_hist1(a, s, lds.hist, v, resident, nrounds);
+  if (tid == 0) {
+    lds.ncand = 0;
+    lds.bucket = 0;
+    lds.remain = 0;
   }
-  if (tid == 0) ncand_s = 0;
   __syncthreads();
-  find_bucket(hist, kHistBins, k, scan_tmp, &bucket_s, &remain_s);
+  find_bucket(lds.hist, kHistBins, s.k, lds.scan_tmp, &lds.bucket, &lds.remain);
   uint32_t pmask = 0x7FFu << 20;
-  uint32_t prefix = (uint32_t)bucket_s << 20;
-  int remain = remain_s;
+  uint32_t prefix = (uint32_t)lds.bucket << 20;
+  int remain = lds.remain;
 
-  // Candidates: prefix elements whose first digit equals the chosen bucket.
   for (int r = 0; r < nrounds; ++r) {
-    if (!resident) load_round(sc, P, r * kRound, v);
+    if (!resident) load_round(s.sc, s.P, r * kRoundWhole, v);
 #pragma unroll
-    for (int e = 0; e < kEpt; ++e) {
-      const int j = elem_pos(r * kRound, e);
-      if (j < P && (v[e] & pmask) == prefix) {
-        const int slot = atomicAdd(&ncand_s, 1);
-        if (slot < kCandCap) {
-          cand_u[slot] = v[e];
-          cand_j[slot] = j;
-        }
-      }
+    for (int e = 0; e < kEptWhole; ++e) {
+      const bool c = elem_pos<kEptWhole>(r * kRoundWhole, e) < s.P && (v[e] & pmask) == prefix;
+      const int slot = wave_append(&lds.ncand, c);
+      if (c && slot < kCandCap) lds.cand_u[slot] = v[e];
     }
   }
   __syncthreads();
-  const int nc = ncand_s;
+  const int nc = lds.ncand;
   const bool in_lds = nc <= kCandCap;
 
-  // Digits 2 (bits 19..9) and 3 (bits 8..0) on the candidates (or, if they
-  // overflow the LDS list, on every prefix element that matches so far).
   const int shifts[2] = {9, 0};
   const int widths[2] = {11, 9};
   for (int pass = 0; pass < 2; ++pass) {
     const int sh = shifts[pass];
     const uint32_t dmask = (1u << widths[pass]) - 1u;
-    for (int i = tid; i < kHistBins; i += kSelThreads) hist[i] = 0;
+    for (int i = tid; i < kHistBins; i += kSelThreads) lds.hist[i] = 0;
     __syncthreads();
     if (in_lds) {
       for (int base = 0; base < nc; base += kSelThreads) {
         const int i = base + tid;
-        const uint32_t u = (i < nc) ? cand_u[i] : 0u;
-        hist_add(hist, (int)((u >> sh) & dmask), i < nc && (u & pmask) == prefix);
+        const uint32_t u = (i < nc) ? lds.cand_u[i] : 0u;
+        hist_add(lds.hist, (int)((u >> sh) & dmask), i < nc && (u & pmask) == prefix);
       }
     } else {
       for (int r = 0; r < nrounds; ++r) {
-        if (!resident) load_round(sc, P, r * kRound, v);
+        if (!resident) load_round(s.sc, s.P, r * kRoundWhole, v);
 #pragma unroll
-        for (int e = 0; e < kEpt; ++e)
-          hist_add(hist, (int)((v[e] >> sh) & dmask),
-                   elem_pos(r * kRound, e) < P && (v[e] & pmask) == prefix);
+        for (int e = 0; e < kEptWhole; ++e)
+          hist_add(lds.hist, (int)((v[e] >> sh) & dmask),
+                   elem_pos<kEptWhole>(r * kRoundWhole, e) < s.P && (v[e] & pmask) == prefix);
       }
     }
     __syncthreads();
-    find_bucket(hist, 1 << widths[pass], remain, scan_tmp, &bucket_s, &remain_s);
-    prefix |= (uint32_t)bucket_s << sh;
+    find_bucket(lds.hist, 1 << widths[pass], remain, lds.scan_tmp, &lds.bucket, &lds.remain);
+    prefix |= (uint32_t)lds.bucket << sh;
     pmask |= dmask << sh;
-    remain = remain_s;
+    remain = lds.remain;
     __syncthreads();
   }
 
-  // prefix is the exact bit pattern of the k-th largest score; `remain` of the
-  // positions holding it are kept (the lowest ones), plus every larger score.
-  // Ordered compaction, round by round: each wave counts its elements above
-  // and at the threshold, every wave forms the prefix over the waves before
-  // it, and the kept positions are written in (wave, e, lane) order.
-  const uint32_t thr = prefix;
-  const int lane = tid & 63, wave = tid >> 6;
+  // prefix is the exact bit pattern of the k-th largest score; `remain` of
+  // the positions holding it are kept (the lowest ones), plus every larger
+  // score.
   int pos_base = 0, eq_base = 0;
   for (int r = 0; r < nrounds; ++r) {
-    if (!resident) load_round(sc, P, r * kRound, v);
-    int n_gt = 0, n_eq = 0;   // this thread's counts, then the wave's
+    if (!resident) load_round(s.sc, s.P, r * kRoundWhole, v);
+    int kept, ties;
+    compact_round(a, s, v, r * kRoundWhole, prefix, remain, pos_base, eq_base, lds.wave_cnt, &kept,
+                  &ties);
+    pos_base += kept;
+    eq_base += ties;
+  }
+}
+
+// Grid (n_sel, batch [x layers]), 1024 threads: one selection per workgroup.
+template <bool ML>
+__global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a) {
+  const Sel s = sel_of<ML>(a, blockIdx.x, blockIdx.y);
+  if (sel_trivial(a, s)) return;
+  __shared__ SelLds lds;
+  select_whole(a, s, lds);
+}
+
+// Long sequences: the selection split over its rounds ("slices" of kRound
+// positions), in four launches with the same result as select_kernel.
+//  scan:    per slice, the count of elements above the first-digit bucket
+//           and the bucket's elements (its candidates) into the slice's list;
+//  resolve: per selection, digits 2 and 3 over all the slices' candidates,
+//           then each slice's first kept-list position and tie rank;
+//  write:   per slice, the ordered compaction from those offsets;
+//  rest:    the slices whose compaction did not fit the write kernel's LDS.
+// Meta words of a selection: [0] nothing left to select, [1] threshold, [2] ties kept, then
+// per slice: elements above the bucket, candidates, first kept position,
+// ties before it.
+__device__ __forceinline__ int *sel_meta(const SelectArgs &a, const Sel &s) {
+  return a.sel_meta + s.id * (kSelMetaHead + 4 * a.n_slices);
+}
+
+// Positions a wave of the write kernel stages in LDS (kept or tied); more
+// send its slice to select_rest_kernel.
+constexpr int kScanWaveCap = 512;
+
+// Grid (n_slices, n_sel, batch [x layers]), 1024 threads.
+template <bool ML>
+__global__ __launch_bounds__(kSelThreads) void select_scan_kernel(const SelectArgs a) {
+  const Sel s = sel_of<ML>(a, blockIdx.y, blockIdx.z);
+  const int slice = blockIdx.x;
+  const int r0 = slice * kRound;
+  if (s.L <= s.budget || s.k == 0 || r0 >= s.P) return;
+  const int tid = threadIdx.x;
+  __shared__ int hist[kHistBins];
+  __shared__ int scan_tmp[kSelThreads / 64];
+  __shared__ int bucket_s, remain_s, ncand_s, above_s;
+  uint32_t v[kEpt];
+  load_round(s.sc, s.P, r0, v);
+  const int *hg = a.hist + s.layer * a.hist_layer + ((int64_t)s.b * a.Hkv + s.g) * kHistBins;
+  for (int i = tid; i < kHistBins; i += kSelThreads) hist[i] = hg[i];
+  if (tid == 0) {
+    bucket_s = 0;
+    remain_s = 0;
+    ncand_s = 0;
+    above_s = 0;
+  }
+  __syncthreads();
+  find_bucket(hist, kHistBins, s.k, scan_tmp, &bucket_s, &remain_s);
+  const int bucket = bucket_s;
+  // elements above the bucket (counted) and in it (appended to the slice's
+  // list in no particular order: the resolve kernel only counts them)
+  const gptr<uint32_t> cand =
+      to_global(a.sel_cand) + (s.id * a.n_slices + slice) * (int64_t)a.cand_cap;
+  int n_above = 0;
+#pragma unroll
+  for (int e = 0; e < kEpt; ++e) {
+    const bool ok = elem_pos<kEpt>(r0, e) < s.P;
+    const int bin = hist_bin(v[e]);
+    n_above += (int)__popcll(__ballot(ok && bin > bucket));
+    const bool c = ok && bin == bucket;
+    const int at = wave_append(&ncand_s, c);
+    if (c && at < a.cand_cap) cand[at] = v[e];
+  }
+  if ((tid & 63) == 0) atomicAdd(&above_s, n_above);
+  __syncthreads();
+  if (tid == 0) {
+    int *meta = sel_meta(a, s);
+    meta[kSelMetaHead + slice] = above_s;
+    meta[kSelMetaHead + a.n_slices + slice] = ncand_s;
+  }
+}
+
+// Candidates per thread per pass of the resolve kernel when they are read
+// from the slices' lists.
+constexpr int kResolveEpt = 8;
+
+// Grid (n_sel, batch [x layers]), 1024 threads.
+template <bool ML>
+__global__ __launch_bounds__(kSelThreads) void select_resolve_kernel(const SelectArgs a) {
+  const Sel s = sel_of<ML>(a, blockIdx.x, blockIdx.y);
+  const int tid = threadIdx.x;
+  int *meta = sel_meta(a, s);
+  if (sel_trivial(a, s)) {
+    if (tid == 0) meta[0] = 1;
+    return;
+  }
+  __shared__ SelLds lds;
+  __shared__ int cand_off[kMaxSelSlices + 1], gt[kMaxSelSlices], eq[kMaxSelSlices];
+  const int ns = (s.P + kRound - 1) / kRound;
+  const int nsl = a.n_slices;
+  if (tid == 0) {
+    lds.bucket = 0;
+    lds.remain = 0;
+  }
+  const int *hg = a.hist + s.layer * a.hist_layer + ((int64_t)s.b * a.Hkv + s.g) * kHistBins;
+  for (int i = tid; i < kHistBins; i += kSelThreads) lds.hist[i] = hg[i];
+  if (tid < ns) {
+    gt[tid] = meta[kSelMetaHead + tid];
+    eq[tid] = 0;
+    cand_off[tid + 1] = meta[kSelMetaHead + nsl + tid];   // <= cand_cap: a slice's positions
+  }
+  __syncthreads();
+  if (tid == 0) {
+    cand_off[0] = 0;
+    for (int sl = 0; sl < ns; ++sl) cand_off[sl + 1] += cand_off[sl];
+  }
+  find_bucket(lds.hist, kHistBins, s.k, lds.scan_tmp, &lds.bucket, &lds.remain);
+  uint32_t prefix = (uint32_t)lds.bucket << 20;
+  int remain = lds.remain;
+  const int nc = cand_off[ns];
+  const gptr<const uint32_t> cand0 = to_global(a.sel_cand) + s.id * nsl * (int64_t)a.cand_cap;
+  // The candidates into LDS, slices in order (more than fit: read from the
+  // slices' lists on every pass, kResolveEpt per thread at a time).
+  const bool in_lds = nc <= kCandCap;
+  if (in_lds) {
+    for (int sl = 0; sl < ns; ++sl) {
+      const int n = cand_off[sl + 1] - cand_off[sl];
+      const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+          (void *)(cand0 + sl * (int64_t)a.cand_cap), (short)0, n * 4, 0x00020000);
+      for (int base = 0; base < n; base += 4 * kSelThreads) {
+        uint32_t u[4];
+#pragma unroll
+        for (int m = 0; m < 4; ++m)
+          u[m] = __builtin_amdgcn_raw_buffer_load_b32(rs, (base + m * kSelThreads + tid) * 4, 0, 0);
+#pragma unroll
+        for (int m = 0; m < 4; ++m)
+          if (base + m * kSelThreads + tid < n)
+            lds.cand_u[cand_off[sl] + base + m * kSelThreads + tid] = u[m];
+      }
+    }
+  }
+  // fn(u, slice, valid) over every candidate, slice by slice; every thread
+  // makes the same calls.
+  auto each = [&](auto fn) {
+    for (int sl = 0; sl < ns; ++sl) {
+      const int n = cand_off[sl + 1] - cand_off[sl];
+      if (in_lds) {
+        for (int base = 0; base < n; base += kSelThreads) {
+          const int i = base + tid;
+          fn(i < n ? lds.cand_u[cand_off[sl] + i] : 0u, sl, i < n);
+        }
+      } else {
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+            (void *)(cand0 + sl * (int64_t)a.cand_cap), (short)0, n * 4, 0x00020000);
+        for (int base = 0; base < n; base += kResolveEpt * kSelThreads) {
+          uint32_t u[kResolveEpt];
+#pragma unroll
+          for (int m = 0; m < kResolveEpt; ++m)
+            u[m] = __builtin_amdgcn_raw_buffer_load_b32(rs, (base + m * kSelThreads + tid) * 4,
+                                                        0, 0);
+#pragma unroll
+          for (int m = 0; m < kResolveEpt; ++m)
+            fn(u[m], sl, base + m * kSelThreads + tid < n);
+        }
+      }
+    }
+  };
+  __syncthreads();
+  // digits 2 (bits 19..9) and 3 (bits 8..0) over the candidates
+  const int shifts[2] = {9, 0};
+  const int widths[2] = {11, 9};
+  uint32_t pmask = 0x7FFu << 20;
+  for (int pass = 0; pass < 2; ++pass) {
+    const int sh = shifts[pass];
+    const uint32_t dmask = (1u << widths[pass]) - 1u;
+    for (int i = tid; i < kHistBins; i += kSelThreads) lds.hist[i] = 0;
+    __syncthreads();
+    each([&](uint32_t u, int, bool ok) {
+      hist_add(lds.hist, (int)((u >> sh) & dmask), ok && (u & pmask) == prefix);
+    });
+    __syncthreads();
+    find_bucket(lds.hist, 1 << widths[pass], remain, lds.scan_tmp, &lds.bucket, &lds.remain);
+    prefix |= (uint32_t)lds.bucket << sh;
+    pmask |= dmask << sh;
+    remain = lds.remain;
+    __syncthreads();
+  }
+  const uint32_t thr = prefix;
+  // per slice: candidates above the threshold (added to the slice's count of
+  // elements above the bucket) and ties
+  each([&](uint32_t u, int sl, bool ok) {
+    const uint32_t x = u & 0x7FFFFFFFu;
+    const int n_gt = (int)__popcll(__ballot(ok && x > thr));
+    const int n_eq = (int)__popcll(__ballot(ok && x == thr));
+    if ((threadIdx.x & 63) == 0) {
+      if (n_gt) atomicAdd(&gt[sl], n_gt);
+      if (n_eq) atomicAdd(&eq[sl], n_eq);
+    }
+  });
+  __syncthreads();
+  if (tid == 0) {
+    int pos = 0, ties = 0;
+    for (int sl = 0; sl < ns; ++sl) {
+      meta[kSelMetaHead + 2 * nsl + sl] = pos;
+      meta[kSelMetaHead + 3 * nsl + sl] = ties;
+      pos += gt[sl] + max(0, min(eq[sl], remain - ties));
+      ties += eq[sl];
+    }
+    meta[1] = (int)thr;
+    meta[2] = remain;
+    meta[0] = 0;
+  }
+}
+
+// Grid (n_slices, n_sel, batch [x layers]), 1024 threads.  Each wave stages
+// the positions it may keep (above or at the threshold, ties flagged in bit
+// 31) in LDS in position order; after the waves' counts are exchanged, it
+// decides its ties and writes its kept positions.  A slice where some wave
+// has more than kScanWaveCap such positions is marked (-1 in its first meta
+// word, which the resolve kernel has read) and left to select_rest_kernel.
+template <bool ML>
+__global__ __launch_bounds__(kSelThreads) void select_write_kernel(const SelectArgs a) {
+  const Sel s = sel_of<ML>(a, blockIdx.y, blockIdx.z);
+  const int slice = blockIdx.x;
+  const int r0 = slice * kRound;
+  if (s.L <= s.budget || s.k == 0 || r0 >= s.P) return;
+  const int *meta = sel_meta(a, s);
+  if (meta[0]) return;   // nothing left to select
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  __shared__ uint32_t stage[kSelThreads / 64][kScanWaveCap];
+  __shared__ int wave_cnt[3][kSelThreads / 64];
+  const uint32_t thr = (uint32_t)meta[1];
+  const int remain = meta[2];
+  const int pos_base = meta[kSelMetaHead + 2 * a.n_slices + slice];
+  const int eq_base = meta[kSelMetaHead + 3 * a.n_slices + slice];
+  {
+    uint32_t v[kEpt];
+    load_round(s.sc, s.P, r0, v);
+    int n_gt = 0, n_eq = 0, n_st = 0;
 #pragma unroll
     for (int e = 0; e < kEpt; ++e) {
+      const int j = elem_pos<kEpt>(r0, e);
       const uint32_t u = v[e] & 0x7FFFFFFFu;
-      const bool ok = elem_pos(r * kRound, e) < P;
-      n_gt += ok && u > thr;
-      n_eq += ok && u == thr;
-    }
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-      n_gt += __shfl_xor(n_gt, o);
-      n_eq += __shfl_xor(n_eq, o);
+      const bool ok = j < s.P;
+      const bool gt = ok && u > thr, eq = ok && u == thr;
+      n_gt += (int)__popcll(__ballot(gt));
+      n_eq += (int)__popcll(__ballot(eq));
+      const unsigned long long m = __ballot(gt || eq);
+      const int at = n_st + lanes_below(m);
+      if ((gt || eq) && at < kScanWaveCap) stage[wave][at] = (uint32_t)j | (eq ? 0x80000000u : 0u);
+      n_st += (int)__popcll(m);
     }
     if (lane == 0) {
       wave_cnt[0][wave] = n_gt;
       wave_cnt[1][wave] = n_eq;
+      wave_cnt[2][wave] = n_st;
     }
-    __syncthreads();
-    int eq_before = 0, sel_before = 0, eq_total = 0, sel_total = 0;
+  }
+  __syncthreads();
+  bool full = false;
+  int eq_before = 0, sel_before = 0, eq_total = 0;
 #pragma unroll
-    for (int x = 0; x < kSelThreads / 64; ++x) {
-      const int c_gt = wave_cnt[0][x], c_eq = wave_cnt[1][x];
-      const int take = max(0, min(c_eq, remain - (eq_base + eq_total)));   // wave x's kept ties
-      if (x < wave) {
-        eq_before += c_eq;
-        sel_before += c_gt + take;
-      }
-      eq_total += c_eq;
-      sel_total += c_gt + take;
+  for (int x = 0; x < kSelThreads / 64; ++x) {
+    const int c_gt = wave_cnt[0][x], c_eq = wave_cnt[1][x];
+    const int take = max(0, min(c_eq, remain - (eq_base + eq_total)));   // wave x's kept ties
+    if (x < wave) {
+      eq_before += c_eq;
+      sel_before += c_gt + take;
     }
-    __syncthreads();   // wave_cnt is rewritten by the next round
-    int pos = pos_base + sel_before;
-    int eq_rank = eq_base + eq_before;
-#pragma unroll
-    for (int e = 0; e < kEpt; ++e) {
-      const int j = elem_pos(r * kRound, e);
-      const uint32_t u = v[e] & 0x7FFFFFFFu;
-      const bool ok = j < P;
-      const bool gt = ok && u > thr, eq = ok && u == thr;
-      const unsigned long long m_gt = __ballot(gt), m_eq = __ballot(eq);
-      if ((m_gt | m_eq) == 0ull) continue;   // nothing kept at this e (uniform; most e)
-      const bool keep = gt || (eq && eq_rank + lanes_below(m_eq) < remain);
-      const unsigned long long m_keep = __ballot(keep);
-      const int my_pos = pos + lanes_below(m_keep);
-      if (keep && my_pos < k) put(my_pos, j);   // bound holds for finite scores; guards NaN
-      pos += __popcll(m_keep);
-      eq_rank += __popcll(m_eq);
-    }
-    eq_base += eq_total;
-    pos_base += sel_total;
+    eq_total += c_eq;
+    full |= wave_cnt[2][x] > kScanWaveCap;
+  }
+  if (full) {   // left to select_rest_kernel
+    if (tid == 0) a.sel_meta[(s.id * (kSelMetaHead + 4 * a.n_slices)) + kSelMetaHead + slice] = -1;
+    return;
+  }
+  int pos = pos_base + sel_before;
+  int eq_rank = eq_base + eq_before;
+  const int n_st = wave_cnt[2][wave];
+  for (int i0 = 0; i0 < n_st; i0 += 64) {
+    const bool valid = i0 + lane < n_st;
+    const uint32_t x = valid ? stage[wave][i0 + lane] : 0u;
+    const bool eq = valid && (x >> 31);
+    const unsigned long long m_eq = __ballot(eq);
+    const bool keep = valid && (!eq || eq_rank + lanes_below(m_eq) < remain);
+    const unsigned long long m_keep = __ballot(keep);
+    const int my_pos = pos + lanes_below(m_keep);
+    if (keep && my_pos < s.k) sel_put(a, s, my_pos, (int)(x & 0x7FFFFFFFu));
+    pos += (int)__popcll(m_keep);
+    eq_rank += (int)__popcll(m_eq);
+  }
+}
+
+// Grid (n_slices, n_sel, batch [x layers]), 1024 threads: the slices that
+// select_write_kernel marked, by compact_round on the scores, half a slice at
+// a time.
+template <bool ML>
+__global__ __launch_bounds__(kSelThreads) void select_rest_kernel(const SelectArgs a) {
+  const Sel s = sel_of<ML>(a, blockIdx.y, blockIdx.z);
+  const int slice = blockIdx.x;
+  const int r0 = slice * kRound;
+  if (s.L <= s.budget || s.k == 0 || r0 >= s.P) return;
+  const int *meta = sel_meta(a, s);
+  if (meta[0] || meta[kSelMetaHead + slice] != -1) return;
+  __shared__ int wave_cnt[2][kSelThreads / 64];
+  const uint32_t thr = (uint32_t)meta[1];
+  const int remain = meta[2];
+  int pb = meta[kSelMetaHead + 2 * a.n_slices + slice];
+  int eb = meta[kSelMetaHead + 3 * a.n_slices + slice];
+  for (int h = 0; h < kRound / kRoundWhole; ++h) {
+    uint32_t v[kEptWhole];
+    load_round(s.sc, s.P, r0 + h * kRoundWhole, v);
+    int kept, ties;
+    compact_round(a, s, v, r0 + h * kRoundWhole, thr, remain, pb, eb, wave_cnt, &kept, &ties);
+    pb += kept;
+    eb += ties;
   }
 }
 
@@ -362,12 +744,26 @@ hipError_t launch_put_layers(const PutArgs &a, hipStream_t stream) {
 }
 
 hipError_t launch_select(const SelectArgs &a, int n_layers, hipStream_t stream) {
+  const int lb = a.batch * (n_layers > 0 ? n_layers : 1);
+  if (a.sel_meta) {
+    const dim3 slices(a.n_slices, a.n_sel, lb), sels(a.n_sel, lb);
+    if (n_layers > 0) {
+      hipLaunchKernelGGL(select_scan_kernel<true>, slices, dim3(kSelThreads), 0, stream, a);
+      hipLaunchKernelGGL(select_resolve_kernel<true>, sels, dim3(kSelThreads), 0, stream, a);
+      hipLaunchKernelGGL(select_write_kernel<true>, slices, dim3(kSelThreads), 0, stream, a);
+      hipLaunchKernelGGL(select_rest_kernel<true>, slices, dim3(kSelThreads), 0, stream, a);
+    } else {
+      hipLaunchKernelGGL(select_scan_kernel<false>, slices, dim3(kSelThreads), 0, stream, a);
+      hipLaunchKernelGGL(select_resolve_kernel<false>, sels, dim3(kSelThreads), 0, stream, a);
+      hipLaunchKernelGGL(select_write_kernel<false>, slices, dim3(kSelThreads), 0, stream, a);
+      hipLaunchKernelGGL(select_rest_kernel<false>, slices, dim3(kSelThreads), 0, stream, a);
+    }
+    return hipGetLastError();
+  }
   if (n_layers > 0)
-    hipLaunchKernelGGL(select_kernel<true>, dim3(a.n_sel, a.batch * n_layers), dim3(kSelThreads),
-                       0, stream, a);
+    hipLaunchKernelGGL(select_kernel<true>, dim3(a.n_sel, lb), dim3(kSelThreads), 0, stream, a);
   else
-    hipLaunchKernelGGL(select_kernel<false>, dim3(a.n_sel, a.batch), dim3(kSelThreads), 0, stream,
-                       a);
+    hipLaunchKernelGGL(select_kernel<false>, dim3(a.n_sel, lb), dim3(kSelThreads), 0, stream, a);
   return hipGetLastError();
 }
 
