@@ -59,8 +59,8 @@ int compresskv_select_srh(int32_t n_layers, int32_t heads_per_layer, const float
 /* Sizes of one layer's eviction-error estimate (the layer's shapes, dtype,
    strides, cu_seqlens and softmax scale come from its ckv_problem). */
 typedef struct ckv_error_problem {
-  int32_t n_steps;   /* T >= 1 decoding steps per sequence; T * (n_q_heads / n_kv_heads)
-                        <= 64 and batch * T <= 32 */
+  int32_t n_steps;   /* T >= 1 decoding steps per sequence (the kernels take blocks of
+                        steps and sequences; T is bounded by the workspace only) */
   int32_t d_model;   /* rows of W_O, >= 1 */
   int32_t budget;    /* B: rows per (sequence, group) of k_out / v_out, >= 1 */
   float eps;         /* >= 0, e.g. 1e-6 */

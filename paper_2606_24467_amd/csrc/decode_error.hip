@@ -13,7 +13,11 @@
 //                       vectors); per-workgroup sums of y^2
 //   dec_error_kernel    the per-step norms, their ratios and the layer sum
 //
-// Every reduction runs in a fixed order, so the result is deterministic.
+// The kernels take a block of at most kMaxVectors (sequence, step) vectors
+// whose rows per group (steps x query heads of the group) fit kMaxDecRows;
+// longer decodes and larger batches run block after block, each adding its
+// ratios to the sum.  Every reduction runs in a fixed order, so the result is
+// deterministic.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -28,19 +32,22 @@ namespace ckv {
 constexpr int kDecChunk = 256;   // keys per attention workgroup
 constexpr int kDecSub = 64;      // keys per softmax step inside it (one tile per wave)
 constexpr int kProjRows = 16;    // W_O rows per projection workgroup
-constexpr int kMaxDecRows = 64;  // decoding steps x query heads per group
-constexpr int kMaxVectors = 32;  // sequences x decoding steps
+constexpr int kMaxDecRows = 64;  // decoding steps x query heads per group, per block
+constexpr int kMaxVectors = 32;  // sequences x decoding steps, per block
 
+// One block: sequences b0 .. b0 + batch - 1, steps t0 .. t0 + T - 1; the
+// partials and A are indexed by the block's own sequence and step.
 struct DecArgs {
-  const char *q;                 // [batch][T][Hq][D]
+  const char *q;                 // [all sequences][q_T][Hq][D]
   const char *k, *v;             // full caches, byte strides below
-  const char *k_out, *v_out;     // compact caches [batch][Hkv][B][D]
+  const char *k_out, *v_out;     // compact caches [all sequences][Hkv][B][D]
   const int32_t *cu;
   float2 *part_ml;               // [2][batch][Hkv][n_chunks][64] (max, sum), log2 domain
   float *part_o;                 // [2][batch][Hkv][n_chunks][64][D]
   float *a;                      // [2][batch][T][Hq][D]
   int64_t k_st, k_sh, v_st, v_sh;
   int T, Hq, Hkv, G, B, batch, R, n_chunks;
+  int b0, t0, q_T;               // the block's first sequence and step; steps in q
   float c1;                      // softmax scale * log2(e)
 };
 
@@ -87,7 +94,7 @@ __global__ __launch_bounds__(256) void dec_attn_kernel(const DecArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int c = lane & 15, quad = lane >> 4;
   const int g = blockIdx.y, b = (int)blockIdx.z >> 1, cache = (int)blockIdx.z & 1;
-  const DecCache cc = dec_cache<T, D>(a, cache, b, g);
+  const DecCache cc = dec_cache<T, D>(a, cache, a.b0 + b, g);
   const int c0 = (int)blockIdx.x * kDecChunk;
   if (c0 >= cc.n_keys) return;   // uniform
   const int c_end = min(cc.n_keys, c0 + kDecChunk);
@@ -104,7 +111,8 @@ __global__ __launch_bounds__(256) void dec_attn_kernel(const DecArgs a) {
     uint4 val = make_uint4(0, 0, 0, 0);
     if (r < a.R) {
       const int t = r / a.G, h = g * a.G + (r - t * a.G);
-      val = load16(to_global(a.q) + (((int64_t)b * a.T + t) * a.Hq + h) * (D * (int64_t)sizeof(T)) +
+      val = load16(to_global(a.q) +
+                   (((int64_t)(a.b0 + b) * a.q_T + a.t0 + t) * a.Hq + h) * (D * (int64_t)sizeof(T)) +
                    16 * u);
     }
     q_lds[r * STRIDE + u] = val;
@@ -248,7 +256,7 @@ __global__ __launch_bounds__(D) void dec_combine_kernel(const DecArgs a) {
   __shared__ float red[D];
   const int r = blockIdx.x, g = blockIdx.y, b = (int)blockIdx.z >> 1, cache = (int)blockIdx.z & 1;
   const int d = threadIdx.x;
-  const int L = a.cu[b + 1] - a.cu[b];
+  const int L = a.cu[a.b0 + b + 1] - a.cu[a.b0 + b];
   const int n_keys = cache == 0 ? L : min(L, a.B);
   const int nch = (n_keys + kDecChunk - 1) / kDecChunk;
   const int64_t slot0 = (((int64_t)cache * a.batch + b) * a.Hkv + g) * a.n_chunks;
@@ -364,10 +372,11 @@ __global__ __launch_bounds__(256) void dec_proj_kernel(const ProjArgs p) {
 // One workgroup of kMaxVectors waves' worth of lanes: wave n sums vector n's
 // squares over the projection workgroups (lane l: workgroups l, l + 64, ...
 // in order, then a fixed butterfly), forms the ratio, and thread 0 adds the
-// ratios in vector order.
+// ratios in vector order, to zero (first block) or to the sum so far.
 __global__ __launch_bounds__(64 * kMaxVectors / 2) void dec_error_kernel(const float *part_ss,
                                                                         int n_wg, int NV,
-                                                                        float eps, float *err) {
+                                                                        float eps, int first,
+                                                                        float *err) {
   __shared__ float ratio[kMaxVectors];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   for (int n = wave; n < NV; n += blockDim.x / 64) {
@@ -385,7 +394,7 @@ __global__ __launch_bounds__(64 * kMaxVectors / 2) void dec_error_kernel(const f
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    float e = 0.f;
+    float e = first ? 0.f : err[0];
     for (int n = 0; n < NV; ++n) e += ratio[n];
     err[0] = e;
   }
@@ -393,7 +402,7 @@ __global__ __launch_bounds__(64 * kMaxVectors / 2) void dec_error_kernel(const f
 
 template <typename T, int D>
 static void launch_dec_t(const DecArgs &a, const ProjArgs &pa, int rt, int n_wg, float eps,
-                         float *err, hipStream_t s) {
+                         bool first, float *err, hipStream_t s) {
   const dim3 g1(a.n_chunks, a.Hkv, a.batch * 2);
   switch (rt) {
     case 1: hipLaunchKernelGGL((dec_attn_kernel<T, D, 1>), g1, dim3(256), 0, s, a); break;
@@ -409,7 +418,7 @@ static void launch_dec_t(const DecArgs &a, const ProjArgs &pa, int rt, int n_wg,
     default: hipLaunchKernelGGL((dec_proj_kernel<T, 4>), dim3(n_wg), dim3(256), 0, s, pa); break;
   }
   hipLaunchKernelGGL(dec_error_kernel, dim3(1), dim3(64 * kMaxVectors / 2), 0, s, pa.part_ss, n_wg,
-                     pa.NV, eps, err);
+                     pa.NV, eps, first ? 1 : 0, err);
 }
 
 }  // namespace ckv
@@ -420,7 +429,8 @@ using ckv_api::fail;
 using ckv_api::ok;
 
 struct DecPlan {
-  int R = 0, rt = 0, n_chunks = 0, n_wg = 0, NV = 0, lmax = 0;
+  int TS = 0, BS = 0;      // steps and sequences per block
+  int R = 0, rt = 0, n_chunks = 0, n_wg = 0, NV = 0, lmax = 0;   // of a full block
   size_t ml_off = 0, o_off = 0, a_off = 0, ss_off = 0, total = 0;
 };
 
@@ -452,13 +462,12 @@ int check_error_problem(const ckv_problem *p, const ckv_error_problem *e, DecPla
   if (!(e->eps >= 0.f) || !std::isfinite(e->eps))
     return fail(CKV_INVALID_ARGUMENT, "eps must be finite and >= 0");
   const int G = p->n_q_heads / p->n_kv_heads;
-  pl.R = e->n_steps * G;
-  if (pl.R > ckv::kMaxDecRows)
-    return fail(CKV_UNSUPPORTED, "n_steps * (n_q_heads / n_kv_heads) must be <= %d",
-                ckv::kMaxDecRows);
-  pl.NV = p->batch * e->n_steps;
-  if (pl.NV > ckv::kMaxVectors)
-    return fail(CKV_UNSUPPORTED, "batch * n_steps must be <= %d", ckv::kMaxVectors);
+  if (G > ckv::kMaxDecRows)
+    return fail(CKV_UNSUPPORTED, "n_q_heads / n_kv_heads must be <= %d", ckv::kMaxDecRows);
+  pl.TS = std::min({ckv::kMaxDecRows / G, ckv::kMaxVectors, e->n_steps});
+  pl.BS = std::min(p->batch, ckv::kMaxVectors / pl.TS);
+  pl.R = pl.TS * G;
+  pl.NV = pl.BS * pl.TS;
   if ((p->n_q_heads * p->head_dim) % 256 != 0)
     return fail(CKV_UNSUPPORTED, "n_q_heads * head_dim must be a multiple of 256");
   pl.lmax = 0;
@@ -470,7 +479,7 @@ int check_error_problem(const ckv_problem *p, const ckv_error_problem *e, DecPla
   pl.rt = (pl.R + 15) / 16;
   pl.n_chunks = (pl.lmax + ckv::kDecChunk - 1) / ckv::kDecChunk;
   pl.n_wg = (e->d_model + ckv::kProjRows - 1) / ckv::kProjRows;
-  const size_t slots = (size_t)2 * p->batch * p->n_kv_heads * pl.n_chunks * ckv::kMaxDecRows;
+  const size_t slots = (size_t)2 * pl.BS * p->n_kv_heads * pl.n_chunks * ckv::kMaxDecRows;
   pl.ml_off = 0;
   pl.o_off = round256(slots * sizeof(float2));
   pl.a_off = pl.o_off + round256(slots * p->head_dim * sizeof(float));
@@ -527,14 +536,12 @@ int compresskv_layer_error(const ckv_problem *p, const ckv_error_problem *e, con
   a.k_sh = p->k_stride_head * es;
   a.v_st = p->v_stride_tok * es;
   a.v_sh = p->v_stride_head * es;
-  a.T = e->n_steps;
   a.Hq = p->n_q_heads;
   a.Hkv = p->n_kv_heads;
   a.G = p->n_q_heads / p->n_kv_heads;
   a.B = e->budget;
-  a.batch = p->batch;
-  a.R = pl.R;
   a.n_chunks = pl.n_chunks;
+  a.q_T = e->n_steps;
   const double scale = p->scale > 0.f ? (double)p->scale : 1.0 / std::sqrt((double)p->head_dim);
   a.c1 = (float)(scale * 1.4426950408889634);
   ckv::ProjArgs pa{};
@@ -543,18 +550,32 @@ int compresskv_layer_error(const ckv_problem *p, const ckv_error_problem *e, con
   pa.part_ss = reinterpret_cast<float *>(w + pl.ss_off);
   pa.d_model = e->d_model;
   pa.HD = p->n_q_heads * p->head_dim;
-  pa.NV = pl.NV;
   hipStream_t s = (hipStream_t)stream;
-  if (p->dtype == CKV_BF16) {
-    if (p->head_dim == 64)
-      ckv::launch_dec_t<__bf16, 64>(a, pa, pl.rt, pl.n_wg, e->eps, err, s);
-    else
-      ckv::launch_dec_t<__bf16, 128>(a, pa, pl.rt, pl.n_wg, e->eps, err, s);
-  } else {
-    if (p->head_dim == 64)
-      ckv::launch_dec_t<float, 64>(a, pa, pl.rt, pl.n_wg, e->eps, err, s);
-    else
-      ckv::launch_dec_t<float, 128>(a, pa, pl.rt, pl.n_wg, e->eps, err, s);
+  // blocks of sequences x steps, sequences outermost: the sum runs over the
+  // vectors (sequence, step) in that order
+  bool first = true;
+  for (int b0 = 0; b0 < p->batch; b0 += pl.BS) {
+    for (int t0 = 0; t0 < e->n_steps; t0 += pl.TS) {
+      a.b0 = b0;
+      a.t0 = t0;
+      a.batch = std::min(pl.BS, p->batch - b0);
+      a.T = std::min(pl.TS, e->n_steps - t0);
+      a.R = a.T * a.G;
+      pa.NV = a.batch * a.T;
+      const int rt = (a.R + 15) / 16;
+      if (p->dtype == CKV_BF16) {
+        if (p->head_dim == 64)
+          ckv::launch_dec_t<__bf16, 64>(a, pa, rt, pl.n_wg, e->eps, first, err, s);
+        else
+          ckv::launch_dec_t<__bf16, 128>(a, pa, rt, pl.n_wg, e->eps, first, err, s);
+      } else {
+        if (p->head_dim == 64)
+          ckv::launch_dec_t<float, 64>(a, pa, rt, pl.n_wg, e->eps, first, err, s);
+        else
+          ckv::launch_dec_t<float, 128>(a, pa, rt, pl.n_wg, e->eps, first, err, s);
+      }
+      first = false;
+    }
   }
   const hipError_t he = hipGetLastError();
   if (he != hipSuccess)

@@ -120,7 +120,7 @@ def test_allocate_budgets_validation(L):
 
 # -------------------------------------------------------------- layer error
 def _err_case(**kw):
-    c = _Case(**kw)
+    c = _Case(**{k: v for k, v in kw.items() if k in ("lens", "Hq", "Hkv", "D", "dtype")})
     e = C.CkvErrorProblem(n_steps=kw.get("T", 4), d_model=64, budget=32, eps=1e-6)
     return c, e
 
@@ -153,13 +153,24 @@ def test_layer_error_validation(L):
         assert _layer_error(L, c, e, **{n: FAKE + 8}) == C.UNSUPPORTED, n
     assert _layer_error(L, c, e, err=0) == C.INVALID_ARGUMENT
     for field, val, st in [("n_steps", 0, C.INVALID_ARGUMENT), ("d_model", 0, C.INVALID_ARGUMENT),
-                           ("budget", 0, C.INVALID_ARGUMENT), ("eps", -1.0, C.INVALID_ARGUMENT),
-                           ("n_steps", 17, C.UNSUPPORTED)]:     # 17 steps x 4 heads > 64 rows
+                           ("budget", 0, C.INVALID_ARGUMENT), ("eps", -1.0, C.INVALID_ARGUMENT)]:
         c2, e2 = _err_case()
         setattr(e2, field, val)
         assert _layer_error(L, c2, e2) == st, field
-    c3, e3 = _err_case(lens=tuple([50] * 9), T=4)                 # 9 x 4 vectors > 32
-    assert _layer_error(L, c3, e3) == C.UNSUPPORTED
+
+
+def test_layer_error_workspace_is_bounded_by_one_block(L):
+    """Decodes longer than one block of steps (16 at 4 query heads per group)
+    and batches larger than one block of vectors (32) run block after block:
+    the workspace does not grow with them."""
+    def need(T, lens=(100, 200)):
+        c, e = _err_case(T=T, lens=lens)
+        return L.compresskv_layer_error_workspace_bytes(ctypes.byref(c.p), ctypes.byref(e))
+    assert need(1000) == need(16) > need(4) > 0
+    assert need(3, lens=(100,) * 200) == need(3, lens=(100,) * 10)
+
+
+def test_layer_error_unsupported_shapes(L):
     c4, e4 = _err_case(Hq=2, Hkv=2, D=64)                          # Hq * D = 128: not a multiple of 256
     assert _layer_error(L, c4, e4) == C.UNSUPPORTED
     c5, e5 = _err_case(D=96)

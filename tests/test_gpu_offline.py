@@ -161,6 +161,13 @@ def _oracle_error(c, eps=1e-6):
                       dtype=C.F32)),
     ("bf16 one step", dict(lens=(1025,), Hq=8, Hkv=8, D=128, T=1, B=17, d_model=64,
                            dtype=C.BF16)),
+    # more steps and sequences than one block of the kernels holds
+    ("bf16 64 steps G=4 batch 2", dict(lens=(3000, 2200), Hq=32, Hkv=8, D=128, T=64, B=256,
+                                       d_model=512, dtype=C.BF16)),
+    ("bf16 20 steps G=7", dict(lens=(2600,), Hq=28, Hkv=4, D=128, T=20, B=128, d_model=256,
+                               dtype=C.BF16)),
+    ("fp32 40 sequences x 3 steps", dict(lens=tuple(range(100, 900, 20)), Hq=8, Hkv=2, D=64, T=3,
+                                         B=64, d_model=128, dtype=C.F32)),
 ])
 def test_layer_error_matches_oracle(gpu, name, kw):
     _say(f"case layer error {name}")
