@@ -73,10 +73,12 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def algorithmic_bytes(lens, Hkv, D, es, W, n_srh_total, budget):
-    """Bytes the method must move for one layer: all of K once, the SRH window
-    queries, the kept K/V rows read and written, and the int32 indices."""
-    k_bytes = sum(lens) * Hkv * D * es
+def algorithmic_bytes(lens, Hkv, D, es, W, n_srh_total, budget, scored_groups):
+    """Bytes the method must move for one layer: K once for every KV group that
+    has an SRH (with the layer-shared index set a group without one adds
+    nothing to the layer score), the SRH window queries, the kept K/V rows of
+    every group read and written, and the int32 indices."""
+    k_bytes = sum(lens) * scored_groups * D * es
     q_bytes = len(lens) * W * n_srh_total * D * es
     kept = sum(min(budget, L) for L in lens)
     gather = 4 * kept * Hkv * D * es + 4 * kept * Hkv
@@ -85,7 +87,9 @@ def algorithmic_bytes(lens, Hkv, D, es, W, n_srh_total, budget):
 
 def cpu_baseline(layers, w, seconds):
     """The fp64 oracle on (layer, sequence, KV group) units, layer after layer,
-    until about `seconds` of CPU time, scaled to tokens per second per layer."""
+    until about `seconds` of CPU time, scaled to tokens per second per layer.
+    With the layer-shared index set a unit is a (layer, sequence) with all of
+    its groups."""
     import numpy as np
     import oracle as O
 
@@ -105,6 +109,19 @@ def cpu_baseline(layers, w, seconds):
         q_all = lay["q_win"].float().cpu().numpy()
         for b in range(w.batch):
             s0, s1 = int(cu[b]), int(cu[b + 1])
+            if w.index_layer:
+                q = q_all[b:b + 1]
+                k = lay["k"][s0:s1].float().cpu().numpy()
+                v = lay["v"][s0:s1].float().cpu().numpy()
+                t0 = time.perf_counter()
+                O.compress_layer(q, k, v, np.array([0, s1 - s0]), lay["srh_mask"], lay["budget"],
+                                 w.pool_kernel, w.pool_type, index_mode=O.LAYER_SHARED)
+                t_total += time.perf_counter() - t0
+                done_tokens += (s1 - s0) * w.n_kv_heads
+                n += 1
+                if t_total >= seconds:
+                    break
+                continue
             for g in range(w.n_kv_heads):
                 q = q_all[b:b + 1, :, g * G:(g + 1) * G, :]
                 k = lay["k"][s0:s1, g:g + 1, :].float().cpu().numpy()
@@ -135,7 +152,8 @@ def cpu_baseline(layers, w, seconds):
             "kind": "oracle", "blas_threads": int(threads), "host_cpus": os.cpu_count(),
             "cpu_model": cpu_model,
             "note": "numpy fp64; its element-wise exp and max run on one thread",
-            "sample": f"{n} (layer, sequence, KV group) units from layer 0 on "
+            "sample": f"{n} (layer, sequence{'' if w.index_layer else ', KV group'}) units "
+                      f"from layer 0 on "
                       f"({done_tokens} group-tokens, {done_tokens / group_tokens_layer:.2f} "
                       f"layers' worth), {t_total:.1f} s of oracle time, scaled to one layer"}
 
@@ -229,7 +247,11 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=30)
     ap.add_argument("--workload", default="llama32",
-                    help="tiny | llama1 | llama32 | qwen128k | ragged8")
+                    help="tiny | llama1 | llama32 | qwen128k | ragged8 | paper")
+    ap.add_argument("--sets", type=int, default=0,
+                    help="single-layer workloads: input sets the steps rotate over (0: enough "
+                         "for 512 MiB of K and V, at least 5, so no step finds its inputs in "
+                         "the 256 MB last-level cache)")
     ap.add_argument("--layers", type=int, default=0, help="limit the layer count (0: all)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--mode", default="layers", choices=["layers", "per-layer"],
@@ -276,8 +298,22 @@ def main():
     w = wl.get(args.workload)
     n_layers = args.layers or w.n_layers
     es = 2 if w.dtype == wl.BF16 else 4
-    log(f"bench: workload {w.name}, {n_layers} layers, generating inputs on the GPU")
-    layers = [wl.make_layer_device(w, l, args.seed, dev) for l in range(n_layers)]
+    single = n_layers == 1
+    mode = C.INDEX_LAYER if w.index_layer else C.INDEX_PER_GROUP
+    if single:
+        # one layer per step, rotating over input sets (distinct K, V, Q, SRH
+        # masks) so that each step reads its inputs from HBM
+        set_bytes = 2 * sum(int(x) for x in wl.seq_lengths(w, args.seed)) * w.n_kv_heads \
+            * w.head_dim * es
+        n_sets = args.sets or min(1024, max(5, -(-(512 << 20) // set_bytes)))
+        budget0 = int(wl.layer_budgets(w, args.seed)[0])
+        log(f"bench: workload {w.name}, one layer per step over {n_sets} input sets")
+        layers = [wl.make_layer_device(w, r, args.seed, dev, budget=budget0)
+                  for r in range(n_sets)]
+    else:
+        n_sets = 1
+        log(f"bench: workload {w.name}, {n_layers} layers, generating inputs on the GPU")
+        layers = [wl.make_layer_device(w, l, args.seed, dev) for l in range(n_layers)]
     torch.cuda.synchronize()
     lens = [int(x) for x in np.diff(layers[0]["cu_seqlens_host"])]
     budgets = [lay["budget"] for lay in layers]
@@ -290,7 +326,7 @@ def main():
     for lay in layers:
         p = C.Problem(lay["q_win"], lay["k"], lay["v"], lay["cu_seqlens"],
                       cu_seqlens_host=lay["cu_seqlens_host"], pool_kernel=w.pool_kernel,
-                      pool_type=w.pool_type)
+                      pool_type=w.pool_type, index_mode=mode)
         probs.append(p)
         B_l = lay["budget"]
         shape = (w.batch, w.n_kv_heads, B_l, w.head_dim)
@@ -298,7 +334,10 @@ def main():
                      torch.empty(shape, dtype=lay["k"].dtype, device=dev),
                      torch.empty(shape, dtype=lay["v"].dtype, device=dev)))
         n_srh = int(lay["srh_mask"].sum())
-        sb, gb = algorithmic_bytes(lens, w.n_kv_heads, w.head_dim, es, w.window, n_srh, B_l)
+        G = w.n_q_heads // w.n_kv_heads
+        scored = int((lay["srh_mask"].reshape(w.n_kv_heads, G).sum(1) > 0).sum())
+        sb, gb = algorithmic_bytes(lens, w.n_kv_heads, w.head_dim, es, w.window, n_srh, B_l,
+                                   scored)
         score_flops_total += 2 * w.window * n_srh * w.head_dim * sum(lens)
         score_bytes_total += sb
         alg_bytes_total += sb + gb
@@ -308,7 +347,20 @@ def main():
     masks = np.stack([lay["srh_mask"] for lay in layers])
     main = torch.cuda.current_stream()
 
-    if args.mode == "layers":
+    if single:
+        ws1 = torch.empty(max(C.compresskv_workspace_bytes(p, lay["srh_mask"], lay["budget"])
+                              for p, lay in zip(probs, layers)), dtype=torch.uint8, device=dev)
+        step_no = [0]
+
+        def step():
+            r = step_no[0] % n_sets
+            step_no[0] += 1
+            lay, (idx, k_out, v_out) = layers[r], outs[r]
+            C.compresskv_compress_layer(probs[r], lay["q_win"], lay["k"], lay["v"],
+                                        lay["srh_mask"], lay["budget"], idx, k_out, v_out, None,
+                                        ws1, main)
+        n_streams = 1
+    elif args.mode == "layers":
         ws_layers = C.layers_workspace(probs[0], masks, dev)
         call = C.LayersCall(probs[0], q_l, k_l, v_l, masks, budgets, [o[0] for o in outs],
                             [o[1] for o in outs], [o[2] for o in outs], None, ws_layers)
@@ -350,17 +402,32 @@ def main():
     elapsed = time.perf_counter() - t0
     log(f"bench: {args.steps} timed steps in {elapsed * 1e3:.2f} ms")
 
-    # Score phase alone (the two kernels that stream K), every layer in one
-    # multi-layer call, bracketed by events on the stream it runs on.
-    scores_all = torch.empty((n_layers, w.n_kv_heads, probs[0].total_tokens),
-                             dtype=torch.float32, device=dev)
-    ws_s = C.layers_workspace(probs[0], masks, dev)
+    # Score phase alone (the two kernels that stream K), bracketed by events on
+    # the stream it runs on: every layer in one multi-layer call, or (single
+    # layer) one compresskv_score call per input set in turn.
     reps = max(3, args.steps)
     sev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(reps + 1)]
-    for r in range(reps + 1):          # the first repetition is a warm-up
-        sev[r][0].record(main)
-        C.compresskv_score_layers(probs[0], q_l, k_l, masks, scores_all, ws_s, main)
-        sev[r][1].record(main)
+    if single:
+        scores1 = torch.empty((w.n_kv_heads, probs[0].total_tokens), dtype=torch.float32,
+                              device=dev)
+        for r in range(reps + 1):      # the first repetition is a warm-up
+            lay = layers[(r + 1) % n_sets]
+            sev[r][0].record(main)
+            C.compresskv_score(probs[(r + 1) % n_sets], lay["q_win"], lay["k"], lay["srh_mask"],
+                               scores1, ws1, main)
+            sev[r][1].record(main)
+        # per step: the one layer's score bytes, not the sum over the sets
+        score_bytes_total //= n_sets
+        alg_bytes_total //= n_sets
+        score_flops_total //= n_sets
+    else:
+        scores_all = torch.empty((n_layers, w.n_kv_heads, probs[0].total_tokens),
+                                 dtype=torch.float32, device=dev)
+        ws_s = C.layers_workspace(probs[0], masks, dev)
+        for r in range(reps + 1):      # the first repetition is a warm-up
+            sev[r][0].record(main)
+            C.compresskv_score_layers(probs[0], q_l, k_l, masks, scores_all, ws_s, main)
+            sev[r][1].record(main)
     torch.cuda.synchronize()
     score_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in sev[1:]]))
     ms_per_step = elapsed * 1e3 / args.steps
@@ -382,12 +449,19 @@ def main():
         "config": {"workload": f"{w.name}: {n_layers} layers, batch {w.batch}, "
                                f"{w.n_q_heads}q/{w.n_kv_heads}kv heads, D={w.head_dim}, "
                                f"L={'ragged ' + str(w.ragged) if w.ragged else w.seq_len}, "
-                               f"W={w.window}, maxpool {w.pool_kernel}",
+                               f"W={w.window}, maxpool {w.pool_kernel}" +
+                   (f", top {w.srh_per_layer} SRHs per layer, layer-shared index set"
+                    if w.index_layer else ""),
                    "layers": n_layers, "batch": w.batch, "seq_lens": lens[:16],
-                   "budgets": budgets, "mode": args.mode, "streams": n_streams},
+                   "budgets": budgets[:n_layers] if not single else budgets[:1],
+                   "index_set": "layer-shared" if w.index_layer else "per KV group",
+                   "mode": "one layer per step" if single else args.mode,
+                   "input_sets": n_sets, "streams": n_streams},
         "roofline": {"bound": "hbm",
-                     "kernel": f"score phase: stats_kernel + colsum_kernel over {n_layers} "
-                               f"layers (one compresskv_score_layers call)",
+                     "kernel": ("score phase: stats_kernel + colsum_kernel of one layer "
+                                "(compresskv_score, input sets in turn)") if single else
+                               (f"score phase: stats_kernel + colsum_kernel over {n_layers} "
+                                f"layers (one compresskv_score_layers call)"),
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "avg_ms": score_ms, "bytes_per_launch": score_bytes_total},

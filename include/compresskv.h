@@ -122,8 +122,9 @@ size_t compresskv_workspace_bytes(const ckv_problem *p, const uint8_t *srh_mask_
  *   With CKV_INDEX_LAYER every row g holds the layer score (the mean over all
  *   the layer's SRHs of their pooled window sums).
  * srh_mask_host: uint8 [n_q_heads]; every KV group needs at least one SRH
- *   (CKV_INDEX_LAYER: the layer needs one) and at most 12 row tiles
- *   (ceil(W/16) * n_srh <= 12).
+ *   (CKV_INDEX_LAYER: the layer needs one) and at most 16 row tiles
+ *   (ceil(W/16) * n_srh <= 16; 12 for CKV_F32 at head_dim 128), else
+ *   CKV_UNSUPPORTED.
  * Every sequence needs L_b >= W.  ws: >= compresskv_workspace_bytes(), any
  * contents, 256-byte aligned.
  */
@@ -199,7 +200,7 @@ size_t compresskv_layers_workspace_bytes(const ckv_problem *p, int32_t n_layers,
 /*
  * S1-S4 for n_layers layers: scores [n_layers][n_kv_heads][T] fp32 (device),
  * layer l laid out as compresskv_score writes it.  Each layer's SRH groups
- * obey compresskv_score's limit (ceil(W/16) * SRHs per group <= 12).
+ * obey compresskv_score's limit (ceil(W/16) * SRHs per group <= 16, or 12).
  */
 int compresskv_score_layers(const ckv_problem *p, int32_t n_layers,
                             const void *const *q_win_ptrs_host, const void *const *k_ptrs_host,

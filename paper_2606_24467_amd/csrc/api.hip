@@ -176,10 +176,12 @@ int set_row_tiles(const ckv_problem *p, int nmax, Plan &pl) {
   pl.th = (p->window + 15) / 16;
   pl.nmax = nmax;
   pl.rt_max = nmax * pl.th;
-  if (pl.rt_max > 12)
+  // 16 row tiles of fp32 queries at head_dim 128 would not fit the LDS
+  const int cap = (p->dtype == CKV_F32 && p->head_dim == 128) ? 12 : 16;
+  if (pl.rt_max > cap)
     return fail(CKV_UNSUPPORTED,
-                "ceil(window/16) * SRHs per group must be <= 12 (window %d, %d SRHs)", p->window,
-                nmax);
+                "ceil(window/16) * SRHs per group must be <= %d (window %d, %d SRHs)", cap,
+                p->window, nmax);
   pl.head_end_mask = 0;
   for (int rt = 0; rt < 32; ++rt)
     if ((rt + 1) % pl.th == 0) pl.head_end_mask |= 1u << rt;

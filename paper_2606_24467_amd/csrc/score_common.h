@@ -155,7 +155,7 @@ __device__ __forceinline__ void tile_logits_all(const uint4 (&kf)[Slices<T, D>::
 // queries (their rows are never read back), so every loop over row tiles has
 // a compile-time bound and no branch.
 __host__ __device__ constexpr int rt_class(int rt_n) {
-  return rt_n <= 4 ? rt_n : rt_n <= 6 ? 6 : rt_n <= 8 ? 8 : 12;
+  return rt_n <= 4 ? rt_n : rt_n <= 6 ? 6 : rt_n <= 8 ? 8 : rt_n <= 12 ? 12 : 16;
 }
 
 // Calls body.template operator()<RT>() with RT = rt_class(rt_n) (<= RTM).
@@ -168,7 +168,8 @@ __device__ __forceinline__ void dispatch_rt(int rt_n, F &&body) {
     case 4: if constexpr (RTM >= 4) body.template operator()<4>(); break;
     case 6: if constexpr (RTM >= 6) body.template operator()<6>(); break;
     case 8: if constexpr (RTM >= 8) body.template operator()<8>(); break;
-    default: if constexpr (RTM >= 12) body.template operator()<12>(); break;
+    case 12: if constexpr (RTM >= 12) body.template operator()<12>(); break;
+    default: if constexpr (RTM >= 16) body.template operator()<16>(); break;
   }
 }
 

@@ -91,6 +91,7 @@ __host__ __device__ inline int64_t grid_blocks(int Hkv, int nz, int lead, int cp
 // whichever workgroup size covers it.
 // ---------------------------------------------------------------------------
 constexpr int kStatsWaves = 4;
+constexpr int kStatsPartRows = 16 * 16;   // rows of the largest row-tile count (16 tiles)
 
 // Kernels compiled for 8 or more row tiles read the query fragments one slice
 // at a time (see tile_logits_all): without it they need about 296 VGPRs and
@@ -104,7 +105,7 @@ constexpr int kStatsMinWaves = RTM >= 8 && Slices<T, D>::n >= 4 ? 3 : 1;
 
 template <typename T, int D, int RT, bool SB>
 __device__ __forceinline__ void stats_body(const ScoreArgs &a, const Work &w, uint4 *q_lds,
-                                           float2 (*part)[16 * 12]) {
+                                           float2 (*part)[kStatsPartRows]) {
   constexpr int NW = kStatsWaves;
   constexpr int NS = Slices<T, D>::n, RQ = RegTiles<T, D, RT>::v;
   constexpr int NT = 64 * NW;
@@ -216,7 +217,8 @@ __attribute__((amdgpu_waves_per_eu(kStatsMinWaves<T, D, RTM>))) void stats_kerne
   w.rt_n = w.lv.nsrh * a.th;
 
   __shared__ uint4 q_lds[RTM * 16 * QLayout<T, D>::STRIDE];
-  __shared__ float2 part[kStatsWaves][16 * 12];
+  static_assert(RTM * 16 <= kStatsPartRows, "per-wave partials of every row");
+  __shared__ float2 part[kStatsWaves][kStatsPartRows];
   dispatch_rt<RTM>(w.rt_n, [&]<int RT>() { stats_body<T, D, RT, kSliceBarrier<RTM>>(a, w, q_lds, part); });
 }
 
@@ -398,7 +400,15 @@ static hipError_t launch_score_d(const ScoreArgs &a, int rt_max, int nz, hipStre
     case 6: return launch_score_t<T, D, 6, ML>(a, nz, stream);
     case 7:
     case 8: return launch_score_t<T, D, 8, ML>(a, nz, stream);
-    default: return launch_score_t<T, D, 12, ML>(a, nz, stream);
+    case 9:
+    case 10:
+    case 11:
+    case 12: return launch_score_t<T, D, 12, ML>(a, nz, stream);
+    default:
+      // 16 row tiles of fp32 queries at D = 128 do not fit the LDS (the host
+      // caps that shape at 12)
+      if constexpr (sizeof(T) * D <= 256) return launch_score_t<T, D, 16, ML>(a, nz, stream);
+      return hipErrorInvalidConfiguration;
   }
 }
 

@@ -13,18 +13,25 @@ needle-in-a-haystack retrieval) with random data:
   llama32  32 layers of llama1's shape, Dirichlet per-layer budgets, 1-3 SRHs
   qwen128k 28 layers, 28 q / 4 kv heads, D=128, L=131072, W=64, bf16
   ragged8  32 layers, batch 8, lengths U[4096, 16384], 32 q / 8 kv, W=32, bf16
+  paper    the paper's own setting (section 4) on llama32's shape: W=8, max
+           pooling 5, the top 4 SRHs of each layer (any groups; groups
+           without one are allowed), the layer-shared index set, Dirichlet
+           per-layer budgets of 512 on average within [32, 3 x 512]
 
 Recipe (per layer and sequence):
   * Q window, K and V are N(0, 1), drawn in fp32 and rounded to bf16
     (round to nearest even) for the bf16 workloads;
-  * SRH mask: n_g heads of each group chosen without replacement;
+  * SRH mask: n_g heads of each group chosen without replacement (paper:
+    4 heads of the layer chosen without replacement);
   * sinks: positions 0 .. n_sink-1 hold 3*sqrt(D) times the unit mean
     direction of all the group's window queries;
   * needles: n_needle positions in [n_sink + 2k, P - 2k), at least 2k apart,
     hold 3*sqrt(D) times the unit mean direction of the group's SRH window
     queries (k = pooling kernel, P = L - W);
   * per-layer budgets: a Dirichlet(1) split of the total above a per-layer
-    minimum, rounded down, remainder to the largest fractional parts.
+    minimum, rounded down, remainder to the largest fractional parts; with a
+    per-layer maximum, the excess of capped layers is split again over the
+    others in proportion to their shares until none exceeds it.
 """
 from __future__ import annotations
 
@@ -58,6 +65,9 @@ class Workload:
     budget_min: int = 0
     srh_per_group: tuple = (2,)  # one value, or a range (lo, hi) drawn uniformly
     ragged: tuple = ()           # (lo, hi) inclusive lengths when ragged
+    srh_per_layer: int = 0       # > 0: that many SRHs over all of the layer's heads
+    index_layer: bool = False    # one index set per layer (layer-shared)
+    budget_max: int = 0          # > 0: per-layer budget cap of the Dirichlet split
 
 
 WORKLOADS = {
@@ -74,6 +84,9 @@ WORKLOADS = {
     "ragged8": Workload("ragged8", 4, 32, 8, 32, 8, 128, 16384, 32, BF16,
                         n_sink=4, n_needle=16, budget=256, srh_per_group=(2,),
                         ragged=(4096, 16384)),
+    "paper": Workload("paper", 5, 32, 1, 32, 8, 128, 32768, 8, BF16, pool_kernel=5,
+                      n_sink=4, n_needle=16, budget_total_per_layer=512, budget_min=32,
+                      budget_max=3 * 512, srh_per_layer=4, index_layer=True),
 }
 
 
@@ -119,6 +132,18 @@ def layer_budgets(w: Workload, seed: int = 0) -> np.ndarray:
     rest = total - n * w.budget_min
     p = _rng(seed, w.cid, 3).dirichlet(np.ones(n))
     raw = p * rest
+    if w.budget_max:
+        cap = float(w.budget_max - w.budget_min)
+        capped = np.zeros(n, dtype=bool)
+        while True:
+            over = ~capped & (raw > cap)
+            if not over.any():
+                break
+            capped |= over
+            excess = float(np.sum(raw[capped] - cap))
+            raw[capped] = cap
+            free = ~capped
+            raw[free] += excess * p[free] / p[free].sum()
     b = w.budget_min + np.floor(raw).astype(np.int64)
     frac = raw - np.floor(raw)
     short = int(total - b.sum())
@@ -132,6 +157,9 @@ def srh_mask(w: Workload, layer: int, seed: int = 0) -> np.ndarray:
     G = w.n_q_heads // w.n_kv_heads
     rng = _rng(seed, w.cid, 1, layer)
     mask = np.zeros(w.n_q_heads, dtype=np.uint8)
+    if w.srh_per_layer:
+        mask[rng.choice(w.n_q_heads, w.srh_per_layer, replace=False)] = 1
+        return mask
     for g in range(w.n_kv_heads):
         if len(w.srh_per_group) == 1:
             n = w.srh_per_group[0]

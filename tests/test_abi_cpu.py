@@ -145,8 +145,28 @@ def test_mask_rules(L):
     assert c.score(L) == C.INVALID_ARGUMENT
     assert "no Semantic Retrieval Head" in L.compresskv_last_error().decode()
     c = Case(W=64, Hq=32, Hkv=4)
-    c.mask[:] = 1                      # 8 SRHs x 4 row tiles = 32 > 12
+    c.mask[:] = 1                      # 8 SRHs x 4 row tiles = 32 > 16
     assert c.score(L) == C.UNSUPPORTED
+
+
+def test_row_tile_limits(L):
+    """Up to 16 row tiles per group (W = 64 with 4 SRHs in one group); 12
+    for fp32 queries at head_dim 128, whose 16 tiles would not fit the LDS.
+    Only the workspace query runs: it plans the call without touching a
+    device."""
+    def case(dtype, D, n_srh):
+        c = Case(W=64, Hq=32, Hkv=4, D=D, dtype=dtype)
+        c.mask[:] = 0
+        c.mask[:n_srh] = 1             # n_srh SRHs in group 0, 4 row tiles each
+        c.mask[8::8] = 1               # one in every other group
+        return c
+    assert case(C.BF16, 128, 4).ws_bytes(L) > 0
+    assert case(C.F32, 64, 4).ws_bytes(L) > 0
+    assert case(C.F32, 128, 3).ws_bytes(L) > 0
+    assert case(C.F32, 128, 4).ws_bytes(L) == 0
+    assert "must be <= 12" in L.compresskv_last_error().decode()
+    assert case(C.BF16, 128, 5).ws_bytes(L) == 0
+    assert "must be <= 16" in L.compresskv_last_error().decode()
 
 
 def test_mask_rules_of_the_layer_shared_set(L):
@@ -260,7 +280,7 @@ def test_multi_layer_rules_name_the_layer(L):
 
 def test_multi_layer_row_tile_limit_uses_the_largest_layer(L):
     c = LayersCase(n_layers=2, W=64, Hq=32, Hkv=4)
-    c.masks[1, :] = 1                               # layer 1: 8 SRHs x 4 row tiles > 12
+    c.masks[1, :] = 1                               # layer 1: 8 SRHs x 4 row tiles > 16
     assert c.compress_layers(L) == C.UNSUPPORTED
     assert c.ws_bytes(L) == 0
 

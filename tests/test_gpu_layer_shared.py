@@ -20,11 +20,6 @@ def _say(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-@pytest.fixture(autouse=True)
-def _two_pass(monkeypatch):
-    monkeypatch.delenv("CKV_PATH", raising=False)
-
-
 def _drop_groups(x: wl.LayerInputs, groups):
     """Remove every SRH of the given KV groups (the layer keeps the others)."""
     G = x.srh_mask.shape[0] // x.workload.n_kv_heads
@@ -129,3 +124,91 @@ def test_layer_set_multi_layer_call(gpu):
         swaps = _check(x, budgets[l], scores[l].cpu().numpy(), idxs[l].cpu().numpy(),
                        H.raw_bits(kos[l]), H.raw_bits(vos[l]))
         _say(f"  layer {l} ok, boundary swaps {swaps}")
+
+
+def _needles_kept(x, budget, idx):
+    """Needles of the groups that have SRHs (and the sinks) win their pooling
+    neighbourhoods in the layer score; all of them are kept when the prefix
+    budget covers every such neighbourhood."""
+    w = x.workload
+    G = w.n_q_heads // w.n_kv_heads
+    groups = [g for g in range(w.n_kv_heads) if x.srh_mask[g * G:(g + 1) * G].any()]
+    if budget - w.window < (len(groups) * w.n_needle + w.n_sink) * w.pool_kernel:
+        return False
+    for (b, g), pos in x.needles.items():
+        if g in groups:
+            assert set(pos.tolist()) <= set(idx[b, 0].tolist()), (b, g)
+    return True
+
+
+def _paper_stack(xs, budgets, gpu):
+    dts = [H.device_tensors(x, gpu) for x in xs]
+    q, k, v = [d[0] for d in dts], [d[1] for d in dts], [d[2] for d in dts]
+    masks = np.stack([x.srh_mask for x in xs])
+    ps = [_problem(xs[l], q[l], k[l], v[l], dts[0][3]) for l in range(len(xs))]
+    idxs, kos, vos, scores = C.compress_layers(ps[0], q, k, v, masks, budgets, want_scores=True)
+    ref = [C.compress_layer(ps[l], q[l], k[l], v[l], masks[l], int(budgets[l]), want_scores=True)
+           for l in range(len(xs))]
+    torch.cuda.synchronize()
+    for l in range(len(xs)):
+        for got, want in zip((idxs[l], kos[l], vos[l], scores[l]), ref[l]):
+            assert torch.equal(got, want), f"layer {l} differs from the per-layer call"
+    return idxs, kos, vos, scores
+
+
+def test_paper_setting_stack(gpu):
+    """The paper's own setting (section 4): W = 8, max pooling 5, the top 4
+    SRHs of each layer, the layer-shared index set and budgets within
+    [32, 3 x 512], at L = 9001 over 6 layers with the full stack's first
+    budgets: one multi-layer call, bit-identical to per-layer calls, every
+    layer against the oracle."""
+    w = wl.get("paper", seq_len=9001, n_layers=6)
+    budgets = [int(b) for b in wl.layer_budgets(wl.get("paper"))[:6]]
+    xs = [wl.make_layer(w, l, seed=41, budget=B) for l, B in enumerate(budgets)]
+    _say(f"case paper setting stack, budgets {budgets}, SRH masks "
+         f"{[np.flatnonzero(x.srh_mask).tolist() for x in xs]}")
+    idxs, kos, vos, scores = _paper_stack(xs, budgets, gpu)
+    kept_all = 0
+    for l, x in enumerate(xs):
+        idx = idxs[l].cpu().numpy()
+        swaps = _check(x, budgets[l], scores[l].cpu().numpy(), idx, H.raw_bits(kos[l]),
+                       H.raw_bits(vos[l]))
+        kept_all += _needles_kept(x, budgets[l], idx)
+        _say(f"  layer {l} ok, boundary swaps {swaps}")
+    assert kept_all > 0
+
+
+def test_paper_setting_full_stack(gpu):
+    """The same setting at the benchmark's size: 32 layers at L = 32768,
+    inputs drawn on the device; one multi-layer call, bit-identical to
+    per-layer calls on every layer, and three layers against the oracle."""
+    w = wl.get("paper")
+    layers = [wl.make_layer_device(w, l, 0, gpu) for l in range(w.n_layers)]
+    budgets = [d["budget"] for d in layers]
+    _say(f"case paper setting full stack, budgets {budgets}")
+    q = [d["q_win"] for d in layers]
+    k = [d["k"] for d in layers]
+    v = [d["v"] for d in layers]
+    cu, cu_host = layers[0]["cu_seqlens"], layers[0]["cu_seqlens_host"]
+    masks = np.stack([d["srh_mask"] for d in layers])
+    ps = [C.Problem(q[l], k[l], v[l], cu, cu_seqlens_host=cu_host, pool_kernel=w.pool_kernel,
+                    pool_type=w.pool_type, index_mode=C.INDEX_LAYER) for l in range(w.n_layers)]
+    idxs, kos, vos, scores = C.compress_layers(ps[0], q, k, v, masks, budgets, want_scores=True)
+    torch.cuda.synchronize()
+    for l in range(w.n_layers):
+        ref = C.compress_layer(ps[l], q[l], k[l], v[l], masks[l], budgets[l], want_scores=True)
+        torch.cuda.synchronize()
+        for got, want in zip((idxs[l], kos[l], vos[l], scores[l]), ref):
+            assert torch.equal(got, want), f"layer {l} differs from the per-layer call"
+        del ref
+    for l in (0, 13, 31):
+        d = layers[l]
+        x = wl.LayerInputs(workload=w, layer=l, cu_seqlens=cu_host, srh_mask=d["srh_mask"],
+                           budget=d["budget"], q_win=d["q_win"].float().cpu().numpy(),
+                           k=d["k"].float().cpu().numpy(), v=d["v"].float().cpu().numpy(),
+                           needles=d["needles"])
+        idx = idxs[l].cpu().numpy()
+        swaps = _check(x, budgets[l], scores[l].cpu().numpy(), idx, H.raw_bits(kos[l]),
+                       H.raw_bits(vos[l]))
+        _needles_kept(x, budgets[l], idx)
+        _say(f"  layer {l} matches the oracle, boundary swaps {swaps}")

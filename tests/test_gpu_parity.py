@@ -111,6 +111,13 @@ def test_paper_setting_window8_kernel5(gpu):
     run_case(wl.make_layer(w, 0, seed=5), gpu)
 
 
+def test_sixteen_row_tiles(gpu):
+    """W = 64 with 4 SRHs in one group (Qwen's 7 heads per group): 16 row
+    tiles of the scoring kernels."""
+    w = wl.get("qwen128k", seq_len=5000 + 3, srh_per_group=(4,), n_needle=4, budget=300)
+    run_case(wl.make_layer(w, 0, seed=6), gpu)
+
+
 @pytest.mark.parametrize("D", [64, 128])
 def test_fp32_head_dims(gpu, D):
     w = wl.get("tiny", head_dim=D, seq_len=2000 + 5)

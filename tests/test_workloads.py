@@ -40,14 +40,39 @@ def test_bf16_workload_values_are_representable():
         np.testing.assert_array_equal(wl.bf16_bits_to_f32(wl.f32_to_bf16_bits(a)), a)
 
 
-@pytest.mark.parametrize("name", ["llama32", "qwen128k"])
+@pytest.mark.parametrize("name", ["llama32", "qwen128k", "paper"])
 def test_dirichlet_budgets(name):
     w = wl.get(name)
     b = wl.layer_budgets(w)
     assert b.sum() == w.budget_total_per_layer * w.n_layers
     assert b.min() >= w.budget_min
     assert np.array_equal(b, wl.layer_budgets(w))
-    assert b.max() <= w.seq_len
+    assert b.max() <= (w.budget_max or w.seq_len)
+
+
+def test_budget_cap_redistributes_in_proportion():
+    """The paper's [m, M] constraint (section 4: m = 32, M = 3 x the average):
+    with a cap that binds, no layer exceeds it, the total is kept, and every
+    uncapped layer receives at least its uncapped share."""
+    w = wl.get("paper")
+    capped = wl.layer_budgets(w)
+    free = wl.layer_budgets(wl.get("paper", budget_max=0))
+    assert free.max() > w.budget_max            # the cap binds for this seed
+    assert capped.max() == w.budget_max
+    assert capped.sum() == free.sum()
+    below = free < w.budget_max
+    assert np.all(capped[below] >= free[below] - 1)
+
+
+def test_paper_srh_masks_are_four_heads_of_the_layer():
+    w = wl.get("paper")
+    G = w.n_q_heads // w.n_kv_heads
+    empty_groups = 0
+    for layer in range(w.n_layers):
+        m = wl.srh_mask(w, layer)
+        assert m.sum() == 4
+        empty_groups += int((m.reshape(w.n_kv_heads, G).sum(1) == 0).sum())
+    assert empty_groups > 0                     # groups without an SRH occur
 
 
 def test_srh_counts_and_lengths():
