@@ -35,20 +35,37 @@ MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # dense, MI355X
 
 # HBM bytes moved by one score phase (stats_kernel + colsum_kernel), measured
 # with rocprofv3: FETCH_SIZE x 2 (the factor a plain copy of known size gives
-# on this GPU) + WRITE_SIZE, in separate runs (profiles/).  A figure is valid
-# only for the kernel sources it was taken with: keyed by their hash.
+# on this GPU) + WRITE_SIZE, in KiB per dispatch, in separate runs (profiles/).
+# A figure is valid only for the kernel sources it was taken with: keyed by
+# their hash.  Single-layer workloads: one layer's score phase.
+def _traffic(fetch_stats, fetch_colsum, write_stats, write_colsum):
+    return (2 * (fetch_stats + fetch_colsum) + write_stats + write_colsum) * 1024
+
+
 MEASURED_TRAFFIC = {
-    ("llama32", 32, "b44e85fa86dcbab4"): (2 * (1080865.7 + 1168537.7) + 6248.0 + 33069.2) * 1024,
+    ("llama32", 32, "c630a66cd07a2dbe"): _traffic(1080432.45, 1168574.175, 6248.0, 33069.1875),
+    ("qwen128k", 28, "c630a66cd07a2dbe"): _traffic(1852764.65, 1947780.9, 8064.0, 57591.34375),
+    ("ragged8", 32, "c630a66cd07a2dbe"): _traffic(2672889.625, 2843529.3375, 22016.0, 82243.09375),
+    ("paper", 32, "c630a66cd07a2dbe"): _traffic(449888.3625, 482387.7125, 2560.0, 14199.01875),
+    ("llama1", 1, "c630a66cd07a2dbe"): _traffic(33428.1, 40078.6125, 192.0, 1045.63125),
+    ("tiny", 1, "c630a66cd07a2dbe"): _traffic(297.4, 332.25, 16.5, 8.41875),
 }
 
 # MFMA work the score phase executes, from rocprofv3 on the same sources:
 # SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 FLOP of both kernels, and each kernel's
 # SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 XCDs x 1024 SIMDs).
+def _mfma(mops_stats, mops_colsum, busy_stats, busy_colsum, gui_stats, gui_colsum):
+    return {"executed_flops_per_launch": (mops_stats + mops_colsum) * 512,
+            "busy_frac": {"stats_kernel": busy_stats / (gui_stats / 8 * 1024),
+                          "colsum_kernel": busy_colsum / (gui_colsum / 8 * 1024)}}
+
+
 MEASURED_MFMA = {
-    ("llama32", 32, "b44e85fa86dcbab4"): {
-        "executed_flops_per_launch": (275251200 + 290304000) * 512,
-        "busy_frac": {"stats_kernel": 137625600 / (6572285.6 / 8 * 1024),
-                      "colsum_kernel": 145152000 / (7954866.6 / 8 * 1024)}},
+    ("llama32", 32, "c630a66cd07a2dbe"): _mfma(275251200, 290304000, 137625600, 145152000, 6637385.2,
+                                  8146807.4),
+    ("qwen128k", 28, "c630a66cd07a2dbe"): _mfma(939524096, 987693056, 469762048, 493846528, 10763302.2,
+                                   14438370.6),
+    ("paper", 32, "c630a66cd07a2dbe"): _mfma(33554432, 36503552, 16777216, 18251776, 3640013.6, 4104640.0),
 }
 
 
@@ -143,9 +160,17 @@ def cpu_baseline(layers, w, seconds):
     t_layer = t_total * group_tokens_layer / done_tokens
     cpu_model = ""
     try:
+        info = {}
         with open("/proc/cpuinfo") as f:
-            cpu_model = next((ln.split(":", 1)[1].strip() for ln in f
-                              if ln.startswith("model name")), "")
+            for ln in f:
+                if ":" in ln:
+                    k, v = ln.split(":", 1)
+                    info.setdefault(k.strip(), v.strip())
+                if not ln.strip() and info:
+                    break
+        cpu_model = (f"{info.get('model name', '')} ({info.get('vendor_id', '')} family "
+                     f"{info.get('cpu family', '?')} model {info.get('model', '?')} stepping "
+                     f"{info.get('stepping', '?')}, {os.cpu_count()} logical CPUs)")
     except OSError:
         pass
     return {"value": tokens_layer / t_layer, "unit": "tokens/s/layer", "cores": int(threads),
