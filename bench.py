@@ -289,6 +289,9 @@ def main():
     ap.add_argument("--offline", action="store_true",
                     help="only time the offline analyses (SRH scores, layer eviction error) "
                          "and the per-group-budget path, one JSON line each")
+    ap.add_argument("--scoring", default="auto", choices=["auto", "two", "one"],
+                    help="scoring implementation (ckv_problem.scoring): the library's choice, "
+                         "two passes over K, or the single pass")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain elementwise copy of MIB MiB (3 times): the "
                          "reference point that scales the HBM byte counters")
@@ -344,6 +347,7 @@ def main():
     budgets = [lay["budget"] for lay in layers]
     log(f"bench: inputs ready, lengths {lens[:8]}, budgets {budgets[:8]}...")
 
+    scoring = {"auto": C.SCORE_AUTO, "two": C.SCORE_TWO_PASS, "one": C.SCORE_ONE_PASS}[args.scoring]
     probs, outs = [], []
     score_bytes_total = 0
     alg_bytes_total = 0
@@ -351,7 +355,7 @@ def main():
     for lay in layers:
         p = C.Problem(lay["q_win"], lay["k"], lay["v"], lay["cu_seqlens"],
                       cu_seqlens_host=lay["cu_seqlens_host"], pool_kernel=w.pool_kernel,
-                      pool_type=w.pool_type, index_mode=mode)
+                      pool_type=w.pool_type, index_mode=mode, scoring=scoring)
         probs.append(p)
         B_l = lay["budget"]
         shape = (w.batch, w.n_kv_heads, B_l, w.head_dim)
@@ -460,6 +464,8 @@ def main():
     value = tokens * n_layers / (ms_per_step / 1e3)
     achieved = score_bytes_total / (score_ms / 1e3) / 1e9
     e2e_gbs = alg_bytes_total / (ms_per_step / 1e3) / 1e9
+    path_name = {1: "single pass", 2: "two passes"}[
+        C.compresskv_scoring_path(probs[0], layers[0]["srh_mask"])]
     src_key = (w.name, n_layers, kernel_source_hash())
     traffic = MEASURED_TRAFFIC.get(src_key)
     counted = MEASURED_MFMA.get(src_key)
@@ -481,7 +487,8 @@ def main():
                    "budgets": budgets[:n_layers] if not single else budgets[:1],
                    "index_set": "layer-shared" if w.index_layer else "per KV group",
                    "mode": "one layer per step" if single else args.mode,
-                   "input_sets": n_sets, "streams": n_streams},
+                   "input_sets": n_sets, "streams": n_streams,
+                   "scoring": path_name},
         "roofline": {"bound": "hbm",
                      "kernel": ("score phase: stats_kernel + colsum_kernel of one layer "
                                 "(compresskv_score, input sets in turn)") if single else
