@@ -6,7 +6,7 @@
 //   dec_attn_kernel     split-K attention of every (sequence, group, cache):
 //                       the group's rows (decoding step x query head of the
 //                       group) against one 256-key chunk, QK^T on MFMA, online
-//                       softmax in LDS, P.V on the VALU; partial (max, sum, O)
+//                       softmax in LDS, P.V on fp32 MFMA; partial (max, sum, O)
 //   dec_combine_kernel  merges the chunks of every row into A (fp32)
 //   dec_proj_kernel     y = W_O x for x = A_full and A_full - A_comp on fp32
 //                       MFMA (16 rows of W_O per workgroup, one wave per 16
@@ -81,16 +81,17 @@ __device__ __forceinline__ DecCache dec_cache(const DecArgs &a, int cache, int b
 
 // Grid (n_chunks, Hkv, batch * 2), 256 threads.  Rows r = t * G + hh (step t,
 // head g * G + hh); RT = ceil(R / 16) row tiles, padding rows have zero
-// queries.  Thread (rb, db) of the P.V step owns rows rb*RPT .. +RPT and
-// columns 4*db .. 4*db+3.
+// queries.  The P.V step runs on v_mfma_f32_16x16x4_f32 with fp32
+// probabilities and V converted exactly to fp32: wave w owns the output
+// tiles of every row tile and the column tiles w*CTW .. +CTW (lane (quad, c)
+// holds rows 4*quad .. +3 of a tile against column c).
 template <typename T, int D, int RT>
 __global__ __launch_bounds__(256) void dec_attn_kernel(const DecArgs a) {
   constexpr int NS = Slices<T, D>::n, U4 = QLayout<T, D>::U4, STRIDE = QLayout<T, D>::STRIDE;
   constexpr int RP = RT * 16;                  // rows with padding
-  constexpr int DB = D / 4, RB = 256 / DB;     // column and row blocks of the P.V step
-  constexpr int RPT = RP / RB;                 // rows per thread there (>= 1)
+  constexpr int CTW = D / 16 / 4;              // column tiles per wave in the P.V step
   constexpr int ZS = kDecSub + 1;              // padded row of the logits buffer
-  static_assert(RP % RB == 0, "row blocks");
+  static_assert(CTW >= 1 && D % 64 == 0, "column tiles");
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int c = lane & 15, quad = lane >> 4;
   const int g = blockIdx.y, b = (int)blockIdx.z >> 1, cache = (int)blockIdx.z & 1;
@@ -128,12 +129,11 @@ __global__ __launch_bounds__(256) void dec_attn_kernel(const DecArgs a) {
 #pragma unroll
     for (int s = 0; s < NS; ++s) qreg[rt][s] = q_frag<T, D>(q_lds, rt, s, c, quad);
 
-  const int rb = tid / DB, db = tid - rb * DB;
-  float acc[RPT][4];
+  f32x4 acc[RT][CTW];
 #pragma unroll
-  for (int i = 0; i < RPT; ++i)
+  for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-    for (int d = 0; d < 4; ++d) acc[i][d] = 0.f;
+    for (int ct = 0; ct < CTW; ++ct) acc[rt][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   // The K fragments and V rows of a step are loaded into registers one step
   // ahead: the next step's loads are in flight during this step's softmax and
@@ -210,24 +210,28 @@ __global__ __launch_bounds__(256) void dec_attn_kernel(const DecArgs a) {
       }
     }
     __syncthreads();
-    // O = alpha * O + P.V
+    // O = alpha * O + P.V: keys 4 j + quad of the step per MFMA (keys past the
+    // chunk have p = 0)
 #pragma unroll
-    for (int i = 0; i < RPT; ++i) {
-      const int r = rb * RPT + i;
-      const float al = alpha_s[r];
+    for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-      for (int d = 0; d < 4; ++d) acc[i][d] *= al;
-    }
-    const int nk = min(kDecSub, c_end - k0);
-    for (int j = 0; j < nk; ++j) {
-      float vv[4];
+      for (int r = 0; r < 4; ++r) {
+        const float al = alpha_s[rt * 16 + 4 * quad + r];
 #pragma unroll
-      for (int d = 0; d < 4; ++d) vv[d] = (float)vs[j * D + 4 * db + d];
+        for (int ct = 0; ct < CTW; ++ct) acc[rt][ct][r] *= al;
+      }
+#pragma unroll 4
+    for (int j = 0; j < kDecSub / 4; ++j) {
+      const int key = 4 * j + quad;
+      float vv[CTW];
 #pragma unroll
-      for (int i = 0; i < RPT; ++i) {
-        const float p = zs[(rb * RPT + i) * ZS + j];
+      for (int ct = 0; ct < CTW; ++ct) vv[ct] = (float)vs[key * D + 16 * (wave * CTW + ct) + c];
 #pragma unroll
-        for (int d = 0; d < 4; ++d) acc[i][d] = __builtin_fmaf(p, vv[d], acc[i][d]);
+      for (int rt = 0; rt < RT; ++rt) {
+        const float p = zs[(rt * 16 + c) * ZS + key];
+#pragma unroll
+        for (int ct = 0; ct < CTW; ++ct)
+          acc[rt][ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(p, vv[ct], acc[rt][ct], 0, 0, 0);
       }
     }
     __syncthreads();   // zs and vs are rewritten by the next step
@@ -236,14 +240,16 @@ __global__ __launch_bounds__(256) void dec_attn_kernel(const DecArgs a) {
   const int64_t slot = (((int64_t)cache * a.batch + b) * a.Hkv + g) * a.n_chunks + blockIdx.x;
   if (tid < a.R) a.part_ml[slot * kMaxDecRows + tid] = make_float2(m_s[tid], l_s[tid]);
 #pragma unroll
-  for (int i = 0; i < RPT; ++i) {
-    const int r = rb * RPT + i;
-    if (r < a.R) {
-      float *o = a.part_o + (slot * kMaxDecRows + r) * D + 4 * db;
+  for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-      for (int d = 0; d < 4; ++d) o[d] = acc[i][d];
+    for (int r = 0; r < 4; ++r) {
+      const int row = rt * 16 + 4 * quad + r;
+      if (row < a.R) {
+        float *o = a.part_o + (slot * kMaxDecRows + row) * D;
+#pragma unroll
+        for (int ct = 0; ct < CTW; ++ct) o[16 * (wave * CTW + ct) + c] = acc[rt][ct][r];
+      }
     }
-  }
 }
 
 // Grid (R, Hkv, batch * 2), D threads: A of row r of the group from its
