@@ -289,9 +289,10 @@ def main():
     ap.add_argument("--offline", action="store_true",
                     help="only time the offline analyses (SRH scores, layer eviction error) "
                          "and the per-group-budget path, one JSON line each")
-    ap.add_argument("--scoring", default="auto", choices=["auto", "two", "one"],
+    ap.add_argument("--scoring", default="auto", choices=["auto", "two", "one", "two-launches"],
                     help="scoring implementation (ckv_problem.scoring): the library's choice, "
-                         "two passes over K, or the single pass")
+                         "two passes over K (one launch where the shape allows), the single "
+                         "pass, or two passes in two launches")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain elementwise copy of MIB MiB (3 times): the "
                          "reference point that scales the HBM byte counters")
@@ -347,7 +348,8 @@ def main():
     budgets = [lay["budget"] for lay in layers]
     log(f"bench: inputs ready, lengths {lens[:8]}, budgets {budgets[:8]}...")
 
-    scoring = {"auto": C.SCORE_AUTO, "two": C.SCORE_TWO_PASS, "one": C.SCORE_ONE_PASS}[args.scoring]
+    scoring = {"auto": C.SCORE_AUTO, "two": C.SCORE_TWO_PASS, "one": C.SCORE_ONE_PASS,
+               "two-launches": C.SCORE_TWO_LAUNCHES}[args.scoring]
     probs, outs = [], []
     score_bytes_total = 0
     alg_bytes_total = 0
@@ -467,8 +469,12 @@ def main():
     value = tokens * n_layers / (ms_per_step / 1e3)
     achieved = score_bytes_total / (score_ms / 1e3) / 1e9
     e2e_gbs = alg_bytes_total / (ms_per_step / 1e3) / 1e9
-    path_name = {1: "single pass", 2: "two passes"}[
-        C.compresskv_scoring_path(probs[0], layers[0]["srh_mask"])]
+    path_id = C.compresskv_scoring_path(probs[0], layers[0]["srh_mask"])
+    path_name = {1: "single pass", 2: "two passes, two launches",
+                 3: "two passes, one launch"}[path_id]
+    score_kernels = {1: "onepass_kernel (+ catch-up and boundary kernels)",
+                     2: "stats_kernel + colsum_kernel",
+                     3: "fused_kernel (+ its fill and catch-up kernels)"}[path_id]
     src_key = (w.name, n_layers, kernel_source_hash())
     traffic = MEASURED_TRAFFIC.get(src_key)
     counted = MEASURED_MFMA.get(src_key)
@@ -493,9 +499,9 @@ def main():
                    "input_sets": n_sets, "streams": n_streams,
                    "scoring": path_name},
         "roofline": {"bound": "hbm",
-                     "kernel": ("score phase: stats_kernel + colsum_kernel of one layer "
+                     "kernel": (f"score phase: {score_kernels} of one layer "
                                 "(compresskv_score, input sets in turn)") if single else
-                               (f"score phase: stats_kernel + colsum_kernel over {n_layers} "
+                               (f"score phase: {score_kernels} over {n_layers} "
                                 f"layers (one compresskv_score_layers call)"),
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,

@@ -75,8 +75,11 @@ extern "C" {
 /* how S1-S4 are computed (the results agree within the scores' tolerance;
    each choice is deterministic) */
 #define CKV_SCORE_AUTO 0     /* the library's choice (see compresskv_scoring_path) */
-#define CKV_SCORE_TWO_PASS 1 /* two passes over K: row statistics, then window sums */
+#define CKV_SCORE_TWO_PASS 1 /* two passes over K: row statistics, then window sums; in one
+                                launch where the shape allows (see compresskv_scoring_path) */
 #define CKV_SCORE_ONE_PASS 2 /* K read once; CKV_UNSUPPORTED where it does not apply */
+#define CKV_SCORE_TWO_LAUNCHES 3 /* the two passes always in two launches (same bits as
+                                    CKV_SCORE_TWO_PASS) */
 #define CKV_SPIN_CATCHUP_ALL (-2) /* ckv_problem.spin_limit: see there */
 
 /* Sizes and options of one layer.  head_dim must be 64 or 128. */
@@ -97,13 +100,16 @@ typedef struct ckv_problem {
                                           multiples of 16 bytes (CKV_UNSUPPORTED otherwise) */
   int64_t v_stride_tok, v_stride_head;
   int32_t index_mode;   /* CKV_INDEX_PER_GROUP (0) or CKV_INDEX_LAYER */
-  int32_t scoring;      /* CKV_SCORE_AUTO (0), CKV_SCORE_TWO_PASS or CKV_SCORE_ONE_PASS */
+  int32_t scoring;      /* CKV_SCORE_AUTO (0), _TWO_PASS, _ONE_PASS or _TWO_LAUNCHES */
   int32_t spin_limit;   /* single pass: how many times a unit polls for its segment's row
                            normalisers before it is left to the catch-up kernel that
-                           follows on the same stream (about 1 us per poll); -1 (or any
-                           other negative value) selects the default (64), 0 never waits,
-                           CKV_SPIN_CATCHUP_ALL leaves every unit to the catch-up kernel
-                           (to exercise that path).  Results do not depend on it. */
+                           follows on the same stream (about 1 us per poll); two passes in
+                           one launch: how many times a workgroup polls for its group's
+                           statistics before its column sums are left to the catch-up
+                           kernel.  -1 (or any other negative value) selects the default
+                           (64 single pass, 256 one launch), 0 never waits,
+                           CKV_SPIN_CATCHUP_ALL leaves all of that work to the catch-up
+                           kernel (to exercise that path).  Results do not depend on it. */
   int32_t reserved;     /* must be 0 */
 } ckv_problem;
 
@@ -249,12 +255,20 @@ int compresskv_compress_layer_heads(const ckv_problem *p, const void *q_win, con
 /*
  * Which scoring implementation compresskv_score / _compress_layer will use for
  * this problem: 1 = single pass (each key read once from HBM), 2 = two passes
- * over K.  CKV_SCORE_AUTO and CKV_SCORE_TWO_PASS use two passes (the faster
- * of the two on the measured shapes); CKV_SCORE_ONE_PASS uses the single
- * pass, which needs bf16 inputs, CKV_INDEX_PER_GROUP, batch <= 64 and at most
- * 6 row tiles per group (ceil(W/16) * SRHs), and otherwise returns
- * -CKV_UNSUPPORTED.  The multi-layer calls make the same choice layer by
- * layer.  Negative on invalid arguments (minus the status).
+ * over K in two launches (statistics, then column sums), 3 = the same two
+ * passes in one launch (each group's column-sum workgroups wait inside the
+ * launch for its statistics; same bits as 2).  CKV_SCORE_TWO_PASS uses one
+ * launch for bf16 inputs with at most 6 row tiles per group, else two;
+ * CKV_SCORE_AUTO does the same where every sequence also spans at least 16
+ * statistics chunks (about 8k-16k keys; shorter sequences leave most of the
+ * one launch's workgroups idle), else two launches (on the measured shapes
+ * the single pass is slower than either);
+ * CKV_SCORE_TWO_LAUNCHES always uses two launches; CKV_SCORE_ONE_PASS uses
+ * the single pass, which needs bf16 inputs, CKV_INDEX_PER_GROUP, batch <= 64
+ * and at most 6 row tiles per group (ceil(W/16) * SRHs), and otherwise
+ * returns -CKV_UNSUPPORTED.  The multi-layer calls make the same choice over
+ * all their layers (single pass: layer by layer).  Negative on invalid
+ * arguments (minus the status).
  */
 int compresskv_scoring_path(const ckv_problem *p, const uint8_t *srh_mask_host);
 

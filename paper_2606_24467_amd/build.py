@@ -22,6 +22,11 @@ FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++20", "-fPIC",
     # packed fp32 VALU instructions stay off in every kernel of this library
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # a * b + c is fused only where the source says so (__builtin_fmaf): the
+    # rounding of the same device function then does not depend on the kernel
+    # it is inlined into (a multi-layer call and per-layer calls give the same
+    # bits whatever their kernels' template arguments)
+    "-ffp-contract=off",
     "-Wall", "-Wno-unused-result",
 ]
 

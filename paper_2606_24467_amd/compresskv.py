@@ -22,7 +22,7 @@ F32, BF16 = 0, 1
 POOL_MAX, POOL_AVG = 0, 1
 POOL_THEN_MEAN, MEAN_THEN_POOL = 0, 1
 INDEX_PER_GROUP, INDEX_LAYER = 0, 1
-SCORE_AUTO, SCORE_TWO_PASS, SCORE_ONE_PASS = 0, 1, 2
+SCORE_AUTO, SCORE_TWO_PASS, SCORE_ONE_PASS, SCORE_TWO_LAUNCHES = 0, 1, 2, 3
 SPIN_DEFAULT, SPIN_CATCHUP_ALL = -1, -2
 
 _INCLUDE = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")

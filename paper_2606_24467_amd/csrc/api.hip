@@ -45,7 +45,8 @@ struct Plan {
   int lead1 = 1, lead2 = 1;  // leading workgroups per (sequence, group) and layer
   uint32_t head_end_mask = 0;
   // workspace: table | scores | counters (ticket, arrivals, normalisers,
-  // histograms) | partial statistics | skip list | edge window sums
+  // histograms) | partial statistics | skip list | edge window sums | the
+  // one-launch form's catch-up list | split-selection slices
   size_t table_off = 0, scores_off = 0, counters_off = 0, arrive_off = 0, bias_off = 0,
          hist_off = 0, stats_off = 0, skip_off = 0, edges_off = 0, total = 0;
   int64_t stats_layer = 0, hist_layer = 0;   // elements per layer
@@ -59,6 +60,9 @@ struct Plan {
   int n_op = 0;            // layers scored in a single pass: the first n_op table entries
   int op_rt_max = 0, tp_rt_max = 0;   // row tiles of those layers / of the others
   int op_grid = 0;         // persistent workgroups of the single-pass kernel
+  // two-pass scoring in one launch (fused_kernel)
+  bool fused = false;
+  size_t fskip_off = 0;    // its catch-up list: count, then workgroup indices
   std::vector<int> order;  // table entry -> caller's layer (single-pass layers first)
   LayerSrh srh;            // single-layer calls
 };
@@ -113,9 +117,9 @@ int check_problem(const ckv_problem *p) {
   if (p->index_mode != CKV_INDEX_PER_GROUP && p->index_mode != CKV_INDEX_LAYER)
     return fail(CKV_INVALID_ARGUMENT, "index_mode must be CKV_INDEX_PER_GROUP or CKV_INDEX_LAYER");
   if (p->scoring != CKV_SCORE_AUTO && p->scoring != CKV_SCORE_TWO_PASS &&
-      p->scoring != CKV_SCORE_ONE_PASS)
-    return fail(CKV_INVALID_ARGUMENT,
-                "scoring must be CKV_SCORE_AUTO, CKV_SCORE_TWO_PASS or CKV_SCORE_ONE_PASS");
+      p->scoring != CKV_SCORE_ONE_PASS && p->scoring != CKV_SCORE_TWO_LAUNCHES)
+    return fail(CKV_INVALID_ARGUMENT, "scoring must be CKV_SCORE_AUTO, CKV_SCORE_TWO_PASS, "
+                                      "CKV_SCORE_ONE_PASS or CKV_SCORE_TWO_LAUNCHES");
   if (p->reserved != 0) return fail(CKV_INVALID_ARGUMENT, "reserved must be 0");
   if (p->index_mode == CKV_INDEX_LAYER && p->reduce_order != CKV_POOL_THEN_MEAN)
     return fail(CKV_UNSUPPORTED, "CKV_INDEX_LAYER needs reduce_order CKV_POOL_THEN_MEAN");
@@ -226,12 +230,18 @@ int op_units(int L) { return (L + ckv::kOnePassUnitKeys - 1) / ckv::kOnePassUnit
 constexpr int kOnePassMaxRowTiles = 6;
 // Polls of a late normaliser before a unit is left to the catch-up kernel.
 constexpr int kDefaultSpinLimit = 64;
+// Row tiles per group of the fused two-pass launch, and the polls of a
+// group's partials before a workgroup leaves its column sums to catch-up.
+constexpr int kFusedMaxRowTiles = 6;
+constexpr int kFusedMinChunks = 16;   // statistics chunks per sequence for CKV_SCORE_AUTO
+constexpr int kDefaultFusedSpin = 256;
 
 // Whether the problem's shape allows single-pass scoring at all (bf16 keys,
 // per-group selections, a batch that fits the kernel's ticket table); the
 // workspace of such problems always has room for it.
 bool op_shape(const ckv_problem *p) {
-  return p->scoring != CKV_SCORE_TWO_PASS && p->dtype == CKV_BF16 &&
+  return p->scoring != CKV_SCORE_TWO_PASS && p->scoring != CKV_SCORE_TWO_LAUNCHES &&
+         p->dtype == CKV_BF16 &&
          p->index_mode == CKV_INDEX_PER_GROUP && p->batch <= ckv::kOnePassMaxBatch;
 }
 
@@ -318,6 +328,24 @@ void set_layout(const ckv_problem *p, Plan &pl) {
     pl.total = pl.edges_off +
                round_up(units * (size_t)pl.nmax * 2 * pl.ew * sizeof(float), 256);
   }
+  // Both passes in one launch where its workgroups fit two to a CU (bf16, at
+  // most 6 row tiles per group); the library's own choice also needs every
+  // sequence to give most of a group's workgroups a statistics chunk (shorter
+  // sequences leave them idle: two launches are faster there, as measured).
+  bool long_enough = true;
+  for (int b = 0; b < p->batch; ++b)
+    long_enough = long_enough && p->cu_seqlens_host[b + 1] - p->cu_seqlens_host[b] >=
+                                     kFusedMinChunks * pl.chunk1;
+  // (its catch-up list is reserved wherever the shape allows it, so that the
+  // workspace size does not depend on the scoring field)
+  const bool fused_shape = p->dtype == CKV_BF16 && pl.rt_max <= kFusedMaxRowTiles;
+  pl.fused = fused_shape && (p->scoring == CKV_SCORE_TWO_PASS ||
+                             (p->scoring == CKV_SCORE_AUTO && long_enough));
+  if (fused_shape) {
+    pl.fskip_off = round_up(pl.total, 256);
+    const int64_t nb = ckv::fused_blocks(p->n_kv_heads, p->batch * n);
+    pl.total = pl.fskip_off + round_up((size_t)(1 + nb) * sizeof(int), 256);
+  }
   // Selections over more than one slice of prefix positions are split over
   // their slices (per-group index sets, whose first digit the column sums
   // count).
@@ -396,6 +424,11 @@ ckv::ScoreArgs score_args(const ckv_problem *p, const Plan &pl, void *ws) {
   a.pool_type = p->pool_type;
   a.reduce_order = p->reduce_order;
   a.head_end_mask = pl.head_end_mask;
+  a.fused_skip =
+      pl.fused ? reinterpret_cast<int *>(static_cast<char *>(ws) + pl.fskip_off) : nullptr;
+  a.fused_spin = p->spin_limit == CKV_SPIN_CATCHUP_ALL ? -1
+                 : p->spin_limit < 0                 ? kDefaultFusedSpin
+                                                     : p->spin_limit;
   return a;
 }
 
@@ -750,7 +783,7 @@ int compresskv_scoring_path(const ckv_problem *p, const uint8_t *srh_mask_host) 
   if ((st = check_mask(p, srh_mask_host, pl))) return -st;
   if ((st = make_plan(p, 1, pl, true))) return -st;
   ok();
-  return pl.n_op > 0 ? 1 : 2;
+  return pl.n_op > 0 ? 1 : pl.fused ? 3 : 2;
 }
 
 size_t compresskv_workspace_bytes(const ckv_problem *p, const uint8_t *srh_mask_host,

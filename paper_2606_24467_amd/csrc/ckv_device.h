@@ -157,7 +157,19 @@ struct ScoreArgs {
   float c1;               // softmax scale * log2(e): logits in base-2 units
   int32_t pool_kernel, pool_type, reduce_order;
   uint32_t head_end_mask;  // bit rt set if row tile rt is the last tile of an SRH
+  // Both passes in one launch (score_kernels.h, fused_kernel); null: two launches.
+  int *fused_skip;         // [0]: entries, then the workgroups left to the catch-up kernel
+  int32_t fused_spin;      // polls of a group's partials before a workgroup leaves its column
+                           // sums to the catch-up kernel (< 0: all of them)
 };
+
+// Workgroups per (sequence, group) and pass of the fused two-pass launch, and
+// its grid (8 XCDs x 2 passes x kFusedMembers per 8 (sequence, group) pairs;
+// nz sequences x layers).
+constexpr int kFusedMembers = 32;
+__host__ __device__ inline int64_t fused_blocks(int Hkv, int nz) {
+  return (int64_t)kFusedMembers * 8 * 2 * (((int64_t)Hkv * nz + 7) / 8);
+}
 
 // Arguments of the single-pass scoring kernels (operands in the layer table:
 // the launch covers table layers 0 .. n_layers - 1).

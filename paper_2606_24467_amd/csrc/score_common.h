@@ -47,16 +47,20 @@ __device__ __forceinline__ void q_load(const ScoreArgs &a, const LayerView &lv, 
                                        uint4 (&qv)[QStage<T, D, RTM, NT>::n]) {
   constexpr int U4 = QLayout<T, D>::U4;
   const gptr<const char> qb = lv.q;
+  // the group's SRH head indices, one per lane, read once: the query loads
+  // then depend on a single load instead of one per row
+  int hv = 0;
+  if ((int)(threadIdx.x & 63) < lv.nsrh) hv = lv.srh_head[lv.off + (threadIdx.x & 63)];
 #pragma unroll
   for (int it = 0; it < QStage<T, D, RTM, NT>::n; ++it) {
     const int idx = (int)threadIdx.x + it * NT;
     const int row = idx / U4, u = idx - row * U4;
     const int rt = row >> 4, c = row & 15;
     qv[it] = make_uint4(0, 0, 0, 0);
+    const int head = __shfl(hv, min(rt / a.th, 63));   // every lane takes part
     if (rt < rt_n) {
       const int i = (rt % a.th) * 16 + c;
       if (i < a.W) {
-        const int head = lv.srh_head[lv.off + rt / a.th];
         qv[it] = load16(qb + (((int64_t)b * a.W + i) * a.Hq + head) * (int64_t)(D * sizeof(T)) +
                         16 * u);
       }
@@ -309,6 +313,58 @@ __device__ __forceinline__ void merge_row_bias(const ScoreArgs &a, const float2 
     bias_s[row] = (i < a.W) ? m + fast_log2(sm) : INFINITY;
   }
   for (int r = rows + tid; r < rows_cap; r += NT) bias_s[r] = INFINITY;
+}
+
+// merge_row_bias over partials that other workgroups of the same launch
+// publish: each is read at agent scope and carries its own arrival mark (the
+// sum is stored negated, so a set sign bit means written; the slots start at
+// +0 and a sum is never negative).  Until every partial has arrived the reads
+// are repeated, at most `spin` more times; returns false (uniformly) if one
+// never arrived.  Same merge order and arithmetic as merge_row_bias.
+template <int NT, int kBatch = 8>
+__device__ __forceinline__ bool merge_row_bias_marked(const ScoreArgs &a, const float2 *parts,
+                                                      int64_t stride, int n_parts, int rows,
+                                                      int rows_cap, float *bias_s, int spin) {
+  const int tid = threadIdx.x;
+  int tpr = 1;
+  while (tpr * 2 * rows <= NT && tpr < 32) tpr *= 2;
+  const int row = tid / tpr, sub = tid % tpr;
+  float m, sm;
+  for (int attempt = 0;; ++attempt) {
+    m = -INFINITY;
+    sm = 0.f;
+    bool mine = true;
+    if (row < rows) {
+      for (int k0 = sub; k0 < n_parts; k0 += kBatch * tpr) {
+        float2 v[kBatch];
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+          const int k = min(k0 + j * tpr, n_parts - 1);
+          v[j] = load_partial_coherent(parts + (int64_t)k * stride + row);
+        }
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+          if (k0 + j * tpr < n_parts) {
+            mine = mine && signbit(v[j].y);
+            merge_stats(m, sm, v[j].x, -v[j].y);
+          }
+        }
+      }
+    }
+    if (__syncthreads_and(mine)) break;
+    if (attempt >= spin) return false;
+    __builtin_amdgcn_s_sleep(4);
+  }
+  for (int o = 1; o < tpr; o <<= 1) {
+    const float mo = __shfl_xor(m, o), so = __shfl_xor(sm, o);
+    merge_stats(m, sm, mo, so);
+  }
+  if (row < rows && sub == 0) {
+    const int i = row % (16 * a.th);
+    bias_s[row] = (i < a.W) ? m + fast_log2(sm) : INFINITY;
+  }
+  for (int r = rows + tid; r < rows_cap; r += NT) bias_s[r] = INFINITY;
+  return true;
 }
 
 // Window sums of one key tile for every SRH of the group (MFMA operands: A =

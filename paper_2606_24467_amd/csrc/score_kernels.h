@@ -103,7 +103,7 @@ constexpr bool kSliceBarrier = RTM >= 8;
 template <typename T, int D, int RTM>
 constexpr int kStatsMinWaves = RTM >= 8 && Slices<T, D>::n >= 4 ? 3 : 1;
 
-template <typename T, int D, int RT, bool SB>
+template <typename T, int D, int RT, bool SB, bool MARK = false>
 __device__ __forceinline__ void stats_body(const ScoreArgs &a, const Work &w, uint4 *q_lds,
                                            float2 (*part)[kStatsPartRows]) {
   constexpr int NW = kStatsWaves;
@@ -170,7 +170,11 @@ __device__ __forceinline__ void stats_body(const ScoreArgs &a, const Work &w, ui
       float r0 = part[0][tid].x, s_0 = part[0][tid].y;
 #pragma unroll
       for (int v = 1; v < NW; ++v) merge_stats(r0, s_0, part[v][tid].x, part[v][tid].y);
-      parts[(int64_t)chunk * a.row_slots + tid] = make_float2(r0, s_0);
+      if constexpr (MARK) {   // published to the other workgroups of the launch
+        store_partial_coherent(parts + (int64_t)chunk * a.row_slots + tid, make_float2(r0, -s_0));
+      } else {
+        parts[(int64_t)chunk * a.row_slots + tid] = make_float2(r0, s_0);
+      }
     }
     __syncthreads();   // part is reused by the next chunk
     ready = false;
@@ -237,10 +241,13 @@ __attribute__((amdgpu_waves_per_eu(kStatsMinWaves<T, D, RTM>))) void stats_kerne
 // waves per SIMD); four slots measured slower (268 VGPRs, one wave).
 constexpr int kRingCs = 2;
 
-template <typename T, int D, int RT, int CSW, bool SB>
-__device__ __forceinline__ void colsum_body(const ScoreArgs &a, const Work &w, uint4 *q_lds,
+// FUSED: the partials come from the workgroups of the same launch (marked,
+// polled at most `spin` more times); returns false, with nothing written, if
+// one has not arrived.
+template <typename T, int D, int RT, int CSW, bool SB, bool FUSED = false>
+__device__ __forceinline__ bool colsum_body(const ScoreArgs &a, const Work &w, uint4 *q_lds,
                                             float *bias_s, float (*cs)[CSW], float *stage,
-                                            int *hist_s) {
+                                            int *hist_s, int spin = 0) {
   constexpr int NS = Slices<T, D>::n, RQ = RegTiles<T, D, RT>::v;
   constexpr int NT = 64 * kWaves;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -270,10 +277,16 @@ __device__ __forceinline__ void colsum_body(const ScoreArgs &a, const Work &w, u
 
   // Row normalisers bias = ref + log2(sum), merged over every chunk of the
   // statistics pass; rows past the group's own get +inf.
-  merge_row_bias<NT>(a,
-                     a.stats + w.layer * a.stats_layer +
-                         ((int64_t)w.b * a.Hkv + g) * a.parts_stride * a.row_slots,
-                     a.row_slots, (L + a.chunk1 - 1) / a.chunk1, w.rt_n * 16, RT * 16, bias_s);
+  const float2 *parts =
+      a.stats + w.layer * a.stats_layer + ((int64_t)w.b * a.Hkv + g) * a.parts_stride * a.row_slots;
+  const int n_parts = (L + a.chunk1 - 1) / a.chunk1;
+  if constexpr (FUSED) {
+    if (!merge_row_bias_marked<NT>(a, parts, a.row_slots, n_parts, w.rt_n * 16, RT * 16, bias_s,
+                                   spin))
+      return false;
+  } else {
+    merge_row_bias<NT>(a, parts, a.row_slots, n_parts, w.rt_n * 16, RT * 16, bias_s);
+  }
   __syncthreads();
   uint4 qreg[RegTiles<T, D, RT>::n][NS];
 #pragma unroll
@@ -327,6 +340,7 @@ __device__ __forceinline__ void colsum_body(const ScoreArgs &a, const Work &w, u
   }
   flush_hist<NT>(hist_s,
                  a.hist + w.layer * a.hist_layer + ((int64_t)w.b * a.Hkv + g) * kHistBins);
+  return true;
 }
 
 template <typename T, int D, int RTM, bool ML>
@@ -371,12 +385,212 @@ __global__ __launch_bounds__(64 * kWaves) void colsum_kernel(const ScoreArgs a) 
 }
 
 // ---------------------------------------------------------------------------
+// Both passes in one launch (fused_kernel).  The (sequence, group) pairs of
+// the launch ("segments") each get kFusedMembers workgroups: member m first
+// computes the statistics partials of a run of consecutive chunk1 chunks and
+// publishes them (agent-scope stores, each partial marked), then, for a run
+// of chunk2 = kFusedChunk2 chunks, waits until every partial of its segment
+// has arrived and computes the column sums, pooling and histogram exactly as
+// colsum_kernel does.  The normalisers, and so the scores, are bit for bit
+// those of the two-launch form.  While a segment's members wait or work on
+// their column sums, the workgroups of the next segment on the same CUs
+// stream their statistics, so the launch has no drain between the passes.
+// The members of a segment are consecutive workgroups of one XCD (launch
+// order goes round the 8 XCDs), so a segment's members start together; that
+// matters for speed only.  A member whose partials have not all arrived
+// after `fused_spin` polls records itself and returns: fused_catchup_kernel
+// (next on the stream, when every partial is written) does its column sums
+// with the same code.  Key runs are kFusedChunk2 = 1120 (+ 32 halo keys =
+// 9 x 128) so that 32 members cover a 32768-key sequence's column sums.
+// ---------------------------------------------------------------------------
+constexpr int kFusedChunk2 = 1120;
+constexpr int kFusedCsw = kFusedChunk2 + 32;
+
+// LDS of the fused kernel; it runs where two workgroups fit a CU.
+template <typename T, int D, int RTM>
+struct FusedLds {
+  uint4 q[RTM * 16 * QLayout<T, D>::STRIDE];
+  float2 part[kStatsWaves][kStatsPartRows];
+  float bias[RTM * 16];
+  float cs[RTM][kFusedCsw];
+  alignas(16) float stage[kFusedChunk2 + 4];
+  int hist[kHistBins];
+};
+template <typename T, int D, int RTM>
+constexpr bool kFusedFits = RTM <= 6 && sizeof(FusedLds<T, D, RTM>) <= 80 * 1024;
+
+// Segment u of the launch: the group is rotated by the (layer, sequence)
+// index as in block_range.
+__device__ __forceinline__ int fused_group(const ScoreArgs &a, int u) {
+  const int z = u / a.Hkv;
+  return (u % a.Hkv + z) % a.Hkv;
+}
+
+template <bool ML>
+__device__ __forceinline__ bool fused_work(const ScoreArgs &a, int u, Work &w) {
+  const int z = u / a.Hkv;
+  w.g = fused_group(a, u);
+  w.layer = ML ? z / a.batch : 0;
+  w.b = z - w.layer * a.batch;
+  w.lv = layer_view<ML>(a, w.layer, w.g);
+  w.kbase = w.lv.k;
+  w.s0 = a.cu[w.b];
+  w.L = a.cu[w.b + 1] - w.s0;
+  w.P = w.L - a.W;
+  w.rt_n = w.lv.nsrh * a.th;
+  return w.lv.nsrh > 0 && w.L > 0;
+}
+
+// Role of workgroup bid of the fused grid.  Each XCD (bid % 8) serves the
+// segments x, x + 8, x + 16, ... (s_0, s_1, ...) in blocks of kFusedMembers
+// consecutive workgroups: the statistics of s_0 and s_1, then the column sums
+// of s_0, the statistics of s_2, the column sums of s_1, ... and finally the
+// column sums of the last two.  A segment's column sums thus start a whole
+// block of statistics after its own statistics.
+struct FusedRole {
+  int u;        // segment (>= the launch's segments: nothing to do)
+  int member;
+  bool colsum;  // false: statistics
+};
+__device__ __forceinline__ FusedRole fused_role(int bid, int n_seg) {
+  const int x = bid % 8, q = bid / 8;
+  const int k = q / kFusedMembers;
+  const int n = (n_seg - x + 7) / 8;   // segments of this XCD
+  FusedRole r;
+  r.member = q % kFusedMembers;
+  int i;
+  if (k == 0) {
+    i = 0;
+    r.colsum = false;
+  } else if (k >= 2 * n - 1) {
+    i = k - n;   // k = 2n - 1: the last segment's column sums
+    r.colsum = true;
+  } else if (k & 1) {
+    i = (k + 1) / 2;
+    r.colsum = false;
+  } else {
+    i = k / 2 - 1;
+    r.colsum = true;
+  }
+  r.u = (k < 2 * n) ? x + 8 * i : n_seg;
+  return r;
+}
+
+// Zeroes the launch's partial slots (arrival marks), its histograms and the
+// catch-up list before the fused kernel.
+static __global__ __launch_bounds__(256) void fused_fill_kernel(int *p0, int64_t n0, int *p1,
+                                                                int64_t n1, int *p2) {
+  const int64_t n = n0 + n1;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * 256) {
+    if (i < n0) p0[i] = 0;
+    else p1[i - n0] = 0;
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) p2[0] = 0;
+}
+
+// Member `member`'s statistics chunks of segment w: published partials.
+template <typename T, int D, int RTM>
+__device__ __forceinline__ void fused_stats(const ScoreArgs &a, const Work &w, int member,
+                                            FusedLds<T, D, RTM> &sm) {
+  const int n1 = (w.L + a.chunk1 - 1) / a.chunk1;
+  const int c1n = (n1 + kFusedMembers - 1) / kFusedMembers;
+  const int j1 = member * c1n;
+  if (j1 >= n1) return;
+  Work ws = w;
+  ws.c0 = j1 * a.chunk1;
+  ws.n_chunks = min(c1n, n1 - j1);
+  dispatch_rt<RTM>(w.rt_n, [&]<int RT>() {
+    stats_body<T, D, RT, kSliceBarrier<RTM>, true>(a, ws, sm.q, sm.part);
+  });
+  __syncthreads();   // sm is reused by the next phase
+}
+
+// Member `member`'s column-sum chunks of segment w; false if a partial had
+// not arrived after `spin` more polls (nothing written then).
+template <typename T, int D, int RTM>
+__device__ __forceinline__ bool fused_colsum(const ScoreArgs &a, const Work &w, int member,
+                                             FusedLds<T, D, RTM> &sm, int spin) {
+  const int n2 = w.P > 0 ? (w.P + a.chunk2 - 1) / a.chunk2 : 0;
+  const int c2n = (n2 + kFusedMembers - 1) / kFusedMembers;
+  const int j2 = member * c2n;
+  if (j2 >= n2) return true;
+  Work wc = w;
+  wc.c0 = j2 * a.chunk2;
+  wc.n_chunks = min(c2n, n2 - j2);
+  bool ok = true;
+  dispatch_rt<RTM>(w.rt_n, [&]<int RT>() {
+    ok = colsum_body<T, D, RT, kFusedCsw, kSliceBarrier<RTM>, true>(a, wc, sm.q, sm.bias, sm.cs,
+                                                                   sm.stage, sm.hist, spin);
+  });
+  __syncthreads();
+  return ok;
+}
+
+template <typename T, int D, int RTM, bool ML>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void fused_kernel(
+    const ScoreArgs a) {
+  static_assert(64 * kStatsWaves == 256 && 64 * kWaves == 256, "one workgroup shape");
+  const FusedRole r = fused_role(blockIdx.x, a.nz * a.Hkv);
+  if (r.u >= a.nz * a.Hkv) return;
+  __shared__ FusedLds<T, D, RTM> sm;
+  Work w;
+  if (!fused_work<ML>(a, r.u, w)) return;
+  if (!r.colsum) {
+    if (r.member == 0) {   // window positions are always kept
+      const gptr<float> out = w.lv.scores + (int64_t)w.g * a.T + w.s0;
+      for (int j = max(w.P, 0) + (int)threadIdx.x; j < w.L; j += 256) out[j] = INFINITY;
+    }
+    fused_stats<T, D, RTM>(a, w, r.member, sm);
+    return;
+  }
+  const bool done =
+      a.fused_spin >= 0 && fused_colsum<T, D, RTM>(a, w, r.member, sm, a.fused_spin);
+  if (!done && threadIdx.x == 0)
+    a.fused_skip[1 + atomicAdd(&a.fused_skip[0], 1)] = r.u * kFusedMembers + r.member;
+}
+
+// The column sums the fused kernel left (entries u * kFusedMembers + member),
+// after it: every partial is written by then.
+template <typename T, int D, int RTM, bool ML>
+__global__ __launch_bounds__(256) void fused_catchup_kernel(const ScoreArgs a) {
+  __shared__ FusedLds<T, D, RTM> sm;
+  const int n = a.fused_skip[0];
+  for (int i = blockIdx.x; i < n; i += gridDim.x) {
+    const int e = a.fused_skip[1 + i];
+    Work w;
+    fused_work<ML>(a, e / kFusedMembers, w);
+    fused_colsum<T, D, RTM>(a, w, e % kFusedMembers, sm, 0);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Host-side launcher template; grid z = batch * n_layers (n_layers = 1 unless ML).
 // ---------------------------------------------------------------------------
 template <typename T, int D, int RTM, bool ML>
 static hipError_t launch_score_t(const ScoreArgs &args, int nz, hipStream_t stream) {
   ScoreArgs a = args;
   a.nz = nz;
+  if (a.fused_skip != nullptr) {
+    if constexpr (kFusedFits<T, D, RTM>) {
+      a.chunk2 = kFusedChunk2;   // the column-sum runs of the fused grid
+      const int n_layers = ML ? nz / a.batch : 1;
+      const int64_t nb = fused_blocks(a.Hkv, nz);
+      if (nb > INT32_MAX) return hipErrorInvalidConfiguration;
+      hipLaunchKernelGGL(fused_fill_kernel, dim3(1024), dim3(256), 0, stream,
+                         reinterpret_cast<int *>(a.stats), (int64_t)a.stats_layer * n_layers * 2,
+                         a.hist, (int64_t)a.hist_layer * n_layers, a.fused_skip);
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      hipLaunchKernelGGL((fused_kernel<T, D, RTM, ML>), dim3((unsigned)nb), dim3(256), 0, stream,
+                         a);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+      hipLaunchKernelGGL((fused_catchup_kernel<T, D, RTM, ML>), dim3(256), dim3(256), 0, stream, a);
+      return hipGetLastError();
+    } else {
+      return hipErrorInvalidConfiguration;   // the host plans the fused launch only where it fits
+    }
+  }
   const int64_t n1 = grid_blocks(a.Hkv, nz, a.lead1, a.cpw1, a.max_chunks1);
   const int64_t n2 = grid_blocks(a.Hkv, nz, a.lead2, a.cpw2, a.max_chunks2);
   if (n1 < 1 || n2 < 1 || n1 > INT32_MAX || n2 > INT32_MAX) return hipErrorInvalidConfiguration;

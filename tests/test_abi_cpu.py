@@ -106,7 +106,7 @@ INVALID = [
     ("stride zero", dict(v_stride_head=0), C.INVALID_ARGUMENT),
     ("head stride below head_dim", dict(k_stride_head=120), C.INVALID_ARGUMENT),
     ("token stride below head_dim", dict(v_stride_tok=64), C.INVALID_ARGUMENT),
-    ("scoring", dict(scoring=3), C.INVALID_ARGUMENT),
+    ("scoring", dict(scoring=4), C.INVALID_ARGUMENT),
     ("too many kv heads", dict(n_kv_heads=256, n_q_heads=256), C.UNSUPPORTED),
     ("index mode", dict(index_mode=2), C.INVALID_ARGUMENT),
     ("reserved", dict(reserved=1), C.INVALID_ARGUMENT),

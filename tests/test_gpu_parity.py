@@ -223,12 +223,16 @@ def test_deterministic_bits(gpu):
 
 
 def test_scoring_path_choice_for_the_benchmark_shapes(gpu, scoring_path):
-    """CKV_SCORE_AUTO takes the two-pass kernels; the forced paths are
-    honoured, or refused with CKV_UNSUPPORTED where the single pass does not
-    apply."""
+    """CKV_SCORE_AUTO takes the two passes, in one launch for bf16 with at
+    most 6 row tiles per group; CKV_SCORE_TWO_LAUNCHES always in two; the
+    forced paths are honoured, or refused with CKV_UNSUPPORTED where the
+    single pass does not apply."""
     one_pass = {"llama1": True, "llama32": True, "ragged8": True,   # where it may be forced
                 "tiny": False,        # fp32
                 "qwen128k": False}    # W = 64 with 2 SRHs: 8 row tiles per group
+    one_launch = {"llama1": True, "llama32": True, "ragged8": True, "tiny": False,
+                  "qwen128k": False}              # CKV_SCORE_TWO_PASS
+    auto_one_launch = dict(one_launch, ragged8=False)   # 4k-16k keys: two launches
     for name, kw in [("llama1", {}), ("llama32", {}), ("ragged8", {}), ("tiny", {}),
                      ("qwen128k", dict(seq_len=32768))]:
         w = wl.get(name, **kw)
@@ -239,11 +243,14 @@ def test_scoring_path_choice_for_the_benchmark_shapes(gpu, scoring_path):
         k = torch.empty((16, w.n_kv_heads, w.head_dim), device=gpu, dtype=q.dtype)
         cud = torch.from_numpy(cu).to(gpu)
         mask = wl.srh_mask(w, 0)
+        two = 3 if one_launch[name] else 2
         auto = C.Problem(q, k, k, cud, cu_seqlens_host=cu, scoring=C.SCORE_AUTO)
-        assert C.compresskv_scoring_path(auto, mask) == 2, name
+        assert C.compresskv_scoring_path(auto, mask) == (3 if auto_one_launch[name] else 2), name
+        split = C.Problem(q, k, k, cud, cu_seqlens_host=cu, scoring=C.SCORE_TWO_LAUNCHES)
+        assert C.compresskv_scoring_path(split, mask) == 2, name
         forced = C.Problem(q, k, k, cud, cu_seqlens_host=cu, scoring=PATHS[scoring_path])
         if scoring_path == "two":
-            assert C.compresskv_scoring_path(forced, mask) == 2, name
+            assert C.compresskv_scoring_path(forced, mask) == two, name
         elif one_pass[name]:
             assert C.compresskv_scoring_path(forced, mask) == 1, name
         else:
