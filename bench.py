@@ -33,39 +33,62 @@ METRIC = "prompt tokens compressed/sec per layer (1 GPU); % HBM roofline; MFMA u
 HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # dense, MI355X
 
-# HBM bytes moved by one score phase (stats_kernel + colsum_kernel), measured
-# with rocprofv3: FETCH_SIZE x 2 (the factor a plain copy of known size gives
-# on this GPU) + WRITE_SIZE, in KiB per dispatch, in separate runs (profiles/).
-# A figure is valid only for the kernel sources it was taken with: keyed by
-# their hash.  Single-layer workloads: one layer's score phase.
-def _traffic(fetch_stats, fetch_colsum, write_stats, write_colsum):
-    return (2 * (fetch_stats + fetch_colsum) + write_stats + write_colsum) * 1024
+# HBM bytes moved by one score phase (its kernels: fused_fill_kernel +
+# fused_kernel + fused_catchup_kernel in one launch, or stats_kernel +
+# colsum_kernel), measured with rocprofv3: FETCH_SIZE x 2 (the factor a plain
+# copy of known size gives on this GPU) + WRITE_SIZE, in KiB per dispatch, in
+# separate runs (profiles/).  A figure is valid only for the kernel sources it
+# was taken with: keyed by their hash.  Single-layer workloads: one layer's
+# score phase.
+def _traffic(**kernels):
+    """kernel name -> (FETCH_SIZE KiB, WRITE_SIZE KiB) per dispatch."""
+    return sum(2 * f + w for f, w in kernels.values()) * 1024
 
 
 MEASURED_TRAFFIC = {
-    ("llama32", 32, "c630a66cd07a2dbe"): _traffic(1080432.45, 1168574.175, 6248.0, 33069.1875),
-    ("qwen128k", 28, "c630a66cd07a2dbe"): _traffic(1852764.65, 1947780.9, 8064.0, 57591.34375),
-    ("ragged8", 32, "c630a66cd07a2dbe"): _traffic(2672889.625, 2843529.3375, 22016.0, 82243.09375),
-    ("paper", 32, "c630a66cd07a2dbe"): _traffic(449888.3625, 482387.7125, 2560.0, 14199.01875),
-    ("llama1", 1, "c630a66cd07a2dbe"): _traffic(33428.1, 40078.6125, 192.0, 1045.63125),
-    ("tiny", 1, "c630a66cd07a2dbe"): _traffic(297.4, 332.25, 16.5, 8.41875),
+    ("llama32", 32, "05a14804cfdb7f0c"): _traffic(
+        fused_fill_kernel=(14.58, 8192.03),
+        fused_kernel=(2286203.83, 37605.53),
+        fused_catchup_kernel=(11.5, 0.0)),
+    ("paper", 32, "05a14804cfdb7f0c"): _traffic(
+        fused_fill_kernel=(14.53, 4096.03),
+        fused_kernel=(959187.85, 14993.56),
+        fused_catchup_kernel=(17.0, 0.0)),
+    ("llama1", 1, "05a14804cfdb7f0c"): _traffic(
+        fused_fill_kernel=(14.51, 192.03),
+        fused_kernel=(63584.68, 1172.08),
+        fused_catchup_kernel=(18.0, 0.0)),
+    ("qwen128k", 28, "05a14804cfdb7f0c"): _traffic(
+        stats_kernel=(1852906.74, 8064.0),
+        colsum_kernel=(1947911.93, 57591.34)),
+    ("ragged8", 32, "05a14804cfdb7f0c"): _traffic(
+        stats_kernel=(2673305.86, 22016.0),
+        colsum_kernel=(2843553.59, 82244.47)),
+    ("tiny", 1, "05a14804cfdb7f0c"): _traffic(
+        stats_kernel=(299.29, 16.5),
+        colsum_kernel=(327.0, 8.42)),
 }
 
 # MFMA work the score phase executes, from rocprofv3 on the same sources:
-# SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 FLOP of both kernels, and each kernel's
-# SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 XCDs x 1024 SIMDs).
-def _mfma(mops_stats, mops_colsum, busy_stats, busy_colsum, gui_stats, gui_colsum):
-    return {"executed_flops_per_launch": (mops_stats + mops_colsum) * 512,
-            "busy_frac": {"stats_kernel": busy_stats / (gui_stats / 8 * 1024),
-                          "colsum_kernel": busy_colsum / (gui_colsum / 8 * 1024)}}
+# SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 FLOP summed over its kernels, and each
+# kernel's SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 XCDs x 1024 SIMDs).
+def _mfma(**kernels):
+    """kernel name -> (MFMA_MOPS_BF16, MFMA busy cycles, GRBM_GUI_ACTIVE) per dispatch."""
+    return {"executed_flops_per_launch": sum(m for m, _, _ in kernels.values()) * 512,
+            "busy_frac": {k: b / (g / 8 * 1024) for k, (_, b, g) in kernels.items()}}
 
 
 MEASURED_MFMA = {
-    ("llama32", 32, "c630a66cd07a2dbe"): _mfma(275251200, 290304000, 137625600, 145152000, 6637385.2,
-                                  8146807.4),
-    ("qwen128k", 28, "c630a66cd07a2dbe"): _mfma(939524096, 987693056, 469762048, 493846528, 10763302.2,
-                                   14438370.6),
-    ("paper", 32, "c630a66cd07a2dbe"): _mfma(33554432, 36503552, 16777216, 18251776, 3640013.6, 4104640.0),
+    ("llama32", 32, "05a14804cfdb7f0c"): _mfma(
+        fused_kernel=(581683200.0, 290841600.0, 14884166.03)),
+    ("paper", 32, "05a14804cfdb7f0c"): _mfma(fused_kernel=(70909952.0, 35454976.0, 6625183.12)),
+    ("llama1", 1, "05a14804cfdb7f0c"): _mfma(fused_kernel=(17727488.0, 8863744.0, 798013.41)),
+    ("qwen128k", 28, "05a14804cfdb7f0c"): _mfma(
+        stats_kernel=(939524096.0, 469762048.0, 11049113.59),
+        colsum_kernel=(987693056.0, 493846528.0, 14673099.09)),
+    ("ragged8", 32, "05a14804cfdb7f0c"): _mfma(
+        stats_kernel=(738197504.0, 369098752.0, 19622201.41),
+        colsum_kernel=(731906048.0, 365953024.0, 22953341.09)),
 }
 
 

@@ -442,11 +442,12 @@ __device__ __forceinline__ bool fused_work(const ScoreArgs &a, int u, Work &w) {
 }
 
 // Role of workgroup bid of the fused grid.  Each XCD (bid % 8) serves the
-// segments x, x + 8, x + 16, ... (s_0, s_1, ...) in blocks of kFusedMembers
-// consecutive workgroups: the statistics of s_0 and s_1, then the column sums
-// of s_0, the statistics of s_2, the column sums of s_1, ... and finally the
-// column sums of the last two.  A segment's column sums thus start a whole
-// block of statistics after its own statistics.
+// segments x, x + 8, x + 16, ... (s_0 .. s_{n-1}) in blocks of kFusedMembers
+// consecutive workgroups: the statistics of s_0 .. s_S, then the column sums
+// of s_0 and the statistics of s_{S+1}, the column sums of s_1 and the
+// statistics of s_{S+2}, ..., and finally the remaining column sums.  A
+// segment's column sums thus start S blocks of statistics after its own.
+constexpr int kFusedSlack = 1;
 struct FusedRole {
   int u;        // segment (>= the launch's segments: nothing to do)
   int member;
@@ -458,35 +459,42 @@ __device__ __forceinline__ FusedRole fused_role(int bid, int n_seg) {
   const int n = (n_seg - x + 7) / 8;   // segments of this XCD
   FusedRole r;
   r.member = q % kFusedMembers;
+  const int A = min(kFusedSlack + 1, n);   // statistics blocks before the first column sums
+  const int P = max(0, n - A);             // (column sums, statistics) pairs after them
+  const int t = k - A;
   int i;
-  if (k == 0) {
-    i = 0;
+  if (k < A) {
+    i = k;
     r.colsum = false;
-  } else if (k >= 2 * n - 1) {
-    i = k - n;   // k = 2n - 1: the last segment's column sums
-    r.colsum = true;
-  } else if (k & 1) {
-    i = (k + 1) / 2;
-    r.colsum = false;
+  } else if (t < 2 * P) {
+    r.colsum = (t & 1) == 0;
+    i = r.colsum ? t / 2 : A + t / 2;
   } else {
-    i = k / 2 - 1;
+    i = P + (t - 2 * P);
     r.colsum = true;
   }
   r.u = (k < 2 * n) ? x + 8 * i : n_seg;
   return r;
 }
 
-// Zeroes the launch's partial slots (arrival marks), its histograms and the
-// catch-up list before the fused kernel.
-static __global__ __launch_bounds__(256) void fused_fill_kernel(int *p0, int64_t n0, int *p1,
-                                                                int64_t n1, int *p2) {
-  const int64_t n = n0 + n1;
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n;
+// Zeroes the partial slots the launch uses (arrival marks: the first
+// max_chunks1 of each group's slots), its histograms and the catch-up list
+// before the fused kernel.
+static __global__ __launch_bounds__(256) void fused_fill_kernel(int *stats, int64_t n_groups,
+                                                                int64_t group_stride,
+                                                                int64_t group_ints, int *hist,
+                                                                int64_t hist_ints, int *skip) {
+  const int64_t n0 = n_groups * group_ints;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n0 + hist_ints;
        i += (int64_t)gridDim.x * 256) {
-    if (i < n0) p0[i] = 0;
-    else p1[i - n0] = 0;
+    if (i < n0) {
+      const int64_t g = i / group_ints;
+      stats[g * group_stride + (i - g * group_ints)] = 0;
+    } else {
+      hist[i - n0] = 0;
+    }
   }
-  if (blockIdx.x == 0 && threadIdx.x == 0) p2[0] = 0;
+  if (blockIdx.x == 0 && threadIdx.x == 0) skip[0] = 0;
 }
 
 // Member `member`'s statistics chunks of segment w: published partials.
@@ -577,15 +585,17 @@ static hipError_t launch_score_t(const ScoreArgs &args, int nz, hipStream_t stre
       const int n_layers = ML ? nz / a.batch : 1;
       const int64_t nb = fused_blocks(a.Hkv, nz);
       if (nb > INT32_MAX) return hipErrorInvalidConfiguration;
+      const int64_t slots = (int64_t)a.parts_stride * a.row_slots * 2;   // ints per group
       hipLaunchKernelGGL(fused_fill_kernel, dim3(1024), dim3(256), 0, stream,
-                         reinterpret_cast<int *>(a.stats), (int64_t)a.stats_layer * n_layers * 2,
-                         a.hist, (int64_t)a.hist_layer * n_layers, a.fused_skip);
+                         reinterpret_cast<int *>(a.stats), (int64_t)n_layers * a.batch * a.Hkv,
+                         slots, (int64_t)a.max_chunks1 * a.row_slots * 2, a.hist,
+                         (int64_t)a.hist_layer * n_layers, a.fused_skip);
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
       hipLaunchKernelGGL((fused_kernel<T, D, RTM, ML>), dim3((unsigned)nb), dim3(256), 0, stream,
                          a);
       if ((e = hipGetLastError()) != hipSuccess) return e;
-      hipLaunchKernelGGL((fused_catchup_kernel<T, D, RTM, ML>), dim3(256), dim3(256), 0, stream, a);
+      hipLaunchKernelGGL((fused_catchup_kernel<T, D, RTM, ML>), dim3(64), dim3(256), 0, stream, a);
       return hipGetLastError();
     } else {
       return hipErrorInvalidConfiguration;   // the host plans the fused launch only where it fits
