@@ -258,10 +258,11 @@ int compresskv_compress_layer_heads(const ckv_problem *p, const void *q_win, con
  * over K in two launches (statistics, then column sums), 3 = the same two
  * passes in one launch (each group's column-sum workgroups wait inside the
  * launch for its statistics; same bits as 2).  CKV_SCORE_TWO_PASS uses one
- * launch for bf16 inputs with at most 6 row tiles per group, else two;
- * CKV_SCORE_AUTO does the same where every sequence also spans at least 16
- * statistics chunks (about 8k-16k keys; shorter sequences leave most of the
- * one launch's workgroups idle), else two launches (on the measured shapes
+ * launch for bf16 inputs with at most 8 row tiles per group, else two;
+ * CKV_SCORE_AUTO uses one launch for bf16 inputs with at most 6 row tiles
+ * per group where every sequence also spans at least 16 statistics chunks
+ * (about 8k-16k keys; shorter sequences leave most of the one launch's
+ * workgroups idle), else two launches (the faster on the measured shapes;
  * the single pass is slower than either);
  * CKV_SCORE_TWO_LAUNCHES always uses two launches; CKV_SCORE_ONE_PASS uses
  * the single pass, which needs bf16 inputs, CKV_INDEX_PER_GROUP, batch <= 64

@@ -232,7 +232,12 @@ constexpr int kOnePassMaxRowTiles = 6;
 constexpr int kDefaultSpinLimit = 64;
 // Row tiles per group of the fused two-pass launch, and the polls of a
 // group's partials before a workgroup leaves its column sums to catch-up.
-constexpr int kFusedMaxRowTiles = 6;
+constexpr int kFusedMaxRowTiles = 8;
+// CKV_SCORE_AUTO takes the one launch up to 6 row tiles: at 8 (the Qwen shape,
+// 128 rows per group) two launches measured faster (1.65 against 1.79 ms per
+// score phase; there the statistics kernel runs three waves per SIMD, the
+// one launch two).
+constexpr int kFusedAutoMaxRowTiles = 6;
 constexpr int kFusedMinChunks = 16;   // statistics chunks per sequence for CKV_SCORE_AUTO
 constexpr int kDefaultFusedSpin = 256;
 
@@ -329,7 +334,7 @@ void set_layout(const ckv_problem *p, Plan &pl) {
                round_up(units * (size_t)pl.nmax * 2 * pl.ew * sizeof(float), 256);
   }
   // Both passes in one launch where its workgroups fit two to a CU (bf16, at
-  // most 6 row tiles per group); the library's own choice also needs every
+  // most 8 row tiles per group); the library's own choice also needs every
   // sequence to give most of a group's workgroups a statistics chunk (shorter
   // sequences leave them idle: two launches are faster there, as measured).
   bool long_enough = true;
@@ -340,7 +345,8 @@ void set_layout(const ckv_problem *p, Plan &pl) {
   // workspace size does not depend on the scoring field)
   const bool fused_shape = p->dtype == CKV_BF16 && pl.rt_max <= kFusedMaxRowTiles;
   pl.fused = fused_shape && (p->scoring == CKV_SCORE_TWO_PASS ||
-                             (p->scoring == CKV_SCORE_AUTO && long_enough));
+                             (p->scoring == CKV_SCORE_AUTO && long_enough &&
+                              pl.rt_max <= kFusedAutoMaxRowTiles));
   if (fused_shape) {
     pl.fskip_off = round_up(pl.total, 256);
     const int64_t nb = ckv::fused_blocks(p->n_kv_heads, p->batch * n);

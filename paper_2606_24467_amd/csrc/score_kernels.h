@@ -406,18 +406,30 @@ __global__ __launch_bounds__(64 * kWaves) void colsum_kernel(const ScoreArgs a) 
 constexpr int kFusedChunk2 = 1120;
 constexpr int kFusedCsw = kFusedChunk2 + 32;
 
-// LDS of the fused kernel; it runs where two workgroups fit a CU.
-template <typename T, int D, int RTM>
-struct FusedLds {
+// LDS of the fused kernel; it runs where two workgroups fit a CU.  A
+// workgroup has one role, so the statistics' per-wave partials share their
+// space with the column sums.  The pooled-score staging buffer (STAGE) is
+// left out where it would not fit (8 row tiles): those scores are stored
+// directly, as colsum_kernel does in that case.
+template <typename T, int D, int RTM, bool STAGE>
+struct FusedLdsT {
   uint4 q[RTM * 16 * QLayout<T, D>::STRIDE];
-  float2 part[kStatsWaves][kStatsPartRows];
-  float bias[RTM * 16];
-  float cs[RTM][kFusedCsw];
-  alignas(16) float stage[kFusedChunk2 + 4];
-  int hist[kHistBins];
+  union {
+    float2 part[kStatsWaves][kStatsPartRows];
+    struct {
+      float bias[RTM * 16];
+      float cs[RTM][kFusedCsw];
+      int hist[kHistBins];
+      alignas(16) float stage[STAGE ? kFusedChunk2 + 4 : 1];
+    } c;
+  };
 };
 template <typename T, int D, int RTM>
-constexpr bool kFusedFits = RTM <= 6 && sizeof(FusedLds<T, D, RTM>) <= 80 * 1024;
+constexpr bool kFusedStage = sizeof(FusedLdsT<T, D, RTM, true>) <= 80 * 1024;
+template <typename T, int D, int RTM>
+using FusedLds = FusedLdsT<T, D, RTM, kFusedStage<T, D, RTM>>;
+template <typename T, int D, int RTM>
+constexpr bool kFusedFits = RTM <= 8 && sizeof(FusedLds<T, D, RTM>) <= 80 * 1024;
 
 // Segment u of the launch: the group is rotated by the (layer, sequence)
 // index as in block_range.
@@ -528,8 +540,9 @@ __device__ __forceinline__ bool fused_colsum(const ScoreArgs &a, const Work &w, 
   wc.n_chunks = min(c2n, n2 - j2);
   bool ok = true;
   dispatch_rt<RTM>(w.rt_n, [&]<int RT>() {
-    ok = colsum_body<T, D, RT, kFusedCsw, kSliceBarrier<RTM>, true>(a, wc, sm.q, sm.bias, sm.cs,
-                                                                   sm.stage, sm.hist, spin);
+    ok = colsum_body<T, D, RT, kFusedCsw, kSliceBarrier<RTM>, true>(
+        a, wc, sm.q, sm.c.bias, sm.c.cs, kFusedStage<T, D, RTM> ? sm.c.stage : nullptr, sm.c.hist,
+        spin);
   });
   __syncthreads();
   return ok;

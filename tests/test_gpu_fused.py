@@ -1,4 +1,4 @@
-"""Two passes in one launch (CKV_SCORE_TWO_PASS on bf16 inputs with at most 6
+"""Two passes in one launch (CKV_SCORE_TWO_PASS on bf16 inputs with at most 8
 row tiles per group; CKV_SCORE_AUTO where the sequences are also long) against the same passes in two launches
 (CKV_SCORE_TWO_LAUNCHES): the normalisers merge the same partials in the same
 order, so every output must agree bit for bit, whatever the wait bound of
@@ -46,6 +46,9 @@ CASES = [
     ("window 8, pooling 5, layer-shared", "paper", dict(seq_len=6000, n_layers=1), 300),
     ("window 48, 2 SRHs (6 row tiles)", "llama1", dict(seq_len=40000, window=48, n_needle=8,
                                                          srh_per_group=(2,)), 2000),
+    ("Qwen shape, window 64, 2 SRHs (8 row tiles)", "qwen128k", dict(seq_len=20000 + 3,
+                                                                    n_layers=1, n_needle=8),
+     900),
 ]
 
 
@@ -59,7 +62,7 @@ def test_one_launch_matches_two_launches_bitwise(gpu, case):
     assert path == 2
     for spin in SPINS:
         path, got = _layer_outputs(x, gpu, C.SCORE_TWO_PASS, spin, budget)
-        assert path == 3, "bf16 with at most 6 row tiles runs in one launch"
+        assert path == 3, "bf16 with at most 8 row tiles runs in one launch"
         for a, b, what in zip(got, ref, ("idx", "k_out", "v_out", "scores")):
             assert torch.equal(a, b), f"{what} differs (spin_limit {spin})"
     _say("  ok")

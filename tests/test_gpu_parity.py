@@ -224,15 +224,17 @@ def test_deterministic_bits(gpu):
 
 def test_scoring_path_choice_for_the_benchmark_shapes(gpu, scoring_path):
     """CKV_SCORE_AUTO takes the two passes, in one launch for bf16 with at
-    most 6 row tiles per group; CKV_SCORE_TWO_LAUNCHES always in two; the
+    most 6 row tiles per group and long sequences; CKV_SCORE_TWO_PASS in one
+    launch up to 8 row tiles; CKV_SCORE_TWO_LAUNCHES always in two; the
     forced paths are honoured, or refused with CKV_UNSUPPORTED where the
     single pass does not apply."""
     one_pass = {"llama1": True, "llama32": True, "ragged8": True,   # where it may be forced
                 "tiny": False,        # fp32
                 "qwen128k": False}    # W = 64 with 2 SRHs: 8 row tiles per group
     one_launch = {"llama1": True, "llama32": True, "ragged8": True, "tiny": False,
-                  "qwen128k": False}              # CKV_SCORE_TWO_PASS
-    auto_one_launch = dict(one_launch, ragged8=False)   # 4k-16k keys: two launches
+                  "qwen128k": True}               # CKV_SCORE_TWO_PASS
+    auto_one_launch = dict(one_launch, ragged8=False,   # 4k-16k keys: two launches
+                           qwen128k=False)              # 8 row tiles: two launches
     for name, kw in [("llama1", {}), ("llama32", {}), ("ragged8", {}), ("tiny", {}),
                      ("qwen128k", dict(seq_len=32768))]:
         w = wl.get(name, **kw)
