@@ -45,7 +45,12 @@ def _replays_match(g, outs, ref, gpu, n=3):
             assert torch.equal(got, want), f"replay {r}: output {i} differs from the eager call"
 
 
-def test_multi_layer_call_in_a_graph(gpu):
+SCORING = {"auto": C.SCORE_AUTO, "one launch": C.SCORE_TWO_PASS,
+           "two launches": C.SCORE_TWO_LAUNCHES}
+
+
+@pytest.mark.parametrize("scoring", sorted(SCORING))
+def test_multi_layer_call_in_a_graph(gpu, scoring):
     w = wl.get("llama32", seq_len=5000 + 7, n_layers=3)
     layers = [wl.make_layer_device(w, l, 0, gpu) for l in range(w.n_layers)]
     q = [d["q_win"] for d in layers]
@@ -53,10 +58,10 @@ def test_multi_layer_call_in_a_graph(gpu):
     v = [d["v"] for d in layers]
     masks = np.stack([d["srh_mask"] for d in layers])
     budgets = [d["budget"] for d in layers]
-    _say(f"case graph, 3-layer stack L={w.seq_len} budgets {budgets}")
+    _say(f"case graph, 3-layer stack L={w.seq_len} budgets {budgets}, scoring {scoring}")
     p = C.Problem(q[0], k[0], v[0], layers[0]["cu_seqlens"],
                   cu_seqlens_host=layers[0]["cu_seqlens_host"], pool_kernel=w.pool_kernel,
-                  pool_type=w.pool_type)
+                  pool_type=w.pool_type, scoring=SCORING[scoring])
     idxs = [torch.empty((1, w.n_kv_heads, B), dtype=torch.int32, device=gpu) for B in budgets]
     k_outs = [torch.empty((1, w.n_kv_heads, B, w.head_dim), dtype=k[0].dtype, device=gpu)
               for B in budgets]
@@ -85,14 +90,16 @@ def test_multi_layer_call_in_a_graph(gpu):
     _replays_match(g, outs, ref2, gpu, n=2)
 
 
-def test_single_layer_call_in_a_graph(gpu):
+@pytest.mark.parametrize("scoring", sorted(SCORING))
+def test_single_layer_call_in_a_graph(gpu, scoring):
     w = wl.get("llama1", seq_len=3000 + 3, n_needle=4, batch=2, ragged=(1500, 3003))
     d = wl.make_layer_device(w, 0, 0, gpu)
     B = 300
-    _say(f"case graph, single layer lengths {np.diff(d['cu_seqlens_host']).tolist()} budget {B}")
+    _say(f"case graph, single layer lengths {np.diff(d['cu_seqlens_host']).tolist()} budget {B}, "
+         f"scoring {scoring}")
     p = C.Problem(d["q_win"], d["k"], d["v"], d["cu_seqlens"],
                   cu_seqlens_host=d["cu_seqlens_host"], pool_kernel=w.pool_kernel,
-                  pool_type=w.pool_type)
+                  pool_type=w.pool_type, scoring=SCORING[scoring])
     shape = (w.batch, w.n_kv_heads, B, w.head_dim)
     idx = torch.empty(shape[:3], dtype=torch.int32, device=gpu)
     k_out = torch.empty(shape, dtype=d["k"].dtype, device=gpu)
