@@ -46,25 +46,25 @@ def _traffic(**kernels):
 
 
 MEASURED_TRAFFIC = {
-    ("llama32", 32, "9fa707def98dad22"): _traffic(
+    ("llama32", 32, "49e6a09708c8ed70"): _traffic(
         fused_fill_kernel=(10.56, 8192.03),
-        fused_kernel=(2286486.71, 37605.53),
+        fused_kernel=(2286543.97, 37605.53),
         fused_catchup_kernel=(18.0, 0.0)),
-    ("paper", 32, "9fa707def98dad22"): _traffic(
+    ("paper", 32, "49e6a09708c8ed70"): _traffic(
         fused_fill_kernel=(10.53, 4096.03),
-        fused_kernel=(958876.97, 14993.56),
+        fused_kernel=(959031.04, 14993.56),
         fused_catchup_kernel=(18.0, 0.0)),
-    ("llama1", 1, "9fa707def98dad22"): _traffic(
+    ("llama1", 1, "49e6a09708c8ed70"): _traffic(
         fused_fill_kernel=(10.51, 192.03),
-        fused_kernel=(63988.83, 1172.08),
+        fused_kernel=(64009.9, 1172.08),
         fused_catchup_kernel=(18.0, 0.0)),
-    ("qwen128k", 28, "9fa707def98dad22"): _traffic(
-        stats_kernel=(1852994.08, 8064.0),
-        colsum_kernel=(1947915.25, 57591.34)),
-    ("ragged8", 32, "9fa707def98dad22"): _traffic(
-        stats_kernel=(2673197.93, 22016.0),
-        colsum_kernel=(2843528.43, 82244.63)),
-    ("tiny", 1, "9fa707def98dad22"): _traffic(
+    ("qwen128k", 28, "49e6a09708c8ed70"): _traffic(
+        stats_kernel=(1852810.13, 8064.0),
+        colsum_kernel=(1947924.52, 57591.34)),
+    ("ragged8", 32, "49e6a09708c8ed70"): _traffic(
+        stats_kernel=(2673221.4, 22016.0),
+        colsum_kernel=(2843534.85, 82244.47)),
+    ("tiny", 1, "49e6a09708c8ed70"): _traffic(
         stats_kernel=(299.29, 16.5),
         colsum_kernel=(332.0, 8.42)),
 }
@@ -79,18 +79,18 @@ def _mfma(**kernels):
 
 
 MEASURED_MFMA = {
-    ("llama32", 32, "9fa707def98dad22"): _mfma(
-        fused_kernel=(581683200.0, 290841600.0, 14856150.38)),
-    ("paper", 32, "9fa707def98dad22"): _mfma(
-        fused_kernel=(70909952.0, 35454976.0, 6614069.15)),
-    ("llama1", 1, "9fa707def98dad22"): _mfma(
-        fused_kernel=(17727488.0, 8863744.0, 785684.21)),
-    ("qwen128k", 28, "9fa707def98dad22"): _mfma(
-        stats_kernel=(939524096.0, 469762048.0, 10954679.91),
-        colsum_kernel=(987693056.0, 493846528.0, 14595586.76)),
-    ("ragged8", 32, "9fa707def98dad22"): _mfma(
-        stats_kernel=(738197504.0, 369098752.0, 19628507.47),
-        colsum_kernel=(731906048.0, 365953024.0, 22858043.59)),
+    ("llama32", 32, "49e6a09708c8ed70"): _mfma(
+        fused_kernel=(581683200.0, 290841600.0, 14881396.56)),
+    ("paper", 32, "49e6a09708c8ed70"): _mfma(
+        fused_kernel=(70909952.0, 35454976.0, 6603600.29)),
+    ("llama1", 1, "49e6a09708c8ed70"): _mfma(
+        fused_kernel=(17727488.0, 8863744.0, 788046.79)),
+    ("qwen128k", 28, "49e6a09708c8ed70"): _mfma(
+        stats_kernel=(939524096.0, 469762048.0, 10826419.91),
+        colsum_kernel=(987693056.0, 493846528.0, 14448879.15)),
+    ("ragged8", 32, "49e6a09708c8ed70"): _mfma(
+        stats_kernel=(738197504.0, 369098752.0, 19568391.18),
+        colsum_kernel=(731906048.0, 365953024.0, 22791053.53)),
 }
 
 

@@ -4,7 +4,8 @@
 //
 // The window softmax (section 3.3, SnapKV-style window of section 4) needs each
 // window row's statistics over the whole sequence before any column can be
-// normalised, so scoring runs in two kernels over K:
+// normalised, so scoring makes two passes over K, either as two kernels or as
+// the two roles of one kernel (fused_kernel, below):
 //
 //   stats_kernel   S1+S2: per (sequence, KV group, key chunk) it computes the
 //                  logits of all SRH window rows against the chunk's keys on
@@ -385,23 +386,26 @@ __global__ __launch_bounds__(64 * kWaves) void colsum_kernel(const ScoreArgs a) 
 }
 
 // ---------------------------------------------------------------------------
-// Both passes in one launch (fused_kernel).  The (sequence, group) pairs of
-// the launch ("segments") each get kFusedMembers workgroups: member m first
-// computes the statistics partials of a run of consecutive chunk1 chunks and
-// publishes them (agent-scope stores, each partial marked), then, for a run
-// of chunk2 = kFusedChunk2 chunks, waits until every partial of its segment
-// has arrived and computes the column sums, pooling and histogram exactly as
-// colsum_kernel does.  The normalisers, and so the scores, are bit for bit
-// those of the two-launch form.  While a segment's members wait or work on
-// their column sums, the workgroups of the next segment on the same CUs
-// stream their statistics, so the launch has no drain between the passes.
-// The members of a segment are consecutive workgroups of one XCD (launch
-// order goes round the 8 XCDs), so a segment's members start together; that
-// matters for speed only.  A member whose partials have not all arrived
-// after `fused_spin` polls records itself and returns: fused_catchup_kernel
-// (next on the stream, when every partial is written) does its column sums
-// with the same code.  Key runs are kFusedChunk2 = 1120 (+ 32 halo keys =
-// 9 x 128) so that 32 members cover a 32768-key sequence's column sums.
+// Both passes in one launch (fused_kernel).  Each (sequence, group) pair of
+// the launch (a "segment") gets kFusedMembers statistics workgroups and as
+// many column-sum workgroups.  Statistics member m computes the partials of
+// a run of consecutive chunk1 chunks and publishes each with one agent-scope
+// store whose sign bit is the arrival mark.  Column-sum member m waits until
+// every partial of its segment has arrived, merges them in merge_row_bias's
+// order and computes the column sums, pooling and histogram of a run of
+// chunk2 = kFusedChunk2 chunks exactly as colsum_kernel does, so the
+// normalisers, and the scores, are bit for bit those of the two-launch form.
+// The grid interleaves the roles per XCD (fused_role): a segment's column
+// sums start one block of statistics after its own, and while they run the
+// next segment's statistics stream on the same CUs, so the launch has no
+// drain between the passes.  A segment's workgroups are consecutive
+// workgroups of one XCD (launch order goes round the 8 XCDs); that matters
+// for speed only.  A column-sum workgroup whose partials have not all arrived
+// after `fused_spin` polls records itself and returns without writing:
+// fused_catchup_kernel (next on the stream, when every partial is written)
+// does its column sums with the same code.  Key runs are kFusedChunk2 = 1120
+// (+ 32 halo keys = 9 x 128) so that 32 members cover a 32768-key sequence's
+// column sums.
 // ---------------------------------------------------------------------------
 constexpr int kFusedChunk2 = 1120;
 constexpr int kFusedCsw = kFusedChunk2 + 32;
