@@ -331,3 +331,37 @@ def test_forced_single_pass_where_it_does_not_apply(L, name, fields, mask_heads)
         st = getattr(c, call)(L)
         assert st == C.UNSUPPORTED, (call, st, L.compresskv_last_error())
         assert "single-pass" in L.compresskv_last_error().decode()
+
+
+# (lengths, window, SRHs per group, dtype) -> path of CKV_SCORE_AUTO, _TWO_PASS,
+# _TWO_LAUNCHES (1 single pass, 2 two launches, 3 one launch).  Statistics
+# chunks are 512 keys up to 8k-key sequences of 8 groups and 1024 at 32k; the
+# library's own choice takes one launch for bf16, at most 6 row tiles
+# (ceil(W/16) x SRHs) and at least 16 chunks in every sequence.
+PATH_CASES = [
+    ("32k, 2 row tiles", (32768,), 32, 1, C.BF16, (3, 3, 2)),
+    ("8192 keys: 16 chunks of 512", (8192,), 32, 1, C.BF16, (3, 3, 2)),
+    ("8000 keys: under 16 chunks", (8000,), 32, 1, C.BF16, (2, 3, 2)),
+    ("ragged 4k and 16k", (4096, 16384), 32, 1, C.BF16, (2, 3, 2)),
+    ("6 row tiles", (32768,), 48, 2, C.BF16, (3, 3, 2)),
+    ("8 row tiles", (32768,), 64, 2, C.BF16, (2, 3, 2)),
+    ("12 row tiles", (32768,), 64, 3, C.BF16, (2, 2, 2)),
+    ("fp32", (32768,), 32, 1, C.F32, (2, 2, 2)),
+]
+
+
+@pytest.mark.parametrize("name,lens,W,n_srh,dtype,expect", PATH_CASES,
+                         ids=[c[0] for c in PATH_CASES])
+def test_scoring_path_choice_on_the_host(L, name, lens, W, n_srh, dtype, expect):
+    """compresskv_scoring_path needs no GPU for the two-pass forms; each
+    scoring field gets the form the header documents."""
+    L.compresskv_scoring_path.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    L.compresskv_scoring_path.restype = ctypes.c_int
+    c = Case(lens=lens, Hq=32, Hkv=8, W=W, dtype=dtype)
+    c.mask[:] = 0
+    for g in range(8):
+        c.mask[4 * g:4 * g + n_srh] = 1
+    for scoring, want in zip((C.SCORE_AUTO, C.SCORE_TWO_PASS, C.SCORE_TWO_LAUNCHES), expect):
+        _mutate(c, scoring=scoring)
+        got = L.compresskv_scoring_path(ctypes.byref(c.p), c.mask.ctypes.data)
+        assert got == want, (name, scoring, got, L.compresskv_last_error())
