@@ -113,3 +113,29 @@ def test_multi_layer_one_launch_matches_two_launches(gpu):
         torch.cuda.synchronize()
         for part in range(4):
             assert torch.equal(one[part], ref[part][l]), (l, part)
+
+
+def test_full_stack_repeated_calls_match_two_launches(gpu):
+    """The benchmark's 32-layer stack (L = 32768, inputs drawn on the device):
+    ten one-launch calls in a row, each bit for bit equal to the two-launch
+    call, so no call's result depends on how its exchange was timed."""
+    w = wl.get("llama32")
+    layers = [wl.make_layer_device(w, l, 0, gpu) for l in range(w.n_layers)]
+    q = [d["q_win"] for d in layers]
+    k = [d["k"] for d in layers]
+    masks = np.stack([d["srh_mask"] for d in layers])
+    cu, cu_host = layers[0]["cu_seqlens"], layers[0]["cu_seqlens_host"]
+    probs = {s: C.Problem(q[0], k[0], layers[0]["v"], cu, cu_seqlens_host=cu_host,
+                          pool_kernel=w.pool_kernel, pool_type=w.pool_type, scoring=s)
+             for s in (C.SCORE_AUTO, C.SCORE_TWO_LAUNCHES)}
+    assert C.compresskv_scoring_path(probs[C.SCORE_AUTO], masks[0]) == 3
+    ref = C.score_layers(probs[C.SCORE_TWO_LAUNCHES], q, k, masks)
+    p = probs[C.SCORE_AUTO]
+    ws = C.layers_workspace(p, masks, gpu)
+    out = torch.empty_like(ref)
+    for call in range(10):
+        out.fill_(float("nan"))
+        C.compresskv_score_layers(p, q, k, masks, out, ws, torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref), f"call {call} differs from the two launches"
+    _say("  10 calls equal")
