@@ -432,6 +432,8 @@ ckv::ScoreArgs score_args(const ckv_problem *p, const Plan &pl, void *ws) {
   a.head_end_mask = pl.head_end_mask;
   a.fused_skip =
       pl.fused ? reinterpret_cast<int *>(static_cast<char *>(ws) + pl.fskip_off) : nullptr;
+  a.fused_arrive = reinterpret_cast<int *>(static_cast<char *>(ws) + pl.arrive_off);
+  a.fused_bias = reinterpret_cast<float2 *>(static_cast<char *>(ws) + pl.bias_off);
   a.fused_spin = p->spin_limit == CKV_SPIN_CATCHUP_ALL ? -1
                  : p->spin_limit < 0                 ? kDefaultFusedSpin
                                                      : p->spin_limit;
@@ -676,6 +678,9 @@ hipError_t launch_twopass_table(const ckv_problem *p, const Plan &pl, const ckv:
   b.layers = a.layers + pl.n_op;
   b.stats = a.stats + pl.n_op * a.stats_layer;
   b.hist = a.hist + pl.n_op * a.hist_layer;
+  const int64_t groups = (int64_t)p->batch * p->n_kv_heads;
+  b.fused_arrive = a.fused_arrive + pl.n_op * groups;
+  b.fused_bias = a.fused_bias + pl.n_op * groups * a.row_slots;
   return ckv::launch_score_layers(b, p->dtype == CKV_BF16, p->head_dim, pl.tp_rt_max, p->batch,
                                   n_tp, stream);
 }

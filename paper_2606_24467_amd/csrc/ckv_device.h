@@ -159,8 +159,10 @@ struct ScoreArgs {
   uint32_t head_end_mask;  // bit rt set if row tile rt is the last tile of an SRH
   // Both passes in one launch (score_kernels.h, fused_kernel); null: two launches.
   int *fused_skip;         // [0]: entries, then the workgroups left to the catch-up kernel
-  int32_t fused_spin;      // polls of a group's partials before a workgroup leaves its column
-                           // sums to the catch-up kernel (< 0: all of them)
+  int32_t fused_spin;      // polls of a group's normalisers before a workgroup leaves its
+                           // column sums to the catch-up kernel (< 0: all of them)
+  int *fused_arrive;       // [segments] statistics workgroups of a segment that have published
+  float2 *fused_bias;      // [segments][row_slots] (normaliser, -1) once published
 };
 
 // Workgroups per (sequence, group) and pass of the fused two-pass launch, and

@@ -367,6 +367,28 @@ __device__ __forceinline__ bool merge_row_bias_marked(const ScoreArgs &a, const 
   return true;
 }
 
+// Row normalisers that another workgroup of the same launch merged and
+// published (rows_cap entries (bias, -1): the set sign bit marks them
+// written, the slots start at +0), read at agent scope into bias_s; the reads
+// are repeated at most `spin` more times; false (uniformly) if one never
+// arrived.
+template <int NT>
+__device__ __forceinline__ bool read_bias_marked(const float2 *bias_g, int rows_cap,
+                                                 float *bias_s, int spin) {
+  const int tid = threadIdx.x;
+  for (int attempt = 0;; ++attempt) {
+    bool mine = true;
+    for (int r = tid; r < rows_cap; r += NT) {
+      const float2 v = load_partial_coherent(bias_g + r);
+      mine = mine && signbit(v.y);
+      bias_s[r] = v.x;
+    }
+    if (__syncthreads_and(mine)) return true;
+    if (attempt >= spin) return false;
+    __builtin_amdgcn_s_sleep(4);
+  }
+}
+
 // Window sums of one key tile for every SRH of the group (MFMA operands: A =
 // window rows, B = keys; lane (quad, c) holds rows 4*quad .. 4*quad+3 against
 // key c): in-lane over the 4 rows and the SRH's row tiles, then across the

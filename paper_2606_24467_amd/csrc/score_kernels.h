@@ -242,13 +242,15 @@ __attribute__((amdgpu_waves_per_eu(kStatsMinWaves<T, D, RTM>))) void stats_kerne
 // waves per SIMD); four slots measured slower (268 VGPRs, one wave).
 constexpr int kRingCs = 2;
 
-// FUSED: the partials come from the workgroups of the same launch (marked,
-// polled at most `spin` more times); returns false, with nothing written, if
-// one has not arrived.
+// FUSED: the row normalisers come from the same launch: published by the
+// group's last statistics workgroup at bias_g (or, with bias_g null, merged
+// here from the marked partials), polled at most `spin` more times; returns
+// false, with nothing written, if they have not arrived.
 template <typename T, int D, int RT, int CSW, bool SB, bool FUSED = false>
 __device__ __forceinline__ bool colsum_body(const ScoreArgs &a, const Work &w, uint4 *q_lds,
                                             float *bias_s, float (*cs)[CSW], float *stage,
-                                            int *hist_s, int spin = 0) {
+                                            int *hist_s, int spin = 0,
+                                            const float2 *bias_g = nullptr) {
   constexpr int NS = Slices<T, D>::n, RQ = RegTiles<T, D, RT>::v;
   constexpr int NT = 64 * kWaves;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -282,8 +284,9 @@ __device__ __forceinline__ bool colsum_body(const ScoreArgs &a, const Work &w, u
       a.stats + w.layer * a.stats_layer + ((int64_t)w.b * a.Hkv + g) * a.parts_stride * a.row_slots;
   const int n_parts = (L + a.chunk1 - 1) / a.chunk1;
   if constexpr (FUSED) {
-    if (!merge_row_bias_marked<NT>(a, parts, a.row_slots, n_parts, w.rt_n * 16, RT * 16, bias_s,
-                                   spin))
+    if (bias_g != nullptr ? !read_bias_marked<NT>(bias_g, RT * 16, bias_s, spin)
+                          : !merge_row_bias_marked<NT>(a, parts, a.row_slots, n_parts,
+                                                       w.rt_n * 16, RT * 16, bias_s, spin))
       return false;
   } else {
     merge_row_bias<NT>(a, parts, a.row_slots, n_parts, w.rt_n * 16, RT * 16, bias_s);
@@ -390,22 +393,24 @@ __global__ __launch_bounds__(64 * kWaves) void colsum_kernel(const ScoreArgs a) 
 // the launch (a "segment") gets kFusedMembers statistics workgroups and as
 // many column-sum workgroups.  Statistics member m computes the partials of
 // a run of consecutive chunk1 chunks and publishes each with one agent-scope
-// store whose sign bit is the arrival mark.  Column-sum member m waits until
-// every partial of its segment has arrived, merges them in merge_row_bias's
-// order and computes the column sums, pooling and histogram of a run of
-// chunk2 = kFusedChunk2 chunks exactly as colsum_kernel does, so the
-// normalisers, and the scores, are bit for bit those of the two-launch form.
+// store whose sign bit is the arrival mark, then counts itself in the
+// segment's arrival counter; the last to arrive merges the partials in
+// merge_row_bias's order and publishes the row normalisers (marked the same
+// way).  Column-sum member m waits for those and computes the column sums,
+// pooling and histogram of a run of chunk2 = kFusedChunk2 chunks exactly as
+// colsum_kernel does, so the normalisers, and the scores, are bit for bit
+// those of the two-launch form.
 // The grid interleaves the roles per XCD (fused_role): a segment's column
 // sums start one block of statistics after its own, and while they run the
 // next segment's statistics stream on the same CUs, so the launch has no
 // drain between the passes.  A segment's workgroups are consecutive
 // workgroups of one XCD (launch order goes round the 8 XCDs); that matters
-// for speed only.  A column-sum workgroup whose partials have not all arrived
+// for speed only.  A column-sum workgroup whose normalisers have not arrived
 // after `fused_spin` polls records itself and returns without writing:
 // fused_catchup_kernel (next on the stream, when every partial is written)
-// does its column sums with the same code.  Key runs are kFusedChunk2 = 1120
-// (+ 32 halo keys = 9 x 128) so that 32 members cover a 32768-key sequence's
-// column sums.
+// merges the partials itself and does its column sums with the same code.
+// Key runs are kFusedChunk2 = 1120 (+ 32 halo keys = 9 x 128) so that 32
+// members cover a 32768-key sequence's column sums.
 // ---------------------------------------------------------------------------
 constexpr int kFusedChunk2 = 1120;
 constexpr int kFusedCsw = kFusedChunk2 + 32;
@@ -499,15 +504,21 @@ __device__ __forceinline__ FusedRole fused_role(int bid, int n_seg) {
 static __global__ __launch_bounds__(256) void fused_fill_kernel(int *stats, int64_t n_groups,
                                                                 int64_t group_stride,
                                                                 int64_t group_ints, int *hist,
-                                                                int64_t hist_ints, int *skip) {
-  const int64_t n0 = n_groups * group_ints;
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n0 + hist_ints;
+                                                                int64_t hist_ints, int *bias,
+                                                                int64_t bias_ints, int *arrive,
+                                                                int *skip) {
+  const int64_t n0 = n_groups * group_ints, n1 = n0 + hist_ints, n2 = n1 + bias_ints;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n2 + n_groups;
        i += (int64_t)gridDim.x * 256) {
     if (i < n0) {
       const int64_t g = i / group_ints;
       stats[g * group_stride + (i - g * group_ints)] = 0;
-    } else {
+    } else if (i < n1) {
       hist[i - n0] = 0;
+    } else if (i < n2) {
+      bias[i - n1] = 0;
+    } else {
+      arrive[i - n2] = 0;
     }
   }
   if (blockIdx.x == 0 && threadIdx.x == 0) skip[0] = 0;
@@ -515,7 +526,7 @@ static __global__ __launch_bounds__(256) void fused_fill_kernel(int *stats, int6
 
 // Member `member`'s statistics chunks of segment w: published partials.
 template <typename T, int D, int RTM>
-__device__ __forceinline__ void fused_stats(const ScoreArgs &a, const Work &w, int member,
+__device__ __forceinline__ void fused_stats(const ScoreArgs &a, const Work &w, int u, int member,
                                             FusedLds<T, D, RTM> &sm) {
   const int n1 = (w.L + a.chunk1 - 1) / a.chunk1;
   const int c1n = (n1 + kFusedMembers - 1) / kFusedMembers;
@@ -526,6 +537,26 @@ __device__ __forceinline__ void fused_stats(const ScoreArgs &a, const Work &w, i
   ws.n_chunks = min(c1n, n1 - j1);
   dispatch_rt<RTM>(w.rt_n, [&]<int RT>() {
     stats_body<T, D, RT, kSliceBarrier<RTM>, true>(a, ws, sm.q, sm.part);
+    // every partial store of this workgroup is issued (stats_body ends with a
+    // barrier); the last of the segment's statistics workgroups to arrive
+    // merges all partials (reading each mark) and publishes the normalisers
+    __shared__ int last_s;
+    if (threadIdx.x == 0)
+      last_s = __hip_atomic_fetch_add(&a.fused_arrive[u], 1, __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_AGENT) ==
+               (n1 + c1n - 1) / c1n - 1;
+    __syncthreads();
+    if (last_s) {
+      const float2 *parts = a.stats + w.layer * a.stats_layer +
+                            ((int64_t)w.b * a.Hkv + w.g) * a.parts_stride * a.row_slots;
+      if (merge_row_bias_marked<256>(a, parts, a.row_slots, n1, w.rt_n * 16, RT * 16, sm.c.bias,
+                                     1 << 16)) {
+        __syncthreads();
+        for (int r = threadIdx.x; r < RT * 16; r += 256)
+          store_partial_coherent(a.fused_bias + (int64_t)u * a.row_slots + r,
+                                 make_float2(sm.c.bias[r], -1.f));
+      }
+    }
   });
   __syncthreads();   // sm is reused by the next phase
 }
@@ -534,7 +565,8 @@ __device__ __forceinline__ void fused_stats(const ScoreArgs &a, const Work &w, i
 // not arrived after `spin` more polls (nothing written then).
 template <typename T, int D, int RTM>
 __device__ __forceinline__ bool fused_colsum(const ScoreArgs &a, const Work &w, int member,
-                                             FusedLds<T, D, RTM> &sm, int spin) {
+                                             FusedLds<T, D, RTM> &sm, int spin,
+                                             const float2 *bias_g) {
   const int n2 = w.P > 0 ? (w.P + a.chunk2 - 1) / a.chunk2 : 0;
   const int c2n = (n2 + kFusedMembers - 1) / kFusedMembers;
   const int j2 = member * c2n;
@@ -546,7 +578,7 @@ __device__ __forceinline__ bool fused_colsum(const ScoreArgs &a, const Work &w, 
   dispatch_rt<RTM>(w.rt_n, [&]<int RT>() {
     ok = colsum_body<T, D, RT, kFusedCsw, kSliceBarrier<RTM>, true>(
         a, wc, sm.q, sm.c.bias, sm.c.cs, kFusedStage<T, D, RTM> ? sm.c.stage : nullptr, sm.c.hist,
-        spin);
+        spin, bias_g);
   });
   __syncthreads();
   return ok;
@@ -566,11 +598,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void f
       const gptr<float> out = w.lv.scores + (int64_t)w.g * a.T + w.s0;
       for (int j = max(w.P, 0) + (int)threadIdx.x; j < w.L; j += 256) out[j] = INFINITY;
     }
-    fused_stats<T, D, RTM>(a, w, r.member, sm);
+    fused_stats<T, D, RTM>(a, w, r.u, r.member, sm);
     return;
   }
   const bool done =
-      a.fused_spin >= 0 && fused_colsum<T, D, RTM>(a, w, r.member, sm, a.fused_spin);
+      a.fused_spin >= 0 && fused_colsum<T, D, RTM>(a, w, r.member, sm, a.fused_spin,
+                                                   a.fused_bias + (int64_t)r.u * a.row_slots);
   if (!done && threadIdx.x == 0)
     a.fused_skip[1 + atomicAdd(&a.fused_skip[0], 1)] = r.u * kFusedMembers + r.member;
 }
@@ -585,7 +618,7 @@ __global__ __launch_bounds__(256) void fused_catchup_kernel(const ScoreArgs a) {
     const int e = a.fused_skip[1 + i];
     Work w;
     fused_work<ML>(a, e / kFusedMembers, w);
-    fused_colsum<T, D, RTM>(a, w, e % kFusedMembers, sm, 0);
+    fused_colsum<T, D, RTM>(a, w, e % kFusedMembers, sm, 0, nullptr);
   }
 }
 
@@ -603,10 +636,12 @@ static hipError_t launch_score_t(const ScoreArgs &args, int nz, hipStream_t stre
       const int64_t nb = fused_blocks(a.Hkv, nz);
       if (nb > INT32_MAX) return hipErrorInvalidConfiguration;
       const int64_t slots = (int64_t)a.parts_stride * a.row_slots * 2;   // ints per group
+      const int64_t n_groups = (int64_t)n_layers * a.batch * a.Hkv;
       hipLaunchKernelGGL(fused_fill_kernel, dim3(1024), dim3(256), 0, stream,
-                         reinterpret_cast<int *>(a.stats), (int64_t)n_layers * a.batch * a.Hkv,
-                         slots, (int64_t)a.max_chunks1 * a.row_slots * 2, a.hist,
-                         (int64_t)a.hist_layer * n_layers, a.fused_skip);
+                         reinterpret_cast<int *>(a.stats), n_groups, slots,
+                         (int64_t)a.max_chunks1 * a.row_slots * 2, a.hist,
+                         (int64_t)a.hist_layer * n_layers, reinterpret_cast<int *>(a.fused_bias),
+                         n_groups * a.row_slots * 2, a.fused_arrive, a.fused_skip);
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
       hipLaunchKernelGGL((fused_kernel<T, D, RTM, ML>), dim3((unsigned)nb), dim3(256), 0, stream,
