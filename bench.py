@@ -46,27 +46,27 @@ def _traffic(**kernels):
 
 
 MEASURED_TRAFFIC = {
-    ("llama32", 32, "49e6a09708c8ed70"): _traffic(
-        fused_fill_kernel=(10.56, 8192.03),
-        fused_kernel=(2286543.97, 37605.53),
+    ("llama32", 32, "7841ac17a7c91f99"): _traffic(
+        fused_fill_kernel=(11.08, 8385.03),
+        fused_kernel=(2286926.98, 37992.78),
+        fused_catchup_kernel=(11.5, 0.0)),
+    ("paper", 32, "7841ac17a7c91f99"): _traffic(
+        fused_fill_kernel=(11.03, 4161.03),
+        fused_kernel=(959948.02, 15118.56),
+        fused_catchup_kernel=(10.5, 0.0)),
+    ("llama1", 1, "7841ac17a7c91f99"): _traffic(
+        fused_fill_kernel=(11.02, 196.06),
+        fused_kernel=(63429.77, 1184.08),
         fused_catchup_kernel=(18.0, 0.0)),
-    ("paper", 32, "49e6a09708c8ed70"): _traffic(
-        fused_fill_kernel=(10.53, 4096.03),
-        fused_kernel=(959031.04, 14993.56),
-        fused_catchup_kernel=(18.0, 0.0)),
-    ("llama1", 1, "49e6a09708c8ed70"): _traffic(
-        fused_fill_kernel=(10.51, 192.03),
-        fused_kernel=(64009.9, 1172.08),
-        fused_catchup_kernel=(18.0, 0.0)),
-    ("qwen128k", 28, "49e6a09708c8ed70"): _traffic(
-        stats_kernel=(1852810.13, 8064.0),
-        colsum_kernel=(1947924.52, 57591.34)),
-    ("ragged8", 32, "49e6a09708c8ed70"): _traffic(
-        stats_kernel=(2673221.4, 22016.0),
-        colsum_kernel=(2843534.85, 82244.47)),
-    ("tiny", 1, "49e6a09708c8ed70"): _traffic(
-        stats_kernel=(299.29, 16.5),
-        colsum_kernel=(332.0, 8.42)),
+    ("qwen128k", 28, "7841ac17a7c91f99"): _traffic(
+        stats_kernel=(1852807.34, 8064.0),
+        colsum_kernel=(1947790.38, 57591.34)),
+    ("ragged8", 32, "7841ac17a7c91f99"): _traffic(
+        stats_kernel=(2673227.1, 22016.0),
+        colsum_kernel=(2843546.18, 82244.65)),
+    ("tiny", 1, "7841ac17a7c91f99"): _traffic(
+        stats_kernel=(297.42, 16.5),
+        colsum_kernel=(334.25, 8.42)),
 }
 
 # MFMA work the score phase executes, from rocprofv3 on the same sources:
@@ -79,18 +79,18 @@ def _mfma(**kernels):
 
 
 MEASURED_MFMA = {
-    ("llama32", 32, "49e6a09708c8ed70"): _mfma(
-        fused_kernel=(581683200.0, 290841600.0, 14881396.56)),
-    ("paper", 32, "49e6a09708c8ed70"): _mfma(
-        fused_kernel=(70909952.0, 35454976.0, 6603600.29)),
-    ("llama1", 1, "49e6a09708c8ed70"): _mfma(
-        fused_kernel=(17727488.0, 8863744.0, 788046.79)),
-    ("qwen128k", 28, "49e6a09708c8ed70"): _mfma(
-        stats_kernel=(939524096.0, 469762048.0, 10826419.91),
-        colsum_kernel=(987693056.0, 493846528.0, 14448879.15)),
-    ("ragged8", 32, "49e6a09708c8ed70"): _mfma(
-        stats_kernel=(738197504.0, 369098752.0, 19568391.18),
-        colsum_kernel=(731906048.0, 365953024.0, 22791053.53)),
+    ("llama32", 32, "7841ac17a7c91f99"): _mfma(
+        fused_kernel=(581683200.0, 290841600.0, 14426235.76)),
+    ("paper", 32, "7841ac17a7c91f99"): _mfma(
+        fused_kernel=(70909952.0, 35454976.0, 6495632.76)),
+    ("llama1", 1, "7841ac17a7c91f99"): _mfma(
+        fused_kernel=(17727488.0, 8863744.0, 809361.74)),
+    ("qwen128k", 28, "7841ac17a7c91f99"): _mfma(
+        stats_kernel=(939524096.0, 469762048.0, 10580562.24),
+        colsum_kernel=(987693056.0, 493846528.0, 14332006.91)),
+    ("ragged8", 32, "7841ac17a7c91f99"): _mfma(
+        stats_kernel=(738197504.0, 369098752.0, 19578183.35),
+        colsum_kernel=(731906048.0, 365953024.0, 22845427.38)),
 }
 
 
