@@ -5,7 +5,7 @@
 //
 //   dec_attn_kernel     split-K attention of every (sequence, group, cache):
 //                       the group's rows (decoding step x query head of the
-//                       group) against one 256-key chunk, QK^T on MFMA, online
+//                       group) against one 512-key chunk, QK^T on MFMA, online
 //                       softmax in LDS, P.V on fp32 MFMA; partial (max, sum, O)
 //   dec_combine_kernel  merges the chunks of every row into A (fp32)
 //   dec_proj_kernel     y = W_O x for x = A_full and A_full - A_comp on fp32
@@ -29,7 +29,7 @@
 
 namespace ckv {
 
-constexpr int kDecChunk = 256;   // keys per attention workgroup
+constexpr int kDecChunk = 512;   // keys per attention workgroup (eight softmax steps)
 constexpr int kDecSub = 64;      // keys per softmax step inside it (one tile per wave)
 constexpr int kProjRows = 16;    // W_O rows per projection workgroup
 constexpr int kMaxDecRows = 64;  // decoding steps x query heads per group, per block
