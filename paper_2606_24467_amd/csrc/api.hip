@@ -51,7 +51,7 @@ struct Plan {
          hist_off = 0, stats_off = 0, skip_off = 0, edges_off = 0, total = 0;
   int64_t stats_layer = 0, hist_layer = 0;   // elements per layer
   int sel_slices = 0;      // slices of the split selection (0: one workgroup per selection)
-  size_t sel_meta_off = 0, sel_cand_off = 0;
+  size_t sel_meta_off = 0, sel_cand_off = 0, sel_ord_off = 0;
   int max_parts = 0;       // partial-statistics slots per group in the workspace
   // single-pass scoring
   bool op_shape = false;   // the problem's shape allows it (its workspace is reserved)
@@ -362,9 +362,10 @@ void set_layout(const ckv_problem *p, Plan &pl) {
     const int ns = (pmax + ckv::kSelSlice - 1) / ckv::kSelSlice;
     pl.sel_slices = ns;
     pl.sel_meta_off = round_up(pl.total, 256);
-    pl.sel_cand_off =
-        pl.sel_meta_off + round_up(lg * (ckv::kSelMetaHead + 4 * (size_t)ns) * sizeof(int), 256);
-    pl.total = pl.sel_cand_off + round_up(lg * ns * (size_t)ckv::kSelSliceCap * 4, 256);
+    pl.sel_cand_off = pl.sel_meta_off +
+                      round_up(lg * ns * (size_t)ckv::kSelMetaPerSlice * sizeof(int), 256);
+    pl.sel_ord_off = pl.sel_cand_off + round_up(lg * ns * (size_t)ckv::kSelSliceCap * 4, 256);
+    pl.total = pl.sel_ord_off + round_up(lg * ns * (size_t)ckv::kSelSliceCap * 8, 256);
   }
 }
 
@@ -505,6 +506,7 @@ ckv::SelectArgs select_args(const ckv_problem *p, const Plan &pl, const int *his
   if (pl.sel_slices > 0 && s.hist && ws) {
     s.sel_meta = reinterpret_cast<int *>(static_cast<char *>(ws) + pl.sel_meta_off);
     s.sel_cand = reinterpret_cast<uint32_t *>(static_cast<char *>(ws) + pl.sel_cand_off);
+    s.sel_ord = reinterpret_cast<uint64_t *>(static_cast<char *>(ws) + pl.sel_ord_off);
     s.n_slices = pl.sel_slices;
     s.cand_cap = ckv::kSelSliceCap;
   }

@@ -221,17 +221,22 @@ struct SelectArgs {
   int32_t out_groups;      // idx rows each selection writes: 1, or Hkv (layer-shared set)
   GroupBudgets gb;         // per-group budgets (single-layer calls), if gb.on
   // Split selection (sequences longer than one slice; needs hist): per
-  // selection kSelMetaHead + 4 * n_slices meta words and n_slices lists of
-  // cand_cap candidates; NULL sel_meta selects one workgroup per selection.
+  // selection kSelMetaPerSlice * n_slices meta words, n_slices lists of
+  // cand_cap candidate scores and n_slices lists of cand_cap (position,
+  // score) pairs; NULL sel_meta selects one workgroup per selection.
   int *sel_meta;
   uint32_t *sel_cand;
+  uint64_t *sel_ord;   // (score bits << 32) | position, bit 31 marking a candidate
   int32_t n_slices, cand_cap;
 };
 
 constexpr int kSelSlice = 32768;       // positions per slice of the split selection
 constexpr int kMaxSelSlices = 64;      // longest prefix it takes: 64 slices
-constexpr int kSelSliceCap = kSelSlice;   // candidates kept per slice: all its positions
-constexpr int kSelMetaHead = 4;
+constexpr int kSelSliceCap = kSelSlice;   // list entries kept per slice: all its positions
+// Meta words per slice of a split selection: candidates, the 16 waves' list
+// lengths, the slice's first kept-list position, ties in the slices before,
+// the threshold and the ties kept.
+constexpr int kSelMetaPerSlice = 21;
 
 // Layer-shared index set: the layer score from the per-group scores.
 struct CombineArgs {

@@ -370,23 +370,23 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a)
 }
 
 // Long sequences: the selection split over its rounds ("slices" of kRound
-// positions), in four launches with the same result as select_kernel.
-//  scan:    per slice, the count of elements above the first-digit bucket
-//           and the bucket's elements (its candidates) into the slice's list;
+// positions), in three launches with the same result as select_kernel.
+//  scan:    per slice, the elements of the first-digit bucket (its
+//           candidates) into the slice's candidate list, and every element
+//           at or above the bucket, as a (position, score) pair, into the
+//           wave's part of the slice's ordered list (ascending positions);
 //  resolve: per selection, digits 2 and 3 over all the slices' candidates,
-//           then each slice's first kept-list position and tie rank;
-//  write:   per slice, the ordered compaction from those offsets;
-//  rest:    the slices whose compaction did not fit the write kernel's LDS.
-// Meta words of a selection: [0] nothing left to select, [1] threshold, [2] ties kept, then
-// per slice: elements above the bucket, candidates, first kept position,
-// ties before it.
-__device__ __forceinline__ int *sel_meta(const SelectArgs &a, const Sel &s) {
-  return a.sel_meta + s.id * (kSelMetaHead + 4 * a.n_slices);
-}
+//           then each slice's first kept-list position and ties before it;
+//  write:   per slice, the ordered compaction of its ordered list.
+static_assert(kSelMetaPerSlice == 1 + kSelThreads / 64 + 4, "meta words of a slice");
+constexpr int kMetaFirst = 1 + kSelThreads / 64;   // first kept-list position
+constexpr int kMetaTies = kMetaFirst + 1;           // ties in the slices before
+constexpr int kMetaThr = kMetaFirst + 2;            // threshold (score bits)
+constexpr int kMetaRemain = kMetaFirst + 3;         // ties kept in all
 
-// Positions a wave of the write kernel stages in LDS (kept or tied); more
-// send its slice to select_rest_kernel.
-constexpr int kScanWaveCap = 512;
+__device__ __forceinline__ int *sel_meta(const SelectArgs &a, const Sel &s) {
+  return a.sel_meta + s.id * (kSelMetaPerSlice * a.n_slices);
+}
 
 // Grid (n_slices, n_sel, batch [x layers]), 1024 threads.
 template <bool ML>
@@ -395,10 +395,10 @@ __global__ __launch_bounds__(kSelThreads) void select_scan_kernel(const SelectAr
   const int slice = blockIdx.x;
   const int r0 = slice * kRound;
   if (s.L <= s.budget || s.k == 0 || r0 >= s.P) return;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   __shared__ int hist[kHistBins];
   __shared__ int scan_tmp[kSelThreads / 64];
-  __shared__ int bucket_s, remain_s, ncand_s, above_s;
+  __shared__ int bucket_s, remain_s, ncand_s;
   uint32_t v[kEpt];
   load_round(s.sc, s.P, r0, v);
   const int *hg = a.hist + s.layer * a.hist_layer + ((int64_t)s.b * a.Hkv + s.g) * kHistBins;
@@ -407,50 +407,76 @@ __global__ __launch_bounds__(kSelThreads) void select_scan_kernel(const SelectAr
     bucket_s = 0;
     remain_s = 0;
     ncand_s = 0;
-    above_s = 0;
   }
   __syncthreads();
   find_bucket(hist, kHistBins, s.k, scan_tmp, &bucket_s, &remain_s);
   const int bucket = bucket_s;
-  // elements above the bucket (counted) and in it (appended to the slice's
-  // list in no particular order: the resolve kernel only counts them)
-  const gptr<uint32_t> cand =
-      to_global(a.sel_cand) + (s.id * a.n_slices + slice) * (int64_t)a.cand_cap;
-  int n_above = 0;
+  // The bucket's elements go to the candidate list in no particular order
+  // (the resolve kernel only counts them); the elements at or above it go to
+  // the wave's part of the ordered list (its 64 * kEpt positions, in (e,
+  // lane) order, i.e. ascending), bit 31 of the position marking a candidate.
+  const int64_t list = (s.id * a.n_slices + slice) * (int64_t)a.cand_cap;
+  const gptr<uint32_t> cand = to_global(a.sel_cand) + list;
+  const gptr<uint64_t> ord = to_global(a.sel_ord) + list + wave * (64 * kEpt);
+  // the wave's candidates are counted first, so that one LDS atomic
+  // reserves their slots
+  int n_cand = 0;
+#pragma unroll
+  for (int e = 0; e < kEpt; ++e)
+    n_cand += (int)__popcll(__ballot(elem_pos<kEpt>(r0, e) < s.P && hist_bin(v[e]) == bucket));
+  // (the scores are recomputed from below, not kept from the count)
+  int j0 = elem_pos<kEpt>(r0, 0);
+#pragma unroll
+  for (int e = 0; e < kEpt; ++e) asm volatile("" : "+v"(v[e]));
+  asm volatile("" : "+v"(j0));
+  int cand_at = 0;
+  if (lane == 0 && n_cand) cand_at = atomicAdd(&ncand_s, n_cand);
+  cand_at = __shfl(cand_at, 0);
+  int n_ord = 0;
 #pragma unroll
   for (int e = 0; e < kEpt; ++e) {
-    const bool ok = elem_pos<kEpt>(r0, e) < s.P;
+    const int j = j0 + 64 * e;   // elem_pos<kEpt>(r0, e)
+    const bool ok = j < s.P;
     const int bin = hist_bin(v[e]);
-    n_above += (int)__popcll(__ballot(ok && bin > bucket));
     const bool c = ok && bin == bucket;
-    const int at = wave_append(&ncand_s, c);
-    if (c && at < a.cand_cap) cand[at] = v[e];
+    const unsigned long long m_c = __ballot(c);
+    if (c && cand_at + lanes_below(m_c) < a.cand_cap) cand[cand_at + lanes_below(m_c)] = v[e];
+    cand_at += (int)__popcll(m_c);
+    const bool f = ok && bin >= bucket;
+    const unsigned long long m = __ballot(f);
+    if (f)
+      ord[n_ord + lanes_below(m)] = ((uint64_t)(v[e] & 0x7FFFFFFFu) << 32) |
+                                    (uint32_t)j | (c ? 0x80000000u : 0u);
+    n_ord += (int)__popcll(m);
+    __builtin_amdgcn_sched_barrier(0);   // one element's stores at a time
   }
-  if ((tid & 63) == 0) atomicAdd(&above_s, n_above);
+  int *meta = sel_meta(a, s) + slice * kSelMetaPerSlice;
+  if ((tid & 63) == 0) meta[1 + wave] = n_ord;
   __syncthreads();
-  if (tid == 0) {
-    int *meta = sel_meta(a, s);
-    meta[kSelMetaHead + slice] = above_s;
-    meta[kSelMetaHead + a.n_slices + slice] = ncand_s;
-  }
+  if (tid == 0) meta[0] = ncand_s;
 }
 
-// Candidates per thread per pass of the resolve kernel when they are read
-// from the slices' lists.
+// Candidates the resolve kernel keeps in LDS (32 KB), loaded kResolveEpt
+// per thread at a time; more are read from the slices' lists on every pass.
+constexpr int kResolveCandCap = 8192;
 constexpr int kResolveEpt = 8;
+
+struct ResolveLds {
+  int hist[kHistBins];
+  int scan_tmp[kSelThreads / 64];
+  int bucket, remain;
+  int cand_off[kMaxSelSlices + 1], above[kMaxSelSlices], gt[kMaxSelSlices], eq[kMaxSelSlices];
+  uint32_t cand_u[kResolveCandCap];
+};
 
 // Grid (n_sel, batch [x layers]), 1024 threads.
 template <bool ML>
 __global__ __launch_bounds__(kSelThreads) void select_resolve_kernel(const SelectArgs a) {
   const Sel s = sel_of<ML>(a, blockIdx.x, blockIdx.y);
   const int tid = threadIdx.x;
+  if (sel_trivial(a, s)) return;
   int *meta = sel_meta(a, s);
-  if (sel_trivial(a, s)) {
-    if (tid == 0) meta[0] = 1;
-    return;
-  }
-  __shared__ SelLds lds;
-  __shared__ int cand_off[kMaxSelSlices + 1], gt[kMaxSelSlices], eq[kMaxSelSlices];
+  __shared__ ResolveLds lds;
   const int ns = (s.P + kRound - 1) / kRound;
   const int nsl = a.n_slices;
   if (tid == 0) {
@@ -460,49 +486,58 @@ __global__ __launch_bounds__(kSelThreads) void select_resolve_kernel(const Selec
   const int *hg = a.hist + s.layer * a.hist_layer + ((int64_t)s.b * a.Hkv + s.g) * kHistBins;
   for (int i = tid; i < kHistBins; i += kSelThreads) lds.hist[i] = hg[i];
   if (tid < ns) {
-    gt[tid] = meta[kSelMetaHead + tid];
-    eq[tid] = 0;
-    cand_off[tid + 1] = meta[kSelMetaHead + nsl + tid];   // <= cand_cap: a slice's positions
+    const int *m = meta + tid * kSelMetaPerSlice;
+    int n_ord = 0;
+    for (int w = 0; w < kSelThreads / 64; ++w) n_ord += m[1 + w];
+    lds.cand_off[tid + 1] = m[0];          // <= cand_cap: a slice's positions
+    lds.above[tid] = n_ord - m[0];         // the list holds the candidates and those above
+    lds.gt[tid] = 0;
+    lds.eq[tid] = 0;
   }
   __syncthreads();
   if (tid == 0) {
-    cand_off[0] = 0;
-    for (int sl = 0; sl < ns; ++sl) cand_off[sl + 1] += cand_off[sl];
+    lds.cand_off[0] = 0;
+    for (int sl = 0; sl < ns; ++sl) lds.cand_off[sl + 1] += lds.cand_off[sl];
   }
   find_bucket(lds.hist, kHistBins, s.k, lds.scan_tmp, &lds.bucket, &lds.remain);
   uint32_t prefix = (uint32_t)lds.bucket << 20;
   int remain = lds.remain;
-  const int nc = cand_off[ns];
+  const int nc = lds.cand_off[ns];
   const gptr<const uint32_t> cand0 = to_global(a.sel_cand) + s.id * nsl * (int64_t)a.cand_cap;
-  // The candidates into LDS, slices in order (more than fit: read from the
-  // slices' lists on every pass, kResolveEpt per thread at a time).
-  const bool in_lds = nc <= kCandCap;
+  // Candidate i of the concatenation (slices in order) lies in slice sl
+  // (cand_off[sl] <= i < cand_off[sl + 1]).  Into LDS kResolveEpt per thread
+  // at a time: addresses first, then every load at once.
+  const bool in_lds = nc <= kResolveCandCap;
   if (in_lds) {
-    for (int sl = 0; sl < ns; ++sl) {
-      const int n = cand_off[sl + 1] - cand_off[sl];
-      const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-          (void *)(cand0 + sl * (int64_t)a.cand_cap), (short)0, n * 4, 0x00020000);
-      for (int base = 0; base < n; base += 4 * kSelThreads) {
-        uint32_t u[4];
+    int sl = 0;
+    for (int base = 0; base < nc; base += kResolveEpt * kSelThreads) {
+      int64_t at[kResolveEpt];
 #pragma unroll
-        for (int m = 0; m < 4; ++m)
-          u[m] = __builtin_amdgcn_raw_buffer_load_b32(rs, (base + m * kSelThreads + tid) * 4, 0, 0);
-#pragma unroll
-        for (int m = 0; m < 4; ++m)
-          if (base + m * kSelThreads + tid < n)
-            lds.cand_u[cand_off[sl] + base + m * kSelThreads + tid] = u[m];
+      for (int m = 0; m < kResolveEpt; ++m) {
+        const int i = base + m * kSelThreads + tid;
+        at[m] = 0;   // past the end: a valid address, not stored
+        if (i < nc) {
+          while (lds.cand_off[sl + 1] <= i) ++sl;
+          at[m] = sl * (int64_t)a.cand_cap + (i - lds.cand_off[sl]);
+        }
       }
+      uint32_t u[kResolveEpt];
+#pragma unroll
+      for (int m = 0; m < kResolveEpt; ++m) u[m] = cand0[at[m]];
+#pragma unroll
+      for (int m = 0; m < kResolveEpt; ++m)
+        if (base + m * kSelThreads + tid < nc) lds.cand_u[base + m * kSelThreads + tid] = u[m];
     }
   }
   // fn(u, slice, valid) over every candidate, slice by slice; every thread
   // makes the same calls.
   auto each = [&](auto fn) {
     for (int sl = 0; sl < ns; ++sl) {
-      const int n = cand_off[sl + 1] - cand_off[sl];
+      const int c0 = lds.cand_off[sl], n = lds.cand_off[sl + 1] - c0;
       if (in_lds) {
         for (int base = 0; base < n; base += kSelThreads) {
           const int i = base + tid;
-          fn(i < n ? lds.cand_u[cand_off[sl] + i] : 0u, sl, i < n);
+          fn(i < n ? lds.cand_u[c0 + i] : 0u, sl, i < n);
         }
       } else {
         const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
@@ -514,8 +549,7 @@ __global__ __launch_bounds__(kSelThreads) void select_resolve_kernel(const Selec
             u[m] = __builtin_amdgcn_raw_buffer_load_b32(rs, (base + m * kSelThreads + tid) * 4,
                                                         0, 0);
 #pragma unroll
-          for (int m = 0; m < kResolveEpt; ++m)
-            fn(u[m], sl, base + m * kSelThreads + tid < n);
+          for (int m = 0; m < kResolveEpt; ++m) fn(u[m], sl, base + m * kSelThreads + tid < n);
         }
       }
     }
@@ -541,134 +575,116 @@ __global__ __launch_bounds__(kSelThreads) void select_resolve_kernel(const Selec
     __syncthreads();
   }
   const uint32_t thr = prefix;
-  // per slice: candidates above the threshold (added to the slice's count of
-  // elements above the bucket) and ties
+  // per slice: candidates above the threshold (added to the slice's elements
+  // above the bucket) and ties
   each([&](uint32_t u, int sl, bool ok) {
     const uint32_t x = u & 0x7FFFFFFFu;
     const int n_gt = (int)__popcll(__ballot(ok && x > thr));
     const int n_eq = (int)__popcll(__ballot(ok && x == thr));
     if ((threadIdx.x & 63) == 0) {
-      if (n_gt) atomicAdd(&gt[sl], n_gt);
-      if (n_eq) atomicAdd(&eq[sl], n_eq);
+      if (n_gt) atomicAdd(&lds.gt[sl], n_gt);
+      if (n_eq) atomicAdd(&lds.eq[sl], n_eq);
     }
   });
   __syncthreads();
   if (tid == 0) {
     int pos = 0, ties = 0;
     for (int sl = 0; sl < ns; ++sl) {
-      meta[kSelMetaHead + 2 * nsl + sl] = pos;
-      meta[kSelMetaHead + 3 * nsl + sl] = ties;
-      pos += gt[sl] + max(0, min(eq[sl], remain - ties));
-      ties += eq[sl];
+      int *m = meta + sl * kSelMetaPerSlice;
+      m[kMetaFirst] = pos;
+      m[kMetaTies] = ties;
+      m[kMetaThr] = (int)thr;
+      m[kMetaRemain] = remain;
+      const int gt = lds.above[sl] + lds.gt[sl];
+      pos += gt + max(0, min(lds.eq[sl], remain - ties));
+      ties += lds.eq[sl];
     }
-    meta[1] = (int)thr;
-    meta[2] = remain;
-    meta[0] = 0;
   }
 }
 
-// Grid (n_slices, n_sel, batch [x layers]), 1024 threads.  Each wave stages
-// the positions it may keep (above or at the threshold, ties flagged in bit
-// 31) in LDS in position order; after the waves' counts are exchanged, it
-// decides its ties and writes its kept positions.  A slice where some wave
-// has more than kScanWaveCap such positions is marked (-1 in its first meta
-// word, which the resolve kernel has read) and left to select_rest_kernel.
+// Ordered-list entries per lane per batch of the write kernel.
+constexpr int kWriteEpt = 8;
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// Grid (n_slices, n_sel, batch [x layers]), 1024 threads.  Wave w compacts
+// the slice's ordered-list part w (ascending positions, 64 entries per
+// step), reading it twice: it counts its entries above the threshold and its ties, the waves'
+// counts are exchanged, and it writes its kept positions from the slice's
+// first kept-list position on.  An entry above the threshold is kept, and of
+// those equal to it the first `remain` of the sequence in position order.
 template <bool ML>
 __global__ __launch_bounds__(kSelThreads) void select_write_kernel(const SelectArgs a) {
   const Sel s = sel_of<ML>(a, blockIdx.y, blockIdx.z);
   const int slice = blockIdx.x;
   const int r0 = slice * kRound;
   if (s.L <= s.budget || s.k == 0 || r0 >= s.P) return;
-  const int *meta = sel_meta(a, s);
-  if (meta[0]) return;   // nothing left to select
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  __shared__ uint32_t stage[kSelThreads / 64][kScanWaveCap];
-  __shared__ int wave_cnt[3][kSelThreads / 64];
-  const uint32_t thr = (uint32_t)meta[1];
-  const int remain = meta[2];
-  const int pos_base = meta[kSelMetaHead + 2 * a.n_slices + slice];
-  const int eq_base = meta[kSelMetaHead + 3 * a.n_slices + slice];
-  {
-    uint32_t v[kEpt];
-    load_round(s.sc, s.P, r0, v);
-    int n_gt = 0, n_eq = 0, n_st = 0;
+  __shared__ int wave_cnt[2][kSelThreads / 64];
+  const int *meta = sel_meta(a, s) + slice * kSelMetaPerSlice;
+  const int n = meta[1 + wave];
+  const uint32_t thr = (uint32_t)meta[kMetaThr];
+  const int room = max(0, meta[kMetaRemain] - meta[kMetaTies]);   // ties still to keep
+  // the wave's part through a buffer resource of n entries: loads past the
+  // end read 0 (and are masked below)
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)(a.sel_ord + (s.id * a.n_slices + slice) * (int64_t)a.cand_cap +
+               wave * (64 * kEpt)),
+      (short)0, n * 8, 0x00020000);
+  auto above = [&](const uint64_t x, bool valid) {
+    return valid && ((((uint32_t)x >> 31) == 0u) || (uint32_t)(x >> 32) > thr);
+  };
+  auto equal = [&](const uint64_t x, bool valid) {
+    return valid && ((uint32_t)x >> 31) != 0u && (uint32_t)(x >> 32) == thr;
+  };
+  // kWriteEpt entries per lane at a time, every load of a batch at once
+  auto load = [&](int b, uint64_t (&e)[kWriteEpt]) {
 #pragma unroll
-    for (int e = 0; e < kEpt; ++e) {
-      const int j = elem_pos<kEpt>(r0, e);
-      const uint32_t u = v[e] & 0x7FFFFFFFu;
-      const bool ok = j < s.P;
-      const bool gt = ok && u > thr, eq = ok && u == thr;
-      n_gt += (int)__popcll(__ballot(gt));
-      n_eq += (int)__popcll(__ballot(eq));
-      const unsigned long long m = __ballot(gt || eq);
-      const int at = n_st + lanes_below(m);
-      if ((gt || eq) && at < kScanWaveCap) stage[wave][at] = (uint32_t)j | (eq ? 0x80000000u : 0u);
-      n_st += (int)__popcll(m);
+    for (int m = 0; m < kWriteEpt; ++m) {
+      const u32x2 r = __builtin_amdgcn_raw_buffer_load_b64(rs, (b + 64 * m + lane) * 8, 0, 0);
+      e[m] = ((uint64_t)r.y << 32) | r.x;
     }
-    if (lane == 0) {
-      wave_cnt[0][wave] = n_gt;
-      wave_cnt[1][wave] = n_eq;
-      wave_cnt[2][wave] = n_st;
+  };
+  int c_gt = 0, c_eq = 0;
+  for (int b = 0; b < n; b += 64 * kWriteEpt) {
+    uint64_t e[kWriteEpt];
+    load(b, e);
+#pragma unroll
+    for (int m = 0; m < kWriteEpt; ++m) {
+      const bool valid = b + 64 * m + lane < n;
+      c_gt += (int)__popcll(__ballot(above(e[m], valid)));
+      c_eq += (int)__popcll(__ballot(equal(e[m], valid)));
     }
+  }
+  if (lane == 0) {
+    wave_cnt[0][wave] = c_gt;
+    wave_cnt[1][wave] = c_eq;
   }
   __syncthreads();
-  bool full = false;
-  int eq_before = 0, sel_before = 0, eq_total = 0;
+  int gt_before = 0, eq_before = 0;
 #pragma unroll
   for (int x = 0; x < kSelThreads / 64; ++x) {
-    const int c_gt = wave_cnt[0][x], c_eq = wave_cnt[1][x];
-    const int take = max(0, min(c_eq, remain - (eq_base + eq_total)));   // wave x's kept ties
     if (x < wave) {
-      eq_before += c_eq;
-      sel_before += c_gt + take;
+      gt_before += wave_cnt[0][x];
+      eq_before += wave_cnt[1][x];
     }
-    eq_total += c_eq;
-    full |= wave_cnt[2][x] > kScanWaveCap;
   }
-  if (full) {   // left to select_rest_kernel
-    if (tid == 0) a.sel_meta[(s.id * (kSelMetaHead + 4 * a.n_slices)) + kSelMetaHead + slice] = -1;
-    return;
-  }
-  int pos = pos_base + sel_before;
-  int eq_rank = eq_base + eq_before;
-  const int n_st = wave_cnt[2][wave];
-  for (int i0 = 0; i0 < n_st; i0 += 64) {
-    const bool valid = i0 + lane < n_st;
-    const uint32_t x = valid ? stage[wave][i0 + lane] : 0u;
-    const bool eq = valid && (x >> 31);
-    const unsigned long long m_eq = __ballot(eq);
-    const bool keep = valid && (!eq || eq_rank + lanes_below(m_eq) < remain);
-    const unsigned long long m_keep = __ballot(keep);
-    const int my_pos = pos + lanes_below(m_keep);
-    if (keep && my_pos < s.k) sel_put(a, s, my_pos, (int)(x & 0x7FFFFFFFu));
-    pos += (int)__popcll(m_keep);
-    eq_rank += (int)__popcll(m_eq);
-  }
-}
-
-// Grid (n_slices, n_sel, batch [x layers]), 1024 threads: the slices that
-// select_write_kernel marked, by compact_round on the scores, half a slice at
-// a time.
-template <bool ML>
-__global__ __launch_bounds__(kSelThreads) void select_rest_kernel(const SelectArgs a) {
-  const Sel s = sel_of<ML>(a, blockIdx.y, blockIdx.z);
-  const int slice = blockIdx.x;
-  const int r0 = slice * kRound;
-  if (s.L <= s.budget || s.k == 0 || r0 >= s.P) return;
-  const int *meta = sel_meta(a, s);
-  if (meta[0] || meta[kSelMetaHead + slice] != -1) return;
-  __shared__ int wave_cnt[2][kSelThreads / 64];
-  const uint32_t thr = (uint32_t)meta[1];
-  const int remain = meta[2];
-  int pb = meta[kSelMetaHead + 2 * a.n_slices + slice];
-  int eb = meta[kSelMetaHead + 3 * a.n_slices + slice];
-  for (int h = 0; h < kRound / kRoundWhole; ++h) {
-    uint32_t v[kEptWhole];
-    load_round(s.sc, s.P, r0 + h * kRoundWhole, v);
-    int kept, ties;
-    compact_round(a, s, v, r0 + h * kRoundWhole, thr, remain, pb, eb, wave_cnt, &kept, &ties);
-    pb += kept;
-    eb += ties;
+  int my = meta[kMetaFirst] + gt_before + min(eq_before, room);
+  int eq_rank = eq_before;
+  for (int b = 0; b < n; b += 64 * kWriteEpt) {
+    uint64_t e[kWriteEpt];
+    load(b, e);
+#pragma unroll
+    for (int m = 0; m < kWriteEpt; ++m) {
+      const bool valid = b + 64 * m + lane < n;
+      const bool eq = equal(e[m], valid);
+      const unsigned long long m_eq = __ballot(eq);
+      const bool keep = above(e[m], valid) || (eq && eq_rank + lanes_below(m_eq) < room);
+      const unsigned long long m_keep = __ballot(keep);
+      const int slot = my + lanes_below(m_keep);
+      if (keep && slot < s.k) sel_put(a, s, slot, (int)((uint32_t)e[m] & 0x7FFFFFFFu));
+      my += (int)__popcll(m_keep);
+      eq_rank += (int)__popcll(m_eq);
+    }
   }
 }
 
@@ -751,12 +767,10 @@ hipError_t launch_select(const SelectArgs &a, int n_layers, hipStream_t stream) 
       hipLaunchKernelGGL(select_scan_kernel<true>, slices, dim3(kSelThreads), 0, stream, a);
       hipLaunchKernelGGL(select_resolve_kernel<true>, sels, dim3(kSelThreads), 0, stream, a);
       hipLaunchKernelGGL(select_write_kernel<true>, slices, dim3(kSelThreads), 0, stream, a);
-      hipLaunchKernelGGL(select_rest_kernel<true>, slices, dim3(kSelThreads), 0, stream, a);
     } else {
       hipLaunchKernelGGL(select_scan_kernel<false>, slices, dim3(kSelThreads), 0, stream, a);
       hipLaunchKernelGGL(select_resolve_kernel<false>, sels, dim3(kSelThreads), 0, stream, a);
       hipLaunchKernelGGL(select_write_kernel<false>, slices, dim3(kSelThreads), 0, stream, a);
-      hipLaunchKernelGGL(select_rest_kernel<false>, slices, dim3(kSelThreads), 0, stream, a);
     }
     return hipGetLastError();
   }

@@ -113,8 +113,8 @@ def test_split_select_ties_straddling_a_slice_boundary(gpu):
 def test_split_select_full_bucket(gpu):
     """Constant keys: every prefix score is equal, each slice's bucket holds
     all of its 32768 positions (more candidates than the resolve kernel keeps
-    in LDS, and more kept positions than the write kernel stages), and the
-    lowest positions are kept."""
+    in LDS, and every position in the slice's ordered list), and the lowest
+    positions are kept."""
     x = _layer([70000, 40000], seed=33, n_needle=0, n_sink=0)
     x.k[:] = 0.0
     W = x.workload.window
