@@ -46,25 +46,25 @@ def _traffic(**kernels):
 
 
 MEASURED_TRAFFIC = {
-    ("llama32", 32, "7841ac17a7c91f99"): _traffic(
-        fused_fill_kernel=(11.08, 8385.03),
-        fused_kernel=(2286926.98, 37992.78),
+    ("llama32", 32, "7f9fea8574bc8c35"): _traffic(
+        fused_fill_kernel=(11.07, 8385.03),
+        fused_kernel=(2286840.01, 37992.78),
         fused_catchup_kernel=(11.5, 0.0)),
-    ("paper", 32, "7841ac17a7c91f99"): _traffic(
+    ("paper", 32, "7f9fea8574bc8c35"): _traffic(
         fused_fill_kernel=(11.03, 4161.03),
-        fused_kernel=(959948.02, 15118.56),
+        fused_kernel=(959899.58, 15118.56),
         fused_catchup_kernel=(10.5, 0.0)),
-    ("llama1", 1, "7841ac17a7c91f99"): _traffic(
-        fused_fill_kernel=(11.02, 196.06),
-        fused_kernel=(63429.77, 1184.08),
+    ("llama1", 1, "7f9fea8574bc8c35"): _traffic(
+        fused_fill_kernel=(11.01, 196.06),
+        fused_kernel=(63444.26, 1184.08),
         fused_catchup_kernel=(18.0, 0.0)),
-    ("qwen128k", 28, "7841ac17a7c91f99"): _traffic(
-        stats_kernel=(1852807.34, 8064.0),
-        colsum_kernel=(1947790.38, 57591.34)),
-    ("ragged8", 32, "7841ac17a7c91f99"): _traffic(
-        stats_kernel=(2673227.1, 22016.0),
-        colsum_kernel=(2843546.18, 82244.65)),
-    ("tiny", 1, "7841ac17a7c91f99"): _traffic(
+    ("qwen128k", 28, "7f9fea8574bc8c35"): _traffic(
+        stats_kernel=(1852714.58, 8064.0),
+        colsum_kernel=(1947639.95, 57591.34)),
+    ("ragged8", 32, "7f9fea8574bc8c35"): _traffic(
+        stats_kernel=(2673161.67, 22016.0),
+        colsum_kernel=(2843577.0, 82242.56)),
+    ("tiny", 1, "7f9fea8574bc8c35"): _traffic(
         stats_kernel=(297.42, 16.5),
         colsum_kernel=(334.25, 8.42)),
 }
@@ -79,18 +79,18 @@ def _mfma(**kernels):
 
 
 MEASURED_MFMA = {
-    ("llama32", 32, "7841ac17a7c91f99"): _mfma(
-        fused_kernel=(581683200.0, 290841600.0, 14426235.76)),
-    ("paper", 32, "7841ac17a7c91f99"): _mfma(
-        fused_kernel=(70909952.0, 35454976.0, 6495632.76)),
-    ("llama1", 1, "7841ac17a7c91f99"): _mfma(
-        fused_kernel=(17727488.0, 8863744.0, 809361.74)),
-    ("qwen128k", 28, "7841ac17a7c91f99"): _mfma(
-        stats_kernel=(939524096.0, 469762048.0, 10580562.24),
-        colsum_kernel=(987693056.0, 493846528.0, 14332006.91)),
-    ("ragged8", 32, "7841ac17a7c91f99"): _mfma(
-        stats_kernel=(738197504.0, 369098752.0, 19578183.35),
-        colsum_kernel=(731906048.0, 365953024.0, 22845427.38)),
+    ("llama32", 32, "7f9fea8574bc8c35"): _mfma(
+        fused_kernel=(581683200.0, 290841600.0, 14110831.91)),
+    ("paper", 32, "7f9fea8574bc8c35"): _mfma(
+        fused_kernel=(70909952.0, 35454976.0, 6371246.21)),
+    ("llama1", 1, "7f9fea8574bc8c35"): _mfma(
+        fused_kernel=(17727488.0, 8863744.0, 805205.82)),
+    ("qwen128k", 28, "7f9fea8574bc8c35"): _mfma(
+        stats_kernel=(939524096.0, 469762048.0, 10013512.88),
+        colsum_kernel=(987693056.0, 493846528.0, 14205209.47)),
+    ("ragged8", 32, "7f9fea8574bc8c35"): _mfma(
+        stats_kernel=(738197504.0, 369098752.0, 18793655.91),
+        colsum_kernel=(731906048.0, 365953024.0, 21214593.44)),
 }
 
 
