@@ -2,8 +2,8 @@
 sets of sequences longer than one slice): its kept lists are exactly the
 oracle's selection on the same fp32 scores (section 3.3: the best prefix
 tokens by score, ties to the lowest position, plus the window), across
-ragged lengths, budgets, ties that straddle a slice boundary and buckets
-holding every position."""
+ragged lengths, budgets, ties that straddle a slice boundary, buckets
+holding every position, multi-layer calls and per-group budgets."""
 import sys
 
 import numpy as np
@@ -126,3 +126,63 @@ def test_split_select_full_bucket(gpu):
         idx, scores = idx.cpu().numpy(), scores.cpu().numpy()
         _check_exact(scores, lambda b, g: idx[b, g], x.cu_seqlens, W, [budget] * 8)
         assert idx[0, 0, :budget - W].tolist() == list(range(budget - W))
+
+
+def test_split_select_multi_layer_ragged_batch(gpu):
+    """A multi-layer call over a ragged batch whose sequences span 3, 1 and 2
+    slices, with a different budget per layer: every layer's kept lists are
+    exactly the oracle's selection on its fp32 scores and equal the
+    per-layer call's bit for bit."""
+    w = wl.get("llama1", batch=3, n_layers=3, n_needle=4)
+    lengths = np.asarray([70000, 5000, 40000])
+    xs = [wl.make_layer(w, l, seed=34, lengths=lengths) for l in range(w.n_layers)]
+    W = w.window
+    budgets = [1024, W + 3, 36000]
+    dts = [H.device_tensors(x, gpu) for x in xs]
+    q, k, v = [d[0] for d in dts], [d[1] for d in dts], [d[2] for d in dts]
+    cu = dts[0][3]
+    masks = np.stack([x.srh_mask for x in xs])
+    p = C.Problem(q[0], k[0], v[0], cu, cu_seqlens_host=xs[0].cu_seqlens,
+                  scoring=C.SCORE_TWO_PASS)
+    _say(f"case multi-layer split select, lengths {lengths.tolist()}, budgets {budgets}")
+    idxs, kos, vos, scores = C.compress_layers(p, q, k, v, masks, budgets, want_scores=True)
+    torch.cuda.synchronize()
+    for l in range(w.n_layers):
+        il, sl = idxs[l].cpu().numpy(), scores[l].cpu().numpy()
+        _check_exact(sl, lambda b, g: il[b, g], xs[0].cu_seqlens, W, [budgets[l]] * 8)
+        pl = C.Problem(q[l], k[l], v[l], cu, cu_seqlens_host=xs[0].cu_seqlens,
+                       scoring=C.SCORE_TWO_PASS)
+        one = C.compress_layer(pl, q[l], k[l], v[l], masks[l], budgets[l], want_scores=True)
+        torch.cuda.synchronize()
+        for got, want in zip((idxs[l], kos[l], vos[l], scores[l]), one):
+            assert torch.equal(got, want), f"layer {l} differs from the per-layer call"
+
+
+def test_split_select_heads_ragged_batch(gpu):
+    """Per-group budgets (compress_layer_heads) over a ragged batch longer
+    than one slice: budgets from the window alone to more than a slice and
+    more than the shorter sequence, kept lists exactly the oracle's selection
+    on the fp32 scores, kept rows equal to the keys and values at those
+    positions."""
+    x = _layer([70000, 40000], seed=35, n_needle=4)
+    W = x.workload.window
+    q, k, v, cu = H.device_tensors(x, gpu)
+    p = C.Problem(q, k, v, cu, cu_seqlens_host=x.cu_seqlens, scoring=C.SCORE_TWO_PASS)
+    budgets = [W, 3000, 257, 36000, 64, W + 1, 45000, 12000]
+    _say(f"case heads split select, budgets {budgets}")
+    idx, k_out, v_out, scores = C.compress_layer_heads(p, q, k, v, x.srh_mask, budgets,
+                                                       want_scores=True)
+    torch.cuda.synchronize()
+    idx, scores = idx.cpu().numpy(), scores.cpu().numpy()
+    off = np.concatenate([[0], np.cumsum(budgets)])
+    _check_exact(scores, lambda b, g: idx[b, off[g]:off[g + 1]], x.cu_seqlens, W, budgets)
+    kb, vb = x.bits("k"), x.bits("v")
+    ko, vo = H.raw_bits(k_out), H.raw_bits(v_out)
+    for b in range(2):
+        s0 = int(x.cu_seqlens[b])
+        for g in range(8):
+            rows = idx[b, off[g]:off[g + 1]]
+            kept = rows >= 0
+            assert np.array_equal(ko[b, off[g]:off[g + 1]][kept], kb[s0 + rows[kept], g])
+            assert np.array_equal(vo[b, off[g]:off[g + 1]][kept], vb[s0 + rows[kept], g])
+            assert not ko[b, off[g]:off[g + 1]][~kept].any()
