@@ -9,8 +9,8 @@
 //                       softmax in LDS, P.V on fp32 MFMA; partial (max, sum, O)
 //   dec_combine_kernel  merges the chunks of every row into A (fp32)
 //   dec_proj_kernel     y = W_O x for x = A_full and A_full - A_comp on fp32
-//                       MFMA (16 rows of W_O per workgroup, one wave per 16
-//                       vectors); per-workgroup sums of y^2
+//                       MFMA (16 rows of W_O per workgroup, 16 waves on
+//                       sixteenths of its columns); per-workgroup sums of y^2
 //   dec_error_kernel    the per-step norms, their ratios and the layer sum
 //
 // The kernels take a block of at most kMaxVectors (sequence, step) vectors
@@ -32,6 +32,7 @@ namespace ckv {
 constexpr int kDecChunk = 512;   // keys per attention workgroup (eight softmax steps)
 constexpr int kDecSub = 64;      // keys per softmax step inside it (one tile per wave)
 constexpr int kProjRows = 16;    // W_O rows per projection workgroup
+constexpr int kProjWaves = 16;   // waves per projection workgroup, each on HD / 16 columns
 constexpr int kMaxDecRows = 64;  // decoding steps x query heads per group, per block
 constexpr int kMaxVectors = 32;  // sequences x decoding steps, per block
 
@@ -303,15 +304,16 @@ struct ProjArgs {
   int d_model, HD, NV;
 };
 
-// Grid (ceil(d_model / 16)), 256 threads.  The vectors are the rows of
+// Grid (ceil(d_model / 16)), 1024 threads.  The vectors are the rows of
 // X = [A_full (NV rows); A_full - A_comp (NV rows); zeros], in XT tiles of 16;
-// wave w computes Y = X W_O^T over the w-th quarter of the columns for every
-// X tile and the workgroup's 16 rows of W_O with v_mfma_f32_16x16x4_f32
+// wave w computes Y = X W_O^T over the w-th sixteenth of the columns for
+// every X tile and the workgroup's 16 rows of W_O with v_mfma_f32_16x16x4_f32
 // (MFMA operands as in the scoring kernels: lane (quad, c) holds floats
-// 16 s + 4 quad .. +3 of row c of each tile).  The quarters are added in
-// order, then y^2 is summed over the 16 rows of W_O (lanes c, fixed butterfly).
+// 16 s + 4 quad .. +3 of row c of each tile).  The sixteen partial products
+// are added in wave order, then y^2 is summed over the 16 rows of W_O (lanes
+// c, fixed butterfly).
 template <typename T, int XT>
-__global__ __launch_bounds__(256) void dec_proj_kernel(const ProjArgs p) {
+__global__ __launch_bounds__(64 * kProjWaves) void dec_proj_kernel(const ProjArgs p) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int c = lane & 15, quad = lane >> 4;
   const int o = (int)blockIdx.x * kProjRows + c;            // this lane's row of W_O
@@ -330,38 +332,68 @@ __global__ __launch_bounds__(256) void dec_proj_kernel(const ProjArgs p) {
   f32x4 acc[XT];
 #pragma unroll
   for (int x = 0; x < XT; ++x) acc[x] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int q4 = p.HD / 4;                                    // columns per wave
-  for (int k0 = wave * q4 + 4 * quad; k0 < (wave + 1) * q4; k0 += 16) {
+  const int qw = p.HD / kProjWaves;                           // columns per wave
+  const int k_end = (wave + 1) * qw;
+  // X tile x's four floats at column k (row as set above), the difference
+  // rows formed here
+  auto x_at = [&](int x, int k) {
+    float4 xv = *reinterpret_cast<const float4 *>(xf[x] + k);
+    if (kind[x] == 1) {
+      const float4 y = *reinterpret_cast<const float4 *>(xc[x] + k);
+      xv = make_float4(xv.x - y.x, xv.y - y.y, xv.z - y.z, xv.w - y.w);
+    } else if (kind[x] == 2) {
+      xv = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    return xv;
+  };
+  auto w_at = [&](int k) {   // four elements of this lane's row of W_O at column k
     float4 wv;
     if constexpr (sizeof(T) == 2) {
-      const uint2 raw = *reinterpret_cast<const uint2 *>(wr + k0);
+      const uint2 raw = *reinterpret_cast<const uint2 *>(wr + k);
       wv = make_float4(__uint_as_float(raw.x << 16), __uint_as_float(raw.x & 0xFFFF0000u),
                        __uint_as_float(raw.y << 16), __uint_as_float(raw.y & 0xFFFF0000u));
     } else {
-      wv = *reinterpret_cast<const float4 *>(wr + k0);
+      wv = *reinterpret_cast<const float4 *>(wr + k);
     }
-    if (!o_ok) wv = make_float4(0.f, 0.f, 0.f, 0.f);
+    return o_ok ? wv : make_float4(0.f, 0.f, 0.f, 0.f);
+  };
+  // 64 columns per trip: lane (quad, c) takes the 16 consecutive columns
+  // k0 + 16 quad .. + 15 of its row of W_O (a whole 32-byte or 64-byte run)
+  // and of its X rows, four MFMA steps of 4 columns each (the products are
+  // summed over the columns, so which 4 columns a step takes is free as long
+  // as W_O and X agree)
+  int k0 = wave * qw;
+  for (; k0 + 64 <= k_end; k0 += 64) {
+    const int kq = k0 + 16 * quad;
+    float4 wv[4];
+#pragma unroll
+    for (int st = 0; st < 4; ++st) wv[st] = w_at(kq + 4 * st);
 #pragma unroll
     for (int x = 0; x < XT; ++x) {
-      float4 xv = *reinterpret_cast<const float4 *>(xf[x] + k0);
-      if (kind[x] == 1) {
-        const float4 y = *reinterpret_cast<const float4 *>(xc[x] + k0);
-        xv = make_float4(xv.x - y.x, xv.y - y.y, xv.z - y.z, xv.w - y.w);
-      } else if (kind[x] == 2) {
-        xv = make_float4(0.f, 0.f, 0.f, 0.f);
-      }
-      acc[x] = mfma_slice<float>(__builtin_bit_cast(uint4, xv), __builtin_bit_cast(uint4, wv),
-                                 acc[x]);
+#pragma unroll
+      for (int st = 0; st < 4; ++st)
+        acc[x] = mfma_slice<float>(__builtin_bit_cast(uint4, x_at(x, kq + 4 * st)),
+                                   __builtin_bit_cast(uint4, wv[st]), acc[x]);
     }
   }
-  __shared__ f32x4 part[4][XT][64];
+  // the rest in steps of 16 columns (lane quad on columns k0 + 4 quad .. + 3)
+  for (; k0 < k_end; k0 += 16) {
+    const float4 wv = w_at(k0 + 4 * quad);
+#pragma unroll
+    for (int x = 0; x < XT; ++x)
+      acc[x] = mfma_slice<float>(__builtin_bit_cast(uint4, x_at(x, k0 + 4 * quad)),
+                                 __builtin_bit_cast(uint4, wv), acc[x]);
+  }
+  __shared__ f32x4 part[kProjWaves][XT][64];
 #pragma unroll
   for (int x = 0; x < XT; ++x) part[wave][x][lane] = acc[x];
   __syncthreads();
-  // wave x < XT finishes X tile x: quarters in order, then the squares
+  // wave x < XT finishes X tile x: the partial products in wave order, then
+  // the squares
   if (wave < XT) {
-    const f32x4 y = ((part[0][wave][lane] + part[1][wave][lane]) + part[2][wave][lane]) +
-                    part[3][wave][lane];
+    f32x4 y = part[0][wave][lane];
+#pragma unroll
+    for (int w = 1; w < kProjWaves; ++w) y = y + part[w][wave][lane];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       float sq = y[r] * y[r];
@@ -418,10 +450,10 @@ static void launch_dec_t(const DecArgs &a, const ProjArgs &pa, int rt, int n_wg,
   }
   hipLaunchKernelGGL((dec_combine_kernel<D>), dim3(a.R, a.Hkv, a.batch * 2), dim3(D), 0, s, a);
   switch ((2 * pa.NV + 15) / 16) {
-    case 1: hipLaunchKernelGGL((dec_proj_kernel<T, 1>), dim3(n_wg), dim3(256), 0, s, pa); break;
-    case 2: hipLaunchKernelGGL((dec_proj_kernel<T, 2>), dim3(n_wg), dim3(256), 0, s, pa); break;
-    case 3: hipLaunchKernelGGL((dec_proj_kernel<T, 3>), dim3(n_wg), dim3(256), 0, s, pa); break;
-    default: hipLaunchKernelGGL((dec_proj_kernel<T, 4>), dim3(n_wg), dim3(256), 0, s, pa); break;
+    case 1: hipLaunchKernelGGL((dec_proj_kernel<T, 1>), dim3(n_wg), dim3(64 * kProjWaves), 0, s, pa); break;
+    case 2: hipLaunchKernelGGL((dec_proj_kernel<T, 2>), dim3(n_wg), dim3(64 * kProjWaves), 0, s, pa); break;
+    case 3: hipLaunchKernelGGL((dec_proj_kernel<T, 3>), dim3(n_wg), dim3(64 * kProjWaves), 0, s, pa); break;
+    default: hipLaunchKernelGGL((dec_proj_kernel<T, 4>), dim3(n_wg), dim3(64 * kProjWaves), 0, s, pa); break;
   }
   hipLaunchKernelGGL(dec_error_kernel, dim3(1), dim3(64 * kMaxVectors / 2), 0, s, pa.part_ss, n_wg,
                      pa.NV, eps, first ? 1 : 0, err);
