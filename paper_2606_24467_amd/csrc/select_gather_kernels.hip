@@ -375,14 +375,18 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a)
 //           candidates) into the slice's candidate list, and every element
 //           at or above the bucket, as a (position, score) pair, into the
 //           wave's part of the slice's ordered list (ascending positions);
+//           slice 0 also passes the first digit on;
 //  resolve: per selection, digits 2 and 3 over all the slices' candidates,
 //           then each slice's first kept-list position and ties before it;
 //  write:   per slice, the ordered compaction of its ordered list.
 static_assert(kSelMetaPerSlice == 1 + kSelThreads / 64 + 4, "meta words of a slice");
 constexpr int kMetaFirst = 1 + kSelThreads / 64;   // first kept-list position
 constexpr int kMetaTies = kMetaFirst + 1;           // ties in the slices before
-constexpr int kMetaThr = kMetaFirst + 2;            // threshold (score bits)
-constexpr int kMetaRemain = kMetaFirst + 3;         // ties kept in all
+// The last two words: the threshold (score bits) and the ties kept in all,
+// from the resolve kernel; before it, slice 0's hold the first-digit bucket
+// and the rank inside it, from the scan.
+constexpr int kMetaThr = kMetaFirst + 2;
+constexpr int kMetaRemain = kMetaFirst + 3;
 
 __device__ __forceinline__ int *sel_meta(const SelectArgs &a, const Sel &s) {
   return a.sel_meta + s.id * (kSelMetaPerSlice * a.n_slices);
@@ -411,6 +415,11 @@ __global__ __launch_bounds__(kSelThreads) void select_scan_kernel(const SelectAr
   __syncthreads();
   find_bucket(hist, kHistBins, s.k, scan_tmp, &bucket_s, &remain_s);
   const int bucket = bucket_s;
+  if (slice == 0 && tid == 0) {   // the same in every slice: for the resolve kernel
+    int *meta0 = sel_meta(a, s);
+    meta0[kMetaThr] = bucket;
+    meta0[kMetaRemain] = remain_s;
+  }
   // The bucket's elements go to the candidate list in no particular order
   // (the resolve kernel only counts them); the elements at or above it go to
   // the wave's part of the ordered list (its 64 * kEpt positions, in (e,
@@ -479,12 +488,10 @@ __global__ __launch_bounds__(kSelThreads) void select_resolve_kernel(const Selec
   __shared__ ResolveLds lds;
   const int ns = (s.P + kRound - 1) / kRound;
   const int nsl = a.n_slices;
-  if (tid == 0) {
-    lds.bucket = 0;
-    lds.remain = 0;
+  if (tid == 0) {   // digit 1, found by the scan
+    lds.bucket = meta[kMetaThr];
+    lds.remain = meta[kMetaRemain];
   }
-  const int *hg = a.hist + s.layer * a.hist_layer + ((int64_t)s.b * a.Hkv + s.g) * kHistBins;
-  for (int i = tid; i < kHistBins; i += kSelThreads) lds.hist[i] = hg[i];
   if (tid < ns) {
     const int *m = meta + tid * kSelMetaPerSlice;
     int n_ord = 0;
@@ -499,7 +506,7 @@ __global__ __launch_bounds__(kSelThreads) void select_resolve_kernel(const Selec
     lds.cand_off[0] = 0;
     for (int sl = 0; sl < ns; ++sl) lds.cand_off[sl + 1] += lds.cand_off[sl];
   }
-  find_bucket(lds.hist, kHistBins, s.k, lds.scan_tmp, &lds.bucket, &lds.remain);
+  __syncthreads();
   uint32_t prefix = (uint32_t)lds.bucket << 20;
   int remain = lds.remain;
   const int nc = lds.cand_off[ns];
